@@ -1,0 +1,280 @@
+"""Seeded synthetic workloads standing in for the paper's benchmark blocks.
+
+The paper measures Inception-V3, RandWire, NASNet-A and SqueezeNet (Table 2,
+Sec. 5).  No dataset or trained weight is needed for latency or parity, so
+each network is replaced by a block of the same shapes built here:
+
+  tiny       2-branch block 1x16x8x8 (used for brute-force schedule checks)
+  inception  Inception-V3 mixed block, 192x35x35 -> 256x35x35
+  randwire   32-node Watts-Strogatz WS(4, 0.75) DAG of sepconv nodes, 78x28x28
+  nasnet     NASNet-A style normal cell, two 168x42x42 inputs -> 840x42x42
+  squeeze    8 SqueezeNet fire modules, 96x55x55 input, two max-pools
+
+A workload is a plain description (``spec``) plus a dict of float32 numpy
+arrays (``tensors``).  The description lists the operators in insertion
+order, which is a topological order; both the oracle and the library read it.
+Inputs are U(-1, 1); weights are N(0, 2 / fan_in) with
+fan_in = (Cin / groups) * kh * kw; biases are zero.
+
+Operator kinds (one schedule unit each, except the two views):
+  conv      dense 2-D cross-correlation + bias, optional ReLU before/after
+  sepconv   sum of inputs -> ReLU -> depthwise kxk (pad k/2) -> pointwise 1x1
+  maxpool / avgpool   kxk window, stride, pad (avg divides by k*k)
+  add       elementwise sum of inputs
+  mean      elementwise mean of inputs
+  concat    channel concatenation (a view: producers write into slices)
+  identity  a view of its input
+"""
+from __future__ import annotations
+
+import copy
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+from . import rng
+
+CONFIG_NAMES = ["tiny", "inception", "randwire", "nasnet", "squeeze"]
+
+
+def _conv(name, inp, cout, k, pad, stride=1, post_relu=1, pre_relu=0, block=-1):
+    kh, kw = (k, k) if isinstance(k, int) else k
+    ph, pw = (pad, pad) if isinstance(pad, int) else pad
+    return {"name": name, "kind": "conv", "in": [inp], "cout": cout,
+            "kh": kh, "kw": kw, "sh": stride, "sw": stride, "ph": ph, "pw": pw,
+            "pre_relu": pre_relu, "post_relu": post_relu, "block": block}
+
+
+def _sep(name, inputs, cout, k, block=-1):
+    return {"name": name, "kind": "sepconv", "in": list(inputs), "cout": cout,
+            "kh": k, "kw": k, "sh": 1, "sw": 1, "ph": k // 2, "pw": k // 2,
+            "pre_relu": 1, "post_relu": 0, "block": block}
+
+
+def _pool(name, inp, kind, k, stride, pad, block=-1):
+    return {"name": name, "kind": kind, "in": [inp], "kh": k, "kw": k,
+            "sh": stride, "sw": stride, "ph": pad, "pw": pad, "block": block}
+
+
+def _view(name, kind, inputs):
+    return {"name": name, "kind": kind, "in": list(inputs)}
+
+
+# ---------------------------------------------------------------- graphs
+
+def spec_tiny(batch: int = 1, seed: int = 0) -> dict:
+    ops = [
+        _conv("A", "x", 16, 1, 0),
+        _conv("B1", "x", 8, 1, 0),
+        _conv("B2", "B1", 16, 3, 1),
+        _view("out", "concat", ["A", "B2"]),
+    ]
+    return {"name": "tiny", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 16, "h": 8, "w": 8}],
+            "ops": ops, "outputs": ["out"]}
+
+
+def spec_inception(batch: int = 1, seed: int = 0) -> dict:
+    ops = [
+        _conv("b1", "x", 64, 1, 0),
+        _conv("b2a", "x", 48, 1, 0),
+        _conv("b2b", "b2a", 64, 5, 2),
+        _conv("b3a", "x", 64, 1, 0),
+        _conv("b3b", "b3a", 96, 3, 1),
+        _conv("b3c", "b3b", 96, 3, 1),
+        _pool("pool", "x", "avgpool", 3, 1, 1),
+        _conv("b4", "pool", 32, 1, 0),
+        _view("out", "concat", ["b1", "b2b", "b3c", "b4"]),
+    ]
+    return {"name": "inception", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 192, "h": 35, "w": 35}],
+            "ops": ops, "outputs": ["out"]}
+
+
+def ws_edges(n: int, k: int, p: float, stream: rng.Stream) -> List[Tuple[int, int]]:
+    """Watts-Strogatz small-world graph, edges oriented low -> high index.
+
+    Ring lattice: node i is joined to i+1 .. i+k/2 (mod n).  Then every
+    lattice edge (i, i+j), j = 1 .. k/2, is rewired with probability p to
+    (i, w), w drawn uniformly among nodes that are neither i nor already
+    adjacent to i.
+    """
+    adj = [set() for _ in range(n)]
+    lattice = []
+    for j in range(1, k // 2 + 1):
+        for i in range(n):
+            a, b = i, (i + j) % n
+            adj[a].add(b)
+            adj[b].add(a)
+            lattice.append((a, b))
+    for a, b in lattice:
+        if stream.u01() < p:
+            cand = [w for w in range(n) if w != a and w not in adj[a]]
+            if not cand:
+                continue
+            w = cand[stream.randint(len(cand))]
+            adj[a].discard(b)
+            adj[b].discard(a)
+            adj[a].add(w)
+            adj[w].add(a)
+    edges = sorted({(min(a, b), max(a, b)) for a in range(n) for b in adj[a]})
+    return edges
+
+
+def spec_randwire(batch: int = 1, seed: int = 0, nodes: int = 32, channels: int = 78,
+                  hw: int = 28) -> dict:
+    stream = rng.Stream(rng.key_of("randwire-graph", seed))
+    edges = ws_edges(nodes, 4, 0.75, stream)
+    preds = [[] for _ in range(nodes)]
+    outdeg = [0] * nodes
+    for a, b in edges:
+        preds[b].append(a)
+        outdeg[a] += 1
+    ops = []
+    for v in range(nodes):
+        ins = [f"n{u}" for u in sorted(preds[v])] or ["x"]
+        ops.append(_sep(f"n{v}", ins, channels, 3))
+    sinks = [f"n{v}" for v in range(nodes) if outdeg[v] == 0]
+    ops.append({"name": "out", "kind": "mean", "in": sinks, "block": -1})
+    return {"name": "randwire", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": channels, "h": hw, "w": hw}],
+            "ops": ops, "outputs": ["out"], "ws_edges": edges}
+
+
+NASNET_OPS = ["sep3", "sep5", "avgpool", "maxpool", "identity"]
+
+
+def spec_nasnet(batch: int = 1, seed: int = 0, channels: int = 168, hw: int = 42) -> dict:
+    stream = rng.Stream(rng.key_of("nasnet-cell", seed))
+    ops = []
+    outs = []
+    choices = []
+    for b in range(5):
+        slot_out = []
+        for s in range(2):
+            inp = ["h", "h_prev"][stream.randint(2)]
+            kind = NASNET_OPS[stream.randint(5)]
+            choices.append((b, s, inp, kind))
+            nm = f"c{b}s{s}"
+            if kind in ("sep3", "sep5"):
+                k = 3 if kind == "sep3" else 5
+                ops.append(_sep(nm + "u1", [inp], channels, k))
+                ops.append(_sep(nm + "u2", [nm + "u1"], channels, k))
+                slot_out.append(nm + "u2")
+            elif kind in ("avgpool", "maxpool"):
+                ops.append(_pool(nm, inp, kind, 3, 1, 1))
+                slot_out.append(nm)
+            else:
+                ops.append(_view(nm, "identity", [inp]))
+                slot_out.append(nm)
+        ops.append({"name": f"add{b}", "kind": "add", "in": slot_out, "block": -1})
+        outs.append(f"add{b}")
+    ops.append(_view("out", "concat", outs))
+    return {"name": "nasnet", "batch": batch, "seed": seed,
+            "inputs": [{"name": "h", "c": channels, "h": hw, "w": hw},
+                       {"name": "h_prev", "c": channels, "h": hw, "w": hw}],
+            "ops": ops, "outputs": ["out"], "choices": choices}
+
+
+FIRE = [(16, 64), (16, 64), (32, 128), (32, 128), (48, 192), (48, 192), (64, 256), (64, 256)]
+
+
+def spec_squeeze(batch: int = 1, seed: int = 0) -> dict:
+    ops = []
+    cur = "x"
+    block = 0
+    for m, (s, e) in enumerate(FIRE, start=1):
+        ops.append(_conv(f"m{m}sq", cur, s, 1, 0, block=block))
+        ops.append(_conv(f"m{m}e1", f"m{m}sq", e, 1, 0, block=block))
+        ops.append(_conv(f"m{m}e3", f"m{m}sq", e, 3, 1, block=block))
+        ops.append(_view(f"m{m}", "concat", [f"m{m}e1", f"m{m}e3"]))
+        cur = f"m{m}"
+        block += 1
+        if m in (3, 7):
+            ops.append(_pool(f"pool{m}", cur, "maxpool", 3, 2, 0, block=block))
+            cur = f"pool{m}"
+            block += 1
+    return {"name": "squeeze", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 96, "h": 55, "w": 55}],
+            "ops": ops, "outputs": [cur]}
+
+
+SPECS = {"tiny": spec_tiny, "inception": spec_inception, "randwire": spec_randwire,
+         "nasnet": spec_nasnet, "squeeze": spec_squeeze}
+
+
+# ---------------------------------------------------------------- shapes
+
+def infer_shapes(spec: dict) -> Dict[str, Tuple[int, int, int]]:
+    """(C, H, W) of every named tensor (batch excluded)."""
+    shp = {t["name"]: (t["c"], t["h"], t["w"]) for t in spec["inputs"]}
+    for op in spec["ops"]:
+        ins = [shp[i] for i in op["in"]]
+        k = op["kind"]
+        c, h, w = ins[0]
+        if k in ("conv", "sepconv", "maxpool", "avgpool"):
+            ho = (h + 2 * op["ph"] - op["kh"]) // op["sh"] + 1
+            wo = (w + 2 * op["pw"] - op["kw"]) // op["sw"] + 1
+            co = op["cout"] if k in ("conv", "sepconv") else c
+            shp[op["name"]] = (co, ho, wo)
+        elif k == "concat":
+            shp[op["name"]] = (sum(s[0] for s in ins), h, w)
+        else:
+            shp[op["name"]] = (c, h, w)
+    return shp
+
+
+def param_shapes(spec: dict) -> List[Tuple[str, tuple, int]]:
+    """(tensor name, shape, fan_in) of every weight / bias, in a fixed order."""
+    shp = infer_shapes(spec)
+    out = []
+    for op in spec["ops"]:
+        cin = shp[op["in"][0]][0]
+        if op["kind"] == "conv":
+            out.append((op["name"] + ".w", (op["cout"], cin, op["kh"], op["kw"]),
+                        cin * op["kh"] * op["kw"]))
+            out.append((op["name"] + ".b", (op["cout"],), 0))
+        elif op["kind"] == "sepconv":
+            out.append((op["name"] + ".dw", (cin, 1, op["kh"], op["kw"]), op["kh"] * op["kw"]))
+            out.append((op["name"] + ".pw", (op["cout"], cin, 1, 1), cin))
+            out.append((op["name"] + ".b", (op["cout"],), 0))
+    return out
+
+
+def make_tensors(spec: dict, seed: int | None = None) -> Dict[str, np.ndarray]:
+    """Seeded inputs U(-1,1), weights N(0, 2/fan_in), zero biases (float32)."""
+    seed = spec.get("seed", 0) if seed is None else seed
+    name = spec["name"]
+    n = spec["batch"]
+    tensors = {}
+    idx = 0
+    for t in spec["inputs"]:
+        # inputs are keyed per image so that batch b's first image equals batch 1's
+        imgs = [rng.uniform_pm1(rng.key_of(name, seed, "input", idx, i), (t["c"], t["h"], t["w"]))
+                for i in range(n)]
+        tensors[t["name"]] = np.stack(imgs, 0)
+        idx += 1
+    for pname, shape, fan_in in param_shapes(spec):
+        if pname.endswith(".b"):
+            tensors[pname] = np.zeros(shape, dtype=np.float32)
+        else:
+            tensors[pname] = rng.normal(rng.key_of(name, seed, "param", pname), shape,
+                                        float(np.sqrt(2.0 / fan_in)))
+    return tensors
+
+
+def make(config: str, batch: int = 1, seed: int = 0):
+    """(spec, tensors) for one of CONFIG_NAMES."""
+    spec = SPECS[config](batch=batch, seed=seed)
+    return spec, make_tensors(spec, seed)
+
+
+def unit_ops(spec: dict) -> List[dict]:
+    """Operators that are schedule units (views excluded), in insertion order."""
+    return [op for op in spec["ops"] if op["kind"] not in ("concat", "identity")]
+
+
+def with_batch(spec: dict, batch: int) -> dict:
+    s = copy.deepcopy(spec)
+    s["batch"] = batch
+    return s

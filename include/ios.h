@@ -1,0 +1,260 @@
+/*
+ * ios.h — C ABI of libios: inter-operator scheduling and stage execution of
+ * multi-branch CNN blocks on one AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the method of "IOS: Inter-Operator Scheduler for CNN
+ * Acceleration" (Ding et al., MLSys 2021):
+ *   - a computation graph G = (V, E) of schedule units (Sec. 3, "Computation
+ *     Graph"; Table 2 "Conv-Relu" / "Relu-SepConv" units);
+ *   - stages executed one after another, each with a parallelization strategy,
+ *     "concurrent execution" or "operator merge" (Sec. 3, "Stage",
+ *     "Parallelization Strategy", "Schedule");
+ *   - the dynamic program over endings that picks the schedule minimising the
+ *     summed stage latency (Sec. 4.1, Algorithm 1), with schedule pruning
+ *     P(r, s) (Sec. 4.3) and block-wise optimisation (Sec. 4.2);
+ *   - stage latencies measured on the device (Sec. 4.1, GenerateStage; Sec. 5).
+ *
+ * Conventions for every call:
+ *   - Activations are float32, NCHW, contiguous; the batch N is fixed per graph.
+ *   - Host arrays passed in are only read during the call and are copied where
+ *     kept (the caller keeps ownership).  Device pointers are never freed by
+ *     the library.
+ *   - Every call returns IOS_OK (0) or a negative IOS_E_* code; on error
+ *     ios_last_error() returns a message for the calling thread and no output
+ *     argument is written.  No C++ exception crosses this ABI.
+ *   - A graph handle (and every schedule made from it) must be used by one
+ *     thread at a time.
+ */
+#ifndef IOS_H_
+#define IOS_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ----------------------------------------------------------------- errors */
+enum {
+  IOS_OK = 0,
+  IOS_E_ARG = -1,            /* null pointer, bad id, value out of range          */
+  IOS_E_SHAPE = -2,          /* tensor shapes do not fit the operator             */
+  IOS_E_STATE = -3,          /* call not allowed before/after ios_graph_finalize  */
+  IOS_E_NOT_MERGEABLE = -4,  /* operator merge asked for a set that cannot merge  */
+  IOS_E_BAD_STAGE = -5,      /* units do not form a valid stage / schedule        */
+  IOS_E_TOO_MANY_OPS = -6,   /* more than 64 schedule units in one block          */
+  IOS_E_OOM = -7,            /* host or device allocation failed                  */
+  IOS_E_HIP = -8,            /* a HIP runtime call failed                         */
+  IOS_E_COST_FN = -9,        /* the caller's cost callback returned non-zero      */
+  IOS_E_UNSUPPORTED = -10,   /* valid request outside what the library supports   */
+  IOS_E_DEVICE = -11         /* a stage kernel reported an error (see ios_device_status) */
+};
+
+/* --------------------------------------------------------------- operators */
+/* Schedule-unit kinds.  CONCAT and IDENTITY are views: they create a tensor
+ * but no schedule unit (producers of a concat write straight into its
+ * channel slices, which plays the role of the paper's split/concat). */
+enum {
+  IOS_CONV = 0,      /* dense conv + bias ("Conv-Relu", Table 2)                 */
+  IOS_SEPCONV = 1,   /* sum(inputs) -> ReLU -> depthwise kxk -> pointwise 1x1    */
+  IOS_POOL_MAX = 2,  /* kxk max pool; taps outside the input are ignored         */
+  IOS_POOL_AVG = 3,  /* kxk average pool; divides by kh*kw (padding counts 0)    */
+  IOS_ADD = 4,       /* elementwise sum of n >= 1 inputs                          */
+  IOS_MEAN = 5,      /* elementwise mean of n >= 1 inputs                         */
+  IOS_CONCAT = 6,    /* channel concatenation, in input order (view)              */
+  IOS_IDENTITY = 7   /* the input itself (view)                                   */
+};
+
+typedef struct {
+  int32_t kind;                /* IOS_CONV .. IOS_IDENTITY                          */
+  int32_t cout;                /* CONV / SEPCONV output channels; ignored otherwise */
+  int32_t kh, kw;              /* CONV, pools: window; SEPCONV: depthwise window    */
+  int32_t stride_h, stride_w;  /* CONV, pools (SEPCONV requires 1)                  */
+  int32_t pad_h, pad_w;        /* zero padding (CONV, SEPCONV, POOL_AVG); max pool
+                                  ignores out-of-bounds taps                        */
+  int32_t pre_relu;            /* ReLU applied to the input (SEPCONV: to the sum)   */
+  int32_t post_relu;           /* ReLU applied to the output (CONV only)            */
+  int32_t block_id;            /* -1 = automatic; else >= 0, see ios_graph_finalize */
+} ios_op_desc;
+
+typedef struct ios_graph ios_graph;
+typedef struct ios_schedule_t ios_schedule_t;
+
+/* Create an empty graph for batch size `batch` (>= 1).  The paper tunes a
+ * schedule per batch size (Sec. 6.2), so the batch is fixed per graph.
+ * *out receives a handle owned by the caller; free it with ios_graph_destroy.
+ * Errors: IOS_E_ARG (batch < 1, out NULL), IOS_E_OOM. */
+int ios_graph_create(int32_t batch, ios_graph **out);
+
+/* Free a graph and every device buffer it owns.  Schedules made from it must
+ * be destroyed first.  NULL is ignored. */
+void ios_graph_destroy(ios_graph *g);
+
+/* Declare a graph input of shape [batch][c][h][w] (float32 NCHW).  Inputs
+ * are numbered 0, 1, ... in call order; ios_run takes them in that order.
+ * *tensor_id receives the input's tensor id.
+ * Errors: IOS_E_ARG (non-positive size, NULL), IOS_E_STATE (after finalize). */
+int ios_add_input(ios_graph *g, int32_t c, int32_t h, int32_t w, int32_t *tensor_id);
+
+/* Append one operator reading tensors in_ids[0 .. n_in-1] (already existing,
+ * so insertion order is topological, Sec. 3).  Its output tensor id is
+ * written to *out_tensor_id; for a schedule unit (every kind but CONCAT and
+ * IDENTITY) that id also names the unit in schedules and cost callbacks.
+ *   CONV     n_in = 1; weights [cout][cin][kh][kw]; bias [cout] or NULL (zero).
+ *   SEPCONV  n_in >= 1 inputs of equal shape, summed; weights = depthwise
+ *            [cin][1][kh][kw] followed by pointwise [cout][cin][1][1];
+ *            bias [cout] or NULL; stride 1, pad (kh/2, kw/2) expected.
+ *   POOL_*   n_in = 1; no weights.
+ *   ADD/MEAN n_in >= 1 inputs of equal shape; no weights.
+ *   CONCAT   n_in >= 1 inputs of equal batch/h/w; each must be a schedule
+ *            unit's output (or a concat of them) not already in a concat.
+ *   IDENTITY n_in = 1.
+ * At most 16 inputs.  Weights are copied.
+ * Errors: IOS_E_ARG, IOS_E_SHAPE, IOS_E_UNSUPPORTED, IOS_E_STATE. */
+int ios_add_op(ios_graph *g, const ios_op_desc *d, const int32_t *in_ids, int32_t n_in,
+               const float *weights, const float *bias, int32_t *out_tensor_id);
+
+/* Mark a tensor as graph output number k (k = 0, 1, ... in call order).  It
+ * must be a whole buffer: a unit output or a concat view that is not itself a
+ * slice of a larger concat, and not a graph input.
+ * Errors: IOS_E_ARG, IOS_E_UNSUPPORTED, IOS_E_STATE. */
+int ios_mark_output(ios_graph *g, int32_t tensor_id);
+
+/* Freeze the graph: assign blocks, plan concat slices, allocate device
+ * intermediates, pack and upload weights.  Must be called once, before any
+ * profile / schedule / run call.  Blocks (Sec. 4.2, optimising each block of a
+ * stacked CNN separately): if every unit has block_id -1, all units form
+ * block 0 when there are at most 64 of them, otherwise the units are cut
+ * before every unit that is an ancestor or descendant of every other unit;
+ * if any unit names a block, all must, a unit's block must not be lower than
+ * its producers', and blocks run in ascending id.  A block holds at most 64
+ * units.  Uses the current HIP device.
+ * Errors: IOS_E_TOO_MANY_OPS, IOS_E_BAD_STAGE, IOS_E_OOM, IOS_E_HIP, IOS_E_STATE. */
+int ios_graph_finalize(ios_graph *g);
+
+/* Number of blocks, and the unit ids of block b in ascending order: bit i of a
+ * block-local stage mask is unit_ids[i].  unit_ids must hold 64 entries.
+ * Errors: IOS_E_ARG, IOS_E_STATE. */
+int ios_graph_blocks(const ios_graph *g, int32_t *n_blocks);
+int ios_block_units(const ios_graph *g, int32_t block, int32_t *n, int32_t *unit_ids);
+
+/* Parallelization strategies of a stage (Sec. 3). */
+enum { IOS_CONCURRENT = 0, IOS_MERGE = 1 };
+
+/* Whether the units can form one operator-merge stage: at least two dense
+ * convs reading the same tensor with equal stride and ReLU flags, each kernel
+ * centring in the largest with the same resulting padding (Sec. 3).
+ * *ok receives 1 or 0.  Errors: IOS_E_ARG, IOS_E_STATE. */
+int ios_stage_mergeable(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t *ok);
+
+/* Measure one stage on the device, as GenerateStage does (Sec. 4.1,
+ * Algorithm 1): the stage's single grouped kernel is launched `warmup` times,
+ * then `repeats` times `reps` back-to-back launches between two HIP events on
+ * the library's stream; *latency_ns receives the median per-launch time,
+ * rounded to ns.  Uses the graph's own buffers (inputs hold zeros), not the
+ * caller's.  Units must lie in one block and be closed under the stage rule:
+ * a unit's producers inside the block are either in the stage or scheduled
+ * before it.  strategy IOS_MERGE requires ios_stage_mergeable.
+ * Blocks the calling thread until the timing is done.
+ * Errors: IOS_E_ARG, IOS_E_BAD_STAGE, IOS_E_NOT_MERGEABLE, IOS_E_HIP, IOS_E_STATE. */
+int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t strategy,
+                      int32_t warmup, int32_t reps, int32_t repeats, int64_t *latency_ns);
+
+/* Cost provider for the dynamic program: latency of stage `stage_mask`
+ * (block-local bits, see ios_block_units; unit_ids lists the same units,
+ * ascending) of block `block` under `strategy`.  Write a latency in ns, or
+ * INT64_MAX for "impossible", to *latency_ns and return 0; any other return
+ * aborts ios_schedule with IOS_E_COST_FN.  Never called with IOS_MERGE for a
+ * set that cannot merge. */
+typedef int (*ios_cost_fn)(void *ctx, int32_t block, uint64_t stage_mask,
+                           const int32_t *unit_ids, int32_t n, int32_t strategy,
+                           int64_t *latency_ns);
+
+enum { IOS_SCHED_DP = 0, IOS_SCHED_SEQUENTIAL = 1, IOS_SCHED_GREEDY = 2 };
+
+typedef struct {
+  int32_t mode;        /* IOS_SCHED_DP (Algorithm 1), SEQUENTIAL (one unit per
+                          stage, ascending id), GREEDY (every ready unit in the
+                          next stage, concurrent) — Sec. 6.1 baselines        */
+  int32_t r;           /* pruning: max units per group; <= 0 = unlimited     */
+  int32_t s;           /* pruning: max groups per stage; <= 0 = unlimited    */
+  int32_t strategies;  /* bit 0 concurrent, bit 1 merge: 3 = IOS-Both,
+                          1 = IOS-Parallel, 2 = IOS-Merge (Sec. 6.1)         */
+  int32_t warmup, reps, repeats;   /* profiler settings when fn is NULL     */
+} ios_sched_opts;
+
+/* Fill opts with the paper's defaults: DP, r = 3, s = 8 (Sec. 5), both
+ * strategies, warmup 3, reps 20, repeats 3. */
+void ios_sched_opts_default(ios_sched_opts *opts);
+
+/* Find a schedule (Algorithm 1, block by block).  With fn == NULL each
+ * candidate stage is measured with ios_profile_stage; otherwise fn(ctx, ...)
+ * supplies latencies.  Ties: a stage keeps concurrent execution only if it is
+ * strictly faster than merge; among equal-cost endings the smallest
+ * block-local mask wins.  *out receives a schedule owned by the caller (free
+ * with ios_schedule_destroy) and *cost_ns the minimised sum of stage
+ * latencies (SEQUENTIAL / GREEDY: the sum under the same cost provider).
+ * Errors: IOS_E_ARG, IOS_E_STATE, IOS_E_COST_FN, IOS_E_HIP, IOS_E_OOM. */
+int ios_schedule(ios_graph *g, const ios_sched_opts *opts, ios_cost_fn fn, void *ctx,
+                 ios_schedule_t **out, int64_t *cost_ns);
+
+/* Build a schedule from an explicit stage list: stage k holds
+ * unit_ids[stage_offsets[k] .. stage_offsets[k+1]-1] with strategy
+ * strategies[k].  Every unit must appear once; each stage must lie in one
+ * block, blocks must appear in ascending order, a unit's producers must be
+ * in earlier stages or in the same stage (concurrent only), and merge stages
+ * must be mergeable.  Errors: IOS_E_ARG, IOS_E_BAD_STAGE, IOS_E_NOT_MERGEABLE. */
+int ios_schedule_from_stages(ios_graph *g, int32_t n_stages, const int32_t *stage_offsets,
+                             const int32_t *unit_ids, const int32_t *strategies,
+                             ios_schedule_t **out);
+
+/* Read a schedule Q = [(S_1, T_1), ..., (S_k, T_k)] (Sec. 3, "Schedule"):
+ * stages in execution order, unit ids ascending inside a stage.  The arrays
+ * belong to the schedule and live until ios_schedule_destroy. */
+int ios_schedule_get(const ios_schedule_t *q, int32_t *n_stages, const int32_t **stage_offsets,
+                     const int32_t **unit_ids, const int32_t **strategies);
+
+/* Search statistics of a DP schedule: distinct states S visited (the empty
+ * set included), (S, S') transitions evaluated (Sec. 4.2) and distinct
+ * stages S' whose latency was requested.  Zero for other schedules. */
+int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transitions,
+                       int64_t *stages_measured);
+
+void ios_schedule_destroy(ios_schedule_t *q);
+
+/* Write the stage-latency table of the graph's last ios_schedule call as JSON
+ * lines {"block", "mask", "units", "concurrent_ns", "merge_ns" (null if not
+ * measured)} to `path`, so that the search can be replayed.
+ * Errors: IOS_E_ARG, IOS_E_STATE (no table). */
+int ios_schedule_dump_costs(const ios_graph *g, const char *path);
+
+/* Execute graph g under schedule q: for each stage in order, one kernel
+ * launch on `hip_stream` (a hipStream_t; NULL = the default stream).
+ * d_inputs[i] points to input i, d_outputs[k] to output k, each a device
+ * buffer of the declared shape owned by the caller.  Asynchronous: returns
+ * after the launches are queued, without synchronising.  Runs of one schedule
+ * must not overlap in time (they share per-stage counters), so issue them on
+ * one stream.  Errors: IOS_E_ARG, IOS_E_STATE, IOS_E_HIP. */
+int ios_run(ios_graph *g, ios_schedule_t *q, const float *const *d_inputs,
+            float *const *d_outputs, void *hip_stream);
+
+/* As ios_run, then records a HIP event before and after every stage launch,
+ * waits for the stream, and writes each stage's GPU time in ns to
+ * stage_ns[0 .. n_stages-1].  For per-stage measurement; blocks the caller. */
+int ios_run_timed(ios_graph *g, ios_schedule_t *q, const float *const *d_inputs,
+                  float *const *d_outputs, void *hip_stream, int64_t *stage_ns);
+
+/* Wait for `hip_stream` and read the graph's device error word: *flags
+ * receives 0 if every stage kernel since the last call finished normally,
+ * else a bit set (1 = an intra-stage dependency wait gave up).  Clears it.
+ * Errors: IOS_E_ARG, IOS_E_HIP. */
+int ios_device_status(ios_graph *g, void *hip_stream, int32_t *flags);
+
+/* Message describing the calling thread's most recent error. */
+const char *ios_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IOS_H_ */

@@ -236,8 +236,12 @@ CostFn = Callable[[int, int], Optional[float]]   # (S' mask, strategy) -> latenc
 
 
 def generate_stage(blk: Block, Sp: int, cost: CostFn, strategies=(CONCURRENT, MERGE)):
-    """GenerateStage: (latency, strategy) of the better of the two."""
-    l_conc = cost(Sp, CONCURRENT) if CONCURRENT in strategies else INF
+    """GenerateStage: (latency, strategy) of the better of the two.
+
+    With concurrent execution switched off (the IOS-Merge variant of Sec. 6.1)
+    a one-unit stage still runs, as the unit alone."""
+    single = Sp & (Sp - 1) == 0
+    l_conc = cost(Sp, CONCURRENT) if (CONCURRENT in strategies or single) else INF
     if MERGE in strategies and mergeable(blk, Sp):
         l_merge = cost(Sp, MERGE)
     else:

@@ -1,0 +1,312 @@
+// Stage lowering, launching and on-device latency measurement.
+//
+// A stage (S', T) of the schedule (Sec. 3) becomes ONE kernel launch whose
+// workgroups each run one tile taken from a table that spans every operator
+// of the stage:
+//   - concurrent execution: every unit keeps its own tiles; units of one
+//     group that depend on each other run in order because a consumer tile
+//     waits until all tiles of its producers have finished (Sec. 3, groups
+//     are executed sequentially, different groups concurrently);
+//   - operator merge: the convs' kernels are zero-padded (centred) to the
+//     largest kernel and stacked along output channels; the input is read
+//     once and each output-channel range is written straight to its own
+//     op's buffer, which stands in for the split operator (Sec. 3).
+// GenerateStage measures a stage by launching it repeatedly between HIP
+// events (Sec. 4.1).
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+
+#include "ios_internal.h"
+
+namespace ios {
+
+int choose_conv_tile(int64_t M, int N);
+
+static int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+static int round_up(int a, int b) { return (a + b - 1) / b * b; }
+
+std::vector<float *> default_buffers(const ios_graph *g) {
+  std::vector<float *> p(g->bufs.size());
+  for (size_t i = 0; i < g->bufs.size(); ++i) p[i] = g->bufs[i].dev;
+  return p;
+}
+
+namespace {
+
+struct SlotMap {
+  std::vector<int> bufs;
+  int get(int b) {
+    for (size_t i = 0; i < bufs.size(); ++i)
+      if (bufs[i] == b) return (int)i;
+    if ((int)bufs.size() >= kMaxSlots) fail(IOS_E_BAD_STAGE, "stage touches more than 64 buffers");
+    bufs.push_back(b);
+    return (int)bufs.size() - 1;
+  }
+};
+
+int resolved(const ios_graph *g, int t) {
+  while (g->tensors[t].kind == T_IDENTITY) t = g->ops[g->tensors[t].op].in[0];
+  return t;
+}
+
+void set_inputs(const ios_graph *g, const Op &op, DevOp &d, SlotMap &sm) {
+  d.n_in = (int)op.in.size();
+  for (int i = 0; i < d.n_in; ++i) {
+    const Tensor &t = g->tensors[resolved(g, op.in[i])];
+    d.in_slot[i] = sm.get(t.buf);
+    d.in_coff[i] = t.coff;
+    d.in_ctot[i] = g->bufs[t.buf].ctot;
+  }
+}
+
+void set_route(const ios_graph *g, DevOp &d, int r, int n0, int out_tensor, SlotMap &sm) {
+  const Tensor &t = g->tensors[out_tensor];
+  d.route_n0[r] = n0;
+  d.route_slot[r] = sm.get(t.buf);
+  d.route_coff[r] = t.coff;
+  d.route_ctot[r] = g->bufs[t.buf].ctot;
+}
+
+void fill_common(const ios_graph *g, const Op &op, DevOp &d) {
+  d.N = g->batch;
+  d.Cin = op.cin; d.H = op.h; d.W = op.wd;
+  d.Ho = op.ho; d.Wo = op.wo;
+  d.kh = op.d.kh; d.kw = op.d.kw;
+  d.sh = op.d.stride_h; d.sw = op.d.stride_w;
+  d.ph = op.d.pad_h; d.pw = op.d.pad_w;
+  d.pre_relu = op.d.pre_relu; d.post_relu = op.d.post_relu;
+}
+
+// Per-tile work estimate (MACs or elementwise ops), for ordering tiles.
+double tile_work(const DevOp &d) {
+  switch (d.kind) {
+    case DK_CONV: {
+      TileShape s = tile_shape(d.tcfg);
+      return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * d.kh * d.kw * d.CinP / s.wk;
+    }
+    case DK_SEP:
+      return (double)kSepBM * d.CinP * (d.kh * d.kw * d.n_in + d.Npad / 4.0);
+    default:
+      return (double)kEltPerTile * (d.kind <= DK_POOL_AVG ? d.kh * d.kw : d.n_in) / 4.0;
+  }
+}
+
+template <class T>
+void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool scratch) {
+  size_t n = std::max<size_t>(v.size(), 1);
+  if (!scratch || *cap < n) {
+    if (scratch && *dptr) hipFree(*dptr);
+    hip_check(hipMalloc(dptr, sizeof(T) * n), "hipMalloc(stage)");
+    if (scratch) *cap = n;
+  }
+  if (!v.empty())
+    hip_check(hipMemcpy(*dptr, v.data(), sizeof(T) * v.size(), hipMemcpyHostToDevice),
+              "hipMemcpy(stage)");
+}
+
+}  // namespace
+
+void free_stage(CompiledStage *cs) {
+  if (!cs->owns) return;
+  if (cs->d_ops) hipFree(cs->d_ops);
+  if (cs->d_tiles) hipFree(cs->d_tiles);
+  if (cs->d_ctr) hipFree(cs->d_ctr);
+  if (cs->d_mw) hipFree(cs->d_mw);
+  if (cs->d_mb) hipFree(cs->d_mb);
+  cs->d_ops = nullptr; cs->d_tiles = nullptr; cs->d_ctr = nullptr;
+  cs->d_mw = nullptr; cs->d_mb = nullptr;
+}
+
+void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
+                   bool scratch) {
+  if (ops.empty()) fail(IOS_E_BAD_STAGE, "empty stage");
+  int blk = g->ops[ops[0]].block;
+  for (size_t i = 0; i < ops.size(); ++i) {
+    if (g->ops[ops[i]].block != blk) fail(IOS_E_BAD_STAGE, "stage spans several blocks");
+    if (i && ops[i] <= ops[i - 1]) fail(IOS_E_BAD_STAGE, "stage units must be distinct, ascending");
+  }
+  SlotMap sm;
+  std::vector<DevOp> dops;
+  std::vector<float> mw, mb;
+  if (strategy == IOS_MERGE) {
+    if (!stage_mergeable(g, ops)) fail(IOS_E_NOT_MERGEABLE, "stage cannot be merged");
+    if ((int)ops.size() > kMaxRoutes) fail(IOS_E_UNSUPPORTED, "merge of more than 8 convs");
+    const Op &o0 = g->ops[ops[0]];
+    int KH = 0, KW = 0, total = 0;
+    for (int i : ops) {
+      KH = std::max(KH, g->ops[i].d.kh);
+      KW = std::max(KW, g->ops[i].d.kw);
+      total += g->ops[i].d.cout;
+    }
+    DevOp d{};
+    d.kind = DK_CONV;
+    fill_common(g, o0, d);
+    d.kh = KH; d.kw = KW;
+    d.ph = o0.d.pad_h + (KH - o0.d.kh) / 2;
+    d.pw = o0.d.pad_w + (KW - o0.d.kw) / 2;
+    d.Cout = total;
+    d.CinP = round_up(o0.cin, 4);
+    d.Npad = round_up(total, 64);
+    d.tcfg = choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total);
+    set_inputs(g, o0, d, sm);
+    // packed [KH*KW][CinP][Npad]: each op's taps placed centred
+    mw.assign((size_t)KH * KW * d.CinP * d.Npad, 0.f);
+    mb.assign(d.Npad, 0.f);
+    int n0 = 0;
+    d.n_routes = (int)ops.size();
+    for (size_t r = 0; r < ops.size(); ++r) {
+      const Op &o = g->ops[ops[r]];
+      int dh = (KH - o.d.kh) / 2, dwc = (KW - o.d.kw) / 2;
+      for (int co = 0; co < o.d.cout; ++co) {
+        mb[n0 + co] = o.b[co];
+        for (int ci = 0; ci < o.cin; ++ci)
+          for (int u = 0; u < o.d.kh; ++u)
+            for (int v = 0; v < o.d.kw; ++v) {
+              int tap = (u + dh) * KW + (v + dwc);
+              mw[((size_t)tap * d.CinP + ci) * d.Npad + n0 + co] =
+                  o.w[(((size_t)co * o.cin + ci) * o.d.kh + u) * o.d.kw + v];
+            }
+      }
+      set_route(g, d, (int)r, n0, o.out, sm);
+      n0 += o.d.cout;
+    }
+    d.route_n0[d.n_routes] = total;
+    dops.push_back(d);
+  } else if (strategy == IOS_CONCURRENT) {
+    for (size_t i = 0; i < ops.size(); ++i) {
+      const Op &o = g->ops[ops[i]];
+      DevOp d{};
+      fill_common(g, o, d);
+      set_inputs(g, o, d, sm);
+      d.Cout = o.d.kind == IOS_CONV || o.d.kind == IOS_SEPCONV ? o.d.cout : o.cin;
+      d.n_routes = 1;
+      set_route(g, d, 0, 0, o.out, sm);
+      d.route_n0[1] = d.Cout;
+      switch (o.d.kind) {
+        case IOS_CONV:
+          d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad;
+          d.wpk = o.d_wpk; d.bias = o.d_bias;
+          break;
+        case IOS_SEPCONV:
+          d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
+          d.wpk = o.d_wpk; d.bias = o.d_bias; d.dw = o.d_dw;
+          break;
+        case IOS_POOL_MAX: d.kind = DK_POOL_MAX; break;
+        case IOS_POOL_AVG: d.kind = DK_POOL_AVG; break;
+        case IOS_ADD: d.kind = DK_ADD; break;
+        case IOS_MEAN: d.kind = DK_MEAN; d.inv_n = 1.0f / (float)o.in.size(); break;
+        default: fail(IOS_E_BAD_STAGE, "not a schedule unit");
+      }
+      // in-stage producers
+      for (int t : o.in)
+        for (int p : unit_producers(g, t)) {
+          auto it = std::find(ops.begin(), ops.end(), p);
+          if (it == ops.end()) continue;
+          int j = (int)(it - ops.begin());
+          bool dup = false;
+          for (int k = 0; k < d.n_deps; ++k) dup |= d.dep[k] == j;
+          if (dup) continue;
+          if (d.n_deps >= kMaxDeps) fail(IOS_E_UNSUPPORTED, "too many in-stage producers");
+          d.dep[d.n_deps++] = j;
+        }
+      dops.push_back(d);
+    }
+    for (auto &d : dops)
+      for (int k = 0; k < d.n_deps; ++k) dops[d.dep[k]].signal = 1;
+  } else {
+    fail(IOS_E_ARG, "unknown strategy");
+  }
+  // tile counts
+  for (auto &d : dops) {
+    int64_t M = (int64_t)d.N * d.Ho * d.Wo;
+    if (d.kind == DK_CONV) {
+      d.tiles_m = cdiv(M, tile_bm(d.tcfg));
+      d.tiles_n = cdiv(d.Cout, tile_bn(d.tcfg));
+    } else if (d.kind == DK_SEP) {
+      d.tiles_m = cdiv(M, kSepBM);
+      d.tiles_n = 1;
+    } else {
+      d.tiles_m = cdiv(M * d.Cout, kEltPerTile);
+      d.tiles_n = 1;
+    }
+    d.n_tiles = d.tiles_m * d.tiles_n;
+  }
+  // tile order: producers before consumers (depth), longer tiles first
+  int n = (int)dops.size();
+  std::vector<int> depth(n, 0);
+  for (int i = 0; i < n; ++i)
+    for (int k = 0; k < dops[i].n_deps; ++k) depth[i] = std::max(depth[i], depth[dops[i].dep[k]] + 1);
+  std::vector<int> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    if (depth[a] != depth[b]) return depth[a] < depth[b];
+    return tile_work(dops[a]) > tile_work(dops[b]);
+  });
+  std::vector<Tile> tiles;
+  bool ticket = false;
+  int lds = 0;
+  for (int i : order) {
+    for (int t = 0; t < dops[i].n_tiles; ++t) tiles.push_back(Tile{i, t});
+    ticket |= dops[i].n_deps > 0;
+    lds = std::max(lds, op_lds_bytes(dops[i]));
+  }
+  cs->ops = dops;
+  cs->tiles = tiles;
+  cs->slot_buf = sm.bufs;
+  cs->lds_bytes = lds;
+  cs->ticket = ticket;
+  cs->owns = !scratch;
+  // device copies
+  if (!mw.empty()) {
+    size_t *wc = scratch ? &g->scratch_w_cap : nullptr, *bc = scratch ? &g->scratch_b_cap : nullptr;
+    size_t dummy_w = 0, dummy_b = 0;
+    grow_upload(&cs->d_mw, wc ? wc : &dummy_w, mw, scratch);
+    grow_upload(&cs->d_mb, bc ? bc : &dummy_b, mb, scratch);
+    cs->ops[0].wpk = cs->d_mw;
+    cs->ops[0].bias = cs->d_mb;
+  }
+  size_t d0 = 0, d1 = 0, d2 = 0;
+  grow_upload(&cs->d_ops, scratch ? &g->scratch_ops_cap : &d0, cs->ops, scratch);
+  grow_upload(&cs->d_tiles, scratch ? &g->scratch_tiles_cap : &d1, cs->tiles, scratch);
+  std::vector<int32_t> ctr(2 + n, 0);
+  grow_upload(&cs->d_ctr, scratch ? &g->scratch_ctr_cap : &d2, ctr, scratch);
+}
+
+void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
+                     hipStream_t stream) {
+  StageArgs a{};
+  for (size_t i = 0; i < cs.slot_buf.size(); ++i) a.slot[i] = buf_ptr[cs.slot_buf[i]];
+  a.ops = cs.d_ops;
+  a.tiles = cs.d_tiles;
+  a.ctr = cs.d_ctr;
+  a.err = g->d_err;
+  a.n_tiles = (int)cs.tiles.size();
+  a.n_ops = (int)cs.ops.size();
+  a.use_ticket = cs.ticket ? 1 : 0;
+  a.spin_limit = 1 << 24;
+  hip_check(launch_stage(a, cs.lds_bytes, stream), "stage launch");
+}
+
+int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,
+                      int reps, int repeats) {
+  if (reps < 1 || repeats < 1 || warmup < 0) fail(IOS_E_ARG, "bad profiling counts");
+  CompiledStage &cs = g->scratch;
+  compile_stage(g, ops, strategy, &cs, true);
+  std::vector<float *> bufs = default_buffers(g);
+  for (int i = 0; i < warmup; ++i) launch_compiled(g, cs, bufs, g->stream);
+  std::vector<double> per;
+  for (int r = 0; r < repeats; ++r) {
+    hip_check(hipEventRecord(g->ev0, g->stream), "hipEventRecord");
+    for (int i = 0; i < reps; ++i) launch_compiled(g, cs, bufs, g->stream);
+    hip_check(hipEventRecord(g->ev1, g->stream), "hipEventRecord");
+    hip_check(hipEventSynchronize(g->ev1), "hipEventSynchronize");
+    float ms = 0.f;
+    hip_check(hipEventElapsedTime(&ms, g->ev0, g->ev1), "hipEventElapsedTime");
+    per.push_back((double)ms * 1e6 / reps);
+  }
+  std::sort(per.begin(), per.end());
+  return (int64_t)(per[per.size() / 2] + 0.5);
+}
+
+}  // namespace ios

@@ -1,0 +1,436 @@
+// Graph IR of libios: tensors, schedule units, views, blocks and the device
+// copies of weights (Sec. 3 "Computation Graph"; Sec. 4.2 block-wise
+// optimisation).
+#include <algorithm>
+#include <cstring>
+#include <functional>
+
+#include "ios_internal.h"
+
+namespace ios {
+
+void fail(int code, const std::string &msg) { throw Error{code, msg}; }
+
+void hip_check(hipError_t e, const char *what) {
+  if (e != hipSuccess)
+    fail(e == hipErrorOutOfMemory ? IOS_E_OOM : IOS_E_HIP,
+         std::string(what) + ": " + hipGetErrorString(e));
+}
+
+static bool is_unit_kind(int k) { return k >= IOS_CONV && k <= IOS_MEAN; }
+
+int unit_op_of_tensor(const ios_graph *g, int tid) {
+  if (tid < 0 || tid >= (int)g->tensors.size()) fail(IOS_E_ARG, "unit id out of range");
+  const Tensor &t = g->tensors[tid];
+  if (t.kind != T_UNIT) fail(IOS_E_ARG, "tensor " + std::to_string(tid) + " is not a unit output");
+  return t.op;
+}
+
+// Schedule units whose outputs a tensor carries (views resolved).
+std::vector<int> unit_producers(const ios_graph *g, int tid) {
+  const Tensor &t = g->tensors[tid];
+  if (t.kind == T_INPUT) return {};
+  if (t.kind == T_UNIT) return {t.op};
+  std::vector<int> out;
+  for (int i : g->ops[t.op].in) {
+    auto p = unit_producers(g, i);
+    out.insert(out.end(), p.begin(), p.end());
+  }
+  return out;
+}
+
+int64_t op_flops(const ios_graph *g, const Op &op) {
+  int64_t n = g->batch;
+  switch (op.d.kind) {
+    case IOS_CONV:
+      return 2 * n * op.ho * op.wo * (int64_t)op.d.cout * op.cin * op.d.kh * op.d.kw;
+    case IOS_SEPCONV:
+      return 2 * n * op.ho * op.wo * (int64_t)op.cin * (op.d.kh * op.d.kw + op.d.cout);
+    case IOS_POOL_MAX:
+    case IOS_POOL_AVG:
+      return n * op.ho * op.wo * (int64_t)op.cin * op.d.kh * op.d.kw;
+    default:
+      return n * op.ho * op.wo * (int64_t)op.cin * (int64_t)op.in.size();
+  }
+}
+
+// ---------------------------------------------------------------- building
+
+static int new_tensor(ios_graph *g, int c, int h, int w, int kind, int op) {
+  Tensor t;
+  t.c = c; t.h = h; t.w = w; t.kind = kind; t.op = op;
+  g->tensors.push_back(t);
+  return (int)g->tensors.size() - 1;
+}
+
+int add_input(ios_graph *g, int c, int h, int w) {
+  if (g->finalized) fail(IOS_E_STATE, "graph already finalized");
+  if (c <= 0 || h <= 0 || w <= 0) fail(IOS_E_ARG, "input sizes must be positive");
+  int id = new_tensor(g, c, h, w, T_INPUT, -1);
+  g->tensors[id].input_index = (int)g->inputs.size();
+  g->inputs.push_back(id);
+  return id;
+}
+
+static int out_size(int in, int k, int s, int p) { return (in + 2 * p - k) / s + 1; }
+
+int add_op(ios_graph *g, const ios_op_desc *d, const int32_t *in_ids, int n_in,
+           const float *weights, const float *bias) {
+  if (g->finalized) fail(IOS_E_STATE, "graph already finalized");
+  if (!d) fail(IOS_E_ARG, "null op descriptor");
+  if (n_in < 1 || n_in > kMaxIn) fail(IOS_E_ARG, "an operator takes 1..16 inputs");
+  if (!in_ids) fail(IOS_E_ARG, "null input list");
+  for (int i = 0; i < n_in; ++i)
+    if (in_ids[i] < 0 || in_ids[i] >= (int)g->tensors.size())
+      fail(IOS_E_ARG, "input tensor id out of range");
+  Op op;
+  op.d = *d;
+  op.in.assign(in_ids, in_ids + n_in);
+  const Tensor &t0 = g->tensors[in_ids[0]];
+  op.cin = t0.c; op.h = t0.h; op.wd = t0.w;
+  int kind = d->kind;
+  int oc = t0.c, oh = t0.h, ow = t0.w;
+  auto same_shape = [&]() {
+    for (int i = 1; i < n_in; ++i) {
+      const Tensor &t = g->tensors[in_ids[i]];
+      if (t.c != t0.c || t.h != t0.h || t.w != t0.w) fail(IOS_E_SHAPE, "inputs differ in shape");
+    }
+  };
+  switch (kind) {
+    case IOS_CONV:
+    case IOS_SEPCONV:
+    case IOS_POOL_MAX:
+    case IOS_POOL_AVG: {
+      if (kind != IOS_SEPCONV && n_in != 1) fail(IOS_E_ARG, "this operator takes one input");
+      if (kind == IOS_SEPCONV) same_shape();
+      if (d->kh < 1 || d->kw < 1 || d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 ||
+          d->pad_w < 0)
+        fail(IOS_E_ARG, "bad kernel / stride / padding");
+      if (kind == IOS_SEPCONV && (d->stride_h != 1 || d->stride_w != 1))
+        fail(IOS_E_UNSUPPORTED, "SEPCONV needs stride 1");
+      if (kind == IOS_POOL_MAX && (d->pad_h >= d->kh || d->pad_w >= d->kw))
+        fail(IOS_E_ARG, "max-pool padding must be smaller than the window");
+      oh = out_size(t0.h, d->kh, d->stride_h, d->pad_h);
+      ow = out_size(t0.w, d->kw, d->stride_w, d->pad_w);
+      if (oh < 1 || ow < 1) fail(IOS_E_SHAPE, "window larger than the padded input");
+      if (kind == IOS_CONV || kind == IOS_SEPCONV) {
+        if (d->cout < 1) fail(IOS_E_ARG, "cout must be positive");
+        if (!weights) fail(IOS_E_ARG, "weights required");
+        oc = d->cout;
+        size_t nw = kind == IOS_CONV
+                        ? (size_t)d->cout * t0.c * d->kh * d->kw
+                        : (size_t)t0.c * d->kh * d->kw + (size_t)d->cout * t0.c;
+        op.w.assign(weights, weights + nw);
+        op.b.assign((size_t)d->cout, 0.f);
+        if (bias) std::memcpy(op.b.data(), bias, sizeof(float) * d->cout);
+        if (kind == IOS_SEPCONV && (t0.c > kMaxChannels || d->cout > kMaxChannels))
+          fail(IOS_E_UNSUPPORTED, "SEPCONV supports at most 256 channels");
+      }
+      break;
+    }
+    case IOS_ADD:
+    case IOS_MEAN:
+      same_shape();
+      break;
+    case IOS_CONCAT: {
+      oc = 0;
+      for (int i = 0; i < n_in; ++i) {
+        const Tensor &t = g->tensors[in_ids[i]];
+        if (t.h != t0.h || t.w != t0.w) fail(IOS_E_SHAPE, "concat inputs differ in size");
+        if (t.kind != T_UNIT && t.kind != T_CONCAT)
+          fail(IOS_E_UNSUPPORTED, "concat members must be unit outputs or concats");
+        if (t.parent >= 0) fail(IOS_E_UNSUPPORTED, "tensor already placed in a concat");
+        for (int j = 0; j < i; ++j)
+          if (in_ids[j] == in_ids[i]) fail(IOS_E_UNSUPPORTED, "tensor repeated in a concat");
+        oc += t.c;
+      }
+      break;
+    }
+    case IOS_IDENTITY:
+      if (n_in != 1) fail(IOS_E_ARG, "identity takes one input");
+      break;
+    default:
+      fail(IOS_E_ARG, "unknown operator kind");
+  }
+  op.ho = oh; op.wo = ow;
+  int op_idx = (int)g->ops.size();
+  int tkind = is_unit_kind(kind) ? T_UNIT : (kind == IOS_CONCAT ? T_CONCAT : T_IDENTITY);
+  int tid = new_tensor(g, oc, oh, ow, tkind, op_idx);
+  op.out = tid;
+  if (is_unit_kind(kind)) {
+    op.unit = (int)g->units.size();
+    g->units.push_back(op_idx);
+  }
+  if (kind == IOS_CONCAT) {
+    int off = 0;
+    for (int i = 0; i < n_in; ++i) {
+      Tensor &m = g->tensors[in_ids[i]];
+      m.parent = tid;
+      m.parent_off = off;
+      off += m.c;
+    }
+  }
+  g->ops.push_back(std::move(op));
+  return tid;
+}
+
+void mark_output(ios_graph *g, int tid) {
+  if (g->finalized) fail(IOS_E_STATE, "graph already finalized");
+  if (tid < 0 || tid >= (int)g->tensors.size()) fail(IOS_E_ARG, "tensor id out of range");
+  int t = tid;
+  while (g->tensors[t].kind == T_IDENTITY) t = g->ops[g->tensors[t].op].in[0];
+  const Tensor &r = g->tensors[t];
+  if (r.kind == T_INPUT) fail(IOS_E_UNSUPPORTED, "a graph input cannot be an output");
+  if (r.parent >= 0) fail(IOS_E_UNSUPPORTED, "an output must not be a slice of a concat");
+  for (int o : g->outputs) {
+    int u = o;
+    while (g->tensors[u].kind == T_IDENTITY) u = g->ops[g->tensors[u].op].in[0];
+    if (u == t) fail(IOS_E_UNSUPPORTED, "tensor already marked as an output");
+  }
+  g->outputs.push_back(tid);
+}
+
+// ---------------------------------------------------------------- blocks
+
+static void assign_blocks(ios_graph *g) {
+  int nu = (int)g->units.size();
+  if (nu == 0) fail(IOS_E_BAD_STAGE, "graph has no schedule units");
+  // unit-level adjacency (global)
+  std::vector<std::vector<int>> succ(nu), pred(nu);
+  for (int v = 0; v < nu; ++v) {
+    const Op &op = g->ops[g->units[v]];
+    for (int t : op.in)
+      for (int p : unit_producers(g, t)) {
+        int u = g->ops[p].unit;
+        if (std::find(succ[u].begin(), succ[u].end(), v) == succ[u].end()) {
+          succ[u].push_back(v);
+          pred[v].push_back(u);
+        }
+      }
+  }
+  std::vector<int> bid(nu);
+  int explicit_n = 0;
+  for (int v = 0; v < nu; ++v) explicit_n += g->ops[g->units[v]].d.block_id >= 0;
+  if (explicit_n != 0 && explicit_n != nu)
+    fail(IOS_E_BAD_STAGE, "either every unit names a block or none does");
+  if (explicit_n == nu) {
+    std::vector<int> ids;
+    for (int v = 0; v < nu; ++v) ids.push_back(g->ops[g->units[v]].d.block_id);
+    std::vector<int> sorted = ids;
+    std::sort(sorted.begin(), sorted.end());
+    sorted.erase(std::unique(sorted.begin(), sorted.end()), sorted.end());
+    for (int v = 0; v < nu; ++v)
+      bid[v] = (int)(std::lower_bound(sorted.begin(), sorted.end(), ids[v]) - sorted.begin());
+    for (int v = 0; v < nu; ++v)
+      for (int u : pred[v])
+        if (bid[u] > bid[v]) fail(IOS_E_BAD_STAGE, "a unit's block precedes its producer's");
+  } else if (nu <= kMaxUnitsPerBlock) {
+    std::fill(bid.begin(), bid.end(), 0);
+  } else {
+    // cut before every unit comparable with all others
+    std::vector<std::vector<char>> anc(nu, std::vector<char>(nu, 0));
+    for (int v = 0; v < nu; ++v)
+      for (int u : pred[v]) {
+        anc[v][u] = 1;
+        for (int w = 0; w < nu; ++w) anc[v][w] |= anc[u][w];
+      }
+    int b = 0;
+    for (int v = 0; v < nu; ++v) {
+      bool cut = v > 0;
+      for (int w = 0; w < nu && cut; ++w)
+        if (w != v && !anc[v][w] && !anc[w][v]) cut = false;
+      if (cut) ++b;
+      bid[v] = b;
+    }
+  }
+  int nb = *std::max_element(bid.begin(), bid.end()) + 1;
+  g->blocks.assign(nb, Block{});
+  for (int v = 0; v < nu; ++v) {
+    Block &B = g->blocks[bid[v]];
+    if ((int)B.ops.size() >= kMaxUnitsPerBlock)
+      fail(IOS_E_TOO_MANY_OPS, "more than 64 schedule units in one block");
+    Op &op = g->ops[g->units[v]];
+    op.block = bid[v];
+    op.local = (int)B.ops.size();
+    B.ops.push_back(g->units[v]);
+  }
+  for (auto &B : g->blocks) {
+    B.succ.assign(B.ops.size(), 0);
+    B.pred.assign(B.ops.size(), 0);
+  }
+  for (int v = 0; v < nu; ++v)
+    for (int u : succ[v]) {
+      const Op &a = g->ops[g->units[v]], &c = g->ops[g->units[u]];
+      if (a.block == c.block) {
+        g->blocks[a.block].succ[a.local] |= 1ull << c.local;
+        g->blocks[a.block].pred[c.local] |= 1ull << a.local;
+      }
+    }
+}
+
+// ---------------------------------------------------------------- merge rule
+
+static int resolve_identity(const ios_graph *g, int t) {
+  while (g->tensors[t].kind == T_IDENTITY) t = g->ops[g->tensors[t].op].in[0];
+  return t;
+}
+
+bool stage_mergeable(const ios_graph *g, const std::vector<int> &ops) {
+  if (ops.size() < 2) return false;
+  const Op &o0 = g->ops[ops[0]];
+  int KH = 0, KW = 0;
+  for (int i : ops) {
+    const Op &o = g->ops[i];
+    if (o.d.kind != IOS_CONV) return false;
+    if (resolve_identity(g, o.in[0]) != resolve_identity(g, o0.in[0])) return false;
+    if (o.d.stride_h != o0.d.stride_h || o.d.stride_w != o0.d.stride_w ||
+        o.d.pre_relu != o0.d.pre_relu || o.d.post_relu != o0.d.post_relu)
+      return false;
+    KH = std::max(KH, o.d.kh);
+    KW = std::max(KW, o.d.kw);
+  }
+  int ph = -1, pw = -1;
+  for (int i : ops) {
+    const Op &o = g->ops[i];
+    if ((KH - o.d.kh) % 2 || (KW - o.d.kw) % 2) return false;
+    int a = o.d.pad_h + (KH - o.d.kh) / 2, b = o.d.pad_w + (KW - o.d.kw) / 2;
+    if (ph < 0) { ph = a; pw = b; }
+    if (a != ph || b != pw) return false;
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------- finalize
+
+static void resolve_buffers(ios_graph *g) {
+  // every root tensor (unit output or concat with no parent) owns a buffer
+  std::function<void(int)> place = [&](int t) {
+    Tensor &T = g->tensors[t];
+    if (T.buf >= 0) return;
+    if (T.kind == T_INPUT) {
+      Buffer b;
+      b.ctot = T.c; b.h = T.h; b.w = T.w; b.input_index = T.input_index;
+      g->bufs.push_back(b);
+      T.buf = (int)g->bufs.size() - 1;
+      T.coff = 0;
+    } else if (T.kind == T_IDENTITY) {
+      int s = g->ops[T.op].in[0];
+      place(s);
+      T.buf = g->tensors[s].buf;
+      T.coff = g->tensors[s].coff;
+    } else if (T.parent >= 0) {
+      place(T.parent);
+      T.buf = g->tensors[T.parent].buf;
+      T.coff = g->tensors[T.parent].coff + T.parent_off;
+    } else {
+      Buffer b;
+      b.ctot = T.c; b.h = T.h; b.w = T.w;
+      g->bufs.push_back(b);
+      T.buf = (int)g->bufs.size() - 1;
+      T.coff = 0;
+    }
+  };
+  for (int t = 0; t < (int)g->tensors.size(); ++t) place(t);
+  for (int k = 0; k < (int)g->outputs.size(); ++k) {
+    int t = resolve_identity(g, g->outputs[k]);
+    g->bufs[g->tensors[t].buf].output_index = k;
+  }
+}
+
+static int round_up(int a, int b) { return (a + b - 1) / b * b; }
+
+// Packed conv weights: [kh*kw][CinP][Npad], k = tap * CinP + ci (tap-major),
+// zero for ci >= Cin and n >= Cout.
+static void pack_conv(const Op &op, std::vector<float> &wpk, std::vector<float> &bias) {
+  int taps = op.d.kh * op.d.kw, CinP = op.CinP, Npad = op.Npad;
+  wpk.assign((size_t)taps * CinP * Npad, 0.f);
+  for (int co = 0; co < op.d.cout; ++co)
+    for (int ci = 0; ci < op.cin; ++ci)
+      for (int t = 0; t < taps; ++t)
+        wpk[((size_t)t * CinP + ci) * Npad + co] = op.w[((size_t)co * op.cin + ci) * taps + t];
+  bias.assign(Npad, 0.f);
+  std::copy(op.b.begin(), op.b.end(), bias.begin());
+}
+
+template <class T>
+static T *upload(const std::vector<T> &v) {
+  T *p = nullptr;
+  hip_check(hipMalloc(&p, sizeof(T) * std::max<size_t>(v.size(), 1)), "hipMalloc(weights)");
+  hip_check(hipMemcpy(p, v.data(), sizeof(T) * v.size(), hipMemcpyHostToDevice), "hipMemcpy");
+  return p;
+}
+
+int choose_conv_tile(int64_t M, int N) {
+  int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
+  int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
+  if (t64 >= 512) return TC_64x64;
+  if (t32 >= 256) return TC_32x32_K4;
+  return TC_16x16_K4;
+}
+
+void finalize_graph(ios_graph *g) {
+  if (g->finalized) fail(IOS_E_STATE, "graph already finalized");
+  assign_blocks(g);
+  resolve_buffers(g);
+  for (const auto &b : g->bufs)
+    if (b.elems(g->batch) >= (size_t)1 << 31) fail(IOS_E_UNSUPPORTED, "tensor of 2^31 or more elements");
+  for (int oi : g->units) {
+    Op &op = g->ops[oi];
+    if (op.d.kind == IOS_CONV) {
+      op.CinP = round_up(op.cin, 4);
+      op.Npad = round_up(op.d.cout, 64);
+      op.tcfg = choose_conv_tile((int64_t)g->batch * op.ho * op.wo, op.d.cout);
+    } else if (op.d.kind == IOS_SEPCONV) {
+      op.CinP = round_up(op.cin, 4);
+      op.Npad = round_up(op.d.cout, 16);
+    }
+  }
+  g->cost_table.assign(g->blocks.size(), {});
+  g->finalized = true;
+}
+
+// Device side of a finalized graph, set up on the first call that needs the
+// GPU: activation buffers (zero-filled), packed weights, stream, events.
+void ensure_device(ios_graph *g) {
+  if (!g->finalized) fail(IOS_E_STATE, "graph not finalized");
+  if (g->device_ready) {
+    hip_check(hipSetDevice(g->device), "hipSetDevice");
+    return;
+  }
+  hip_check(hipGetDevice(&g->device), "hipGetDevice");
+  hip_check(hipStreamCreateWithFlags(&g->stream, hipStreamNonBlocking), "hipStreamCreate");
+  hip_check(hipEventCreate(&g->ev0), "hipEventCreate");
+  hip_check(hipEventCreate(&g->ev1), "hipEventCreate");
+  hip_check(hipMalloc(&g->d_err, sizeof(int32_t)), "hipMalloc(err)");
+  hip_check(hipMemset(g->d_err, 0, sizeof(int32_t)), "hipMemset");
+  for (auto &b : g->bufs) {
+    size_t n = b.elems(g->batch);
+    hip_check(hipMalloc(&b.dev, sizeof(float) * n), "hipMalloc(activation)");
+    hip_check(hipMemset(b.dev, 0, sizeof(float) * n), "hipMemset");
+  }
+  for (int oi : g->units) {
+    Op &op = g->ops[oi];
+    if (op.d.kind == IOS_CONV) {
+      std::vector<float> wpk, bias;
+      pack_conv(op, wpk, bias);
+      op.d_wpk = upload(wpk);
+      op.d_bias = upload(bias);
+    } else if (op.d.kind == IOS_SEPCONV) {
+      int taps = op.d.kh * op.d.kw;
+      std::vector<float> dw(op.w.begin(), op.w.begin() + (size_t)op.cin * taps);
+      std::vector<float> pw((size_t)op.CinP * op.Npad, 0.f);
+      const float *src = op.w.data() + (size_t)op.cin * taps;
+      for (int co = 0; co < op.d.cout; ++co)
+        for (int ci = 0; ci < op.cin; ++ci) pw[(size_t)ci * op.Npad + co] = src[(size_t)co * op.cin + ci];
+      std::vector<float> bias(op.Npad, 0.f);
+      std::copy(op.b.begin(), op.b.end(), bias.begin());
+      op.d_dw = upload(dw);
+      op.d_wpk = upload(pw);
+      op.d_bias = upload(bias);
+    }
+  }
+  hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  g->device_ready = true;
+}
+
+}  // namespace ios

@@ -1,0 +1,230 @@
+// Internal data structures of libios shared by the host sources and the
+// stage kernel.  Nothing here is part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <memory>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/ios.h"
+
+namespace ios {
+
+constexpr int kMaxIn = 16;        // inputs of one operator
+constexpr int kMaxRoutes = 8;     // destinations of one (merged) conv: s <= 8 ops
+constexpr int kMaxDeps = 16;      // in-stage producers one operator waits for
+constexpr int kMaxSlots = 64;     // distinct buffers touched by one stage
+constexpr int kThreads = 256;     // threads per workgroup (4 wave64)
+constexpr int kMaxUnitsPerBlock = 64;
+constexpr int kMaxChannels = 256; // SEPCONV channels (in and out) kept in LDS
+constexpr int64_t kInf = INT64_MAX;
+
+// Kinds of work a stage kernel tile can do.
+enum DevKind : int32_t {
+  DK_CONV = 0,      // implicit-GEMM conv on fp32 MFMA (also merged convs)
+  DK_SEP = 1,       // fused sum -> ReLU -> depthwise -> pointwise (MFMA)
+  DK_POOL_MAX = 2,
+  DK_POOL_AVG = 3,
+  DK_ADD = 4,
+  DK_MEAN = 5,
+};
+
+// Conv tile shapes.  A workgroup has 4 waves arranged WM x WN x WK; each
+// wave owns FM x FN blocks of 16x16 outputs and 1/WK of the reduction.
+enum TileCfg : int32_t {
+  TC_16x16_K4 = 0,   // FM1 FN1 WM1 WN1 WK4
+  TC_32x32_K4 = 1,   // FM2 FN2 WM1 WN1 WK4
+  TC_64x64 = 2,      // FM2 FN2 WM2 WN2 WK1
+  TC_32x64_K2 = 3,   // FM2 FN2 WM1 WN2 WK2
+  TC_COUNT = 4,
+};
+
+struct TileShape { int fm, fn, wm, wn, wk; };
+inline TileShape tile_shape(int cfg) {
+  switch (cfg) {
+    case TC_16x16_K4: return {1, 1, 1, 1, 4};
+    case TC_32x32_K4: return {2, 2, 1, 1, 4};
+    case TC_64x64: return {2, 2, 2, 2, 1};
+    default: return {2, 2, 1, 2, 2};
+  }
+}
+inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
+inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * s.wn; }
+
+// SEPCONV tile: 16 * kSepFM output pixels x every output channel.
+constexpr int kSepFM = 2;
+constexpr int kSepBM = 16 * kSepFM;
+// Elementwise tiles (pool / add / mean): outputs per workgroup.
+constexpr int kEltPerTile = 4 * kThreads;
+
+// One operator of a compiled stage, as the kernel sees it.
+struct DevOp {
+  int32_t kind, tcfg;
+  int32_t n_in;
+  int32_t in_slot[kMaxIn], in_coff[kMaxIn], in_ctot[kMaxIn];
+  int32_t N, Cin, H, W;        // input (batch, channels, height, width)
+  int32_t Cout, Ho, Wo;        // output
+  int32_t kh, kw, sh, sw, ph, pw;
+  int32_t pre_relu, post_relu;
+  int32_t CinP;                // Cin rounded up to 4 (reduction per tap)
+  int32_t Npad;                // row length of the packed weights
+  int32_t tiles_m, tiles_n, n_tiles;
+  int32_t n_routes;            // output column ranges -> destination buffers
+  int32_t route_n0[kMaxRoutes + 1];
+  int32_t route_slot[kMaxRoutes], route_coff[kMaxRoutes], route_ctot[kMaxRoutes];
+  int32_t n_deps;
+  int32_t dep[kMaxDeps];       // stage-local indices of ops this op waits for
+  int32_t signal;              // 1 if another op of the stage waits for this one
+  float inv_n;                 // MEAN: 1 / n_in
+  const float *wpk;            // CONV: [kh*kw][CinP][Npad]; SEP: pointwise [CinP][Npad]
+  const float *bias;           // [Npad]
+  const float *dw;             // SEP: depthwise [Cin][kh*kw]
+};
+
+struct Tile {
+  int32_t op;    // stage-local op index
+  int32_t idx;   // tile index inside the op
+};
+
+struct StageArgs {
+  float *slot[kMaxSlots];
+  const DevOp *ops;
+  const Tile *tiles;
+  int32_t *ctr;        // [0] ticket, [1] finished, [2 + i] tiles done of op i
+  int32_t *err;        // device error word
+  int32_t n_tiles;
+  int32_t n_ops;
+  int32_t use_ticket;  // 1 when some op waits for another op of the stage
+  int32_t spin_limit;  // polls before a dependency wait gives up
+};
+
+// Launch one stage (defined in the HIP translation unit).
+hipError_t launch_stage(const StageArgs &args, int lds_bytes, hipStream_t stream);
+// Dynamic LDS a tile of `op` needs.
+int op_lds_bytes(const DevOp &op);
+
+// ------------------------------------------------------------------ host IR
+
+enum TensorKind { T_INPUT = 0, T_UNIT = 1, T_CONCAT = 2, T_IDENTITY = 3 };
+
+struct Tensor {
+  int c = 0, h = 0, w = 0;
+  int kind = T_INPUT;
+  int op = -1;              // producing op (unit or view)
+  int parent = -1;          // concat tensor containing this one
+  int parent_off = 0;       // channel offset inside the parent
+  int input_index = -1;
+  // resolved at finalize
+  int buf = -1, coff = 0;
+};
+
+struct Buffer {
+  int ctot = 0, h = 0, w = 0;
+  int input_index = -1, output_index = -1;
+  float *dev = nullptr;     // graph-owned storage (dummy for inputs/outputs)
+  size_t elems(int batch) const { return (size_t)batch * ctot * h * w; }
+};
+
+struct Op {
+  ios_op_desc d{};
+  int out = -1;                  // output tensor id
+  std::vector<int> in;           // input tensor ids
+  std::vector<float> w, b;       // host copies of weights / bias
+  int unit = -1;                 // index among schedule units, -1 for views
+  int block = -1, local = -1;    // block and bit inside the block
+  int cin = 0, h = 0, wd = 0, ho = 0, wo = 0;
+  // device copies (units only)
+  int CinP = 0, Npad = 0, tcfg = TC_32x32_K4;
+  float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
+};
+
+struct Block {
+  std::vector<int> ops;          // op indices (units), ascending
+  std::vector<uint64_t> succ, pred;
+  uint64_t full() const { return ops.size() == 64 ? ~0ull : ((1ull << ops.size()) - 1); }
+};
+
+struct CompiledStage {
+  std::vector<DevOp> ops;
+  std::vector<Tile> tiles;
+  std::vector<int> slot_buf;     // slot -> buffer index
+  int lds_bytes = 0;
+  bool ticket = false;
+  // device copies (owned unless `scratch`)
+  DevOp *d_ops = nullptr;
+  Tile *d_tiles = nullptr;
+  int32_t *d_ctr = nullptr;
+  float *d_mw = nullptr, *d_mb = nullptr;   // merged weights / bias
+  bool owns = true;
+};
+
+struct CostRow { int64_t conc = kInf, merge = kInf; bool merge_measured = false; };
+
+}  // namespace ios
+
+struct ios_graph {
+  int batch = 1;
+  bool finalized = false;
+  bool device_ready = false;      // buffers / weights / stream allocated
+  std::vector<ios::Tensor> tensors;
+  std::vector<ios::Buffer> bufs;
+  std::vector<ios::Op> ops;
+  std::vector<int> inputs;       // tensor ids
+  std::vector<int> outputs;      // tensor ids
+  std::vector<int> units;        // op indices that are schedule units
+  std::vector<ios::Block> blocks;
+  hipStream_t stream = nullptr;  // library stream for profiling
+  int device = 0;
+  int32_t *d_err = nullptr;
+  // profiling scratch (reused by every candidate stage)
+  ios::CompiledStage scratch;
+  size_t scratch_ops_cap = 0, scratch_tiles_cap = 0, scratch_ctr_cap = 0, scratch_w_cap = 0,
+         scratch_b_cap = 0;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  // last search's cost table, per block: mask -> latencies
+  std::vector<std::map<uint64_t, ios::CostRow>> cost_table;
+};
+
+struct ios_schedule_t {
+  ios_graph *g = nullptr;
+  std::vector<int32_t> offsets, unit_ids, strategies;
+  std::vector<int> stage_block;
+  int64_t states = 0, transitions = 0, measured = 0;
+  std::vector<std::unique_ptr<ios::CompiledStage>> compiled;
+  std::vector<hipEvent_t> events;
+};
+
+namespace ios {
+
+// Errors: thrown inside the library, turned into codes at the ABI.
+struct Error {
+  int code;
+  std::string msg;
+};
+[[noreturn]] void fail(int code, const std::string &msg);
+void hip_check(hipError_t e, const char *what);
+
+// graph.cpp
+int unit_op_of_tensor(const ios_graph *g, int tensor_id);   // op index or throws
+std::vector<int> unit_producers(const ios_graph *g, int tensor_id);
+void finalize_graph(ios_graph *g);
+void ensure_device(ios_graph *g);
+bool stage_mergeable(const ios_graph *g, const std::vector<int> &ops);
+int64_t op_flops(const ios_graph *g, const Op &op);
+
+// exec.cpp
+void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
+                   bool scratch);
+void free_stage(CompiledStage *cs);
+void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
+                     hipStream_t stream);
+int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,
+                      int reps, int repeats);
+std::vector<float *> default_buffers(const ios_graph *g);
+
+}  // namespace ios

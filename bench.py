@@ -1,0 +1,276 @@
+"""Benchmark: batch-1 latency of an IOS-scheduled multi-branch CNN block on
+one MI355X, with per-stage achieved fp32 TFLOP/s against the MFMA peak.
+
+One *step* is one ``ios_run`` of the whole block (every stage of the
+schedule found by Algorithm 1 with on-device profiling) on inputs already
+resident in HBM.  Default workload: the Inception-V3 mixed block
+(192x35x35 -> 256x35x35), batch 1, seed 0.
+
+Printed as one JSON line (rank 0, N = 1 only):
+  value        median-free mean latency of the timed steps, in microseconds
+  roofline     the stage kernel: algorithmic MFMA FLOPs per launch / its mean
+               launch duration (HIP events on the launch stream), vs the
+               fp32 MFMA peak
+  baselines    the same kernels under the sequential (one unit per launch)
+               and greedy schedules, timed the same way
+  cpu_baseline the oracle (plain fp64 C loops, one thread) on the host
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_TFLOPS = 157.3          # MI355X dense fp32 MFMA (256 CU x 2.4 GHz x 256 flop/clk)
+PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCES = ["paper_2011_01302_amd/csrc/stage_kernel.hip", "paper_2011_01302_amd/csrc/exec.cpp",
+                  "paper_2011_01302_amd/csrc/ios_internal.h"]
+
+
+def kernel_sha() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+# ------------------------------------------------------------------ algorithmic work
+
+def unit_work(spec, batch):
+    """Per unit: (MFMA flops, VALU flops, weight bytes) — algorithmic, i.e.
+    2 x MAC of the operator as defined, no padding of merged kernels."""
+    import workloads as W
+    shp = W.infer_shapes(spec)
+    out = {}
+    for op in W.unit_ops(spec):
+        c, h, w = shp[op["in"][0]]
+        co, ho, wo = shp[op["name"]]
+        px = batch * ho * wo
+        k = op["kind"]
+        if k == "conv":
+            out[op["name"]] = (2 * px * co * c * op["kh"] * op["kw"], 0, 4 * (co * c * op["kh"] * op["kw"] + co))
+        elif k == "sepconv":
+            out[op["name"]] = (2 * px * co * c, 2 * px * c * op["kh"] * op["kw"] + px * c * (len(op["in"]) - 1),
+                               4 * (c * op["kh"] * op["kw"] + co * c + co))
+        elif k in ("maxpool", "avgpool"):
+            out[op["name"]] = (0, px * co * op["kh"] * op["kw"], 0)
+        else:
+            out[op["name"]] = (0, px * co * len(op["in"]), 0)
+    return out
+
+
+def stage_bytes(spec, batch, names):
+    """Compulsory HBM bytes of a stage: inputs from outside it read once,
+    every unit output written once, weights read once."""
+    import workloads as W
+    shp = W.infer_shapes(spec)
+    units = {op["name"]: op for op in W.unit_ops(spec)}
+    views = {op["name"]: op for op in spec["ops"] if op["kind"] in ("concat", "identity")}
+
+    def sources(t):
+        if t in views:
+            s = []
+            for i in views[t]["in"]:
+                s += sources(i)
+            return s
+        return [t]
+    ext = set()
+    for n in names:
+        for t in units[n]["in"]:
+            for s in sources(t):
+                if s not in names:
+                    ext.add(s)
+    by = sum(4 * batch * shp[t][0] * shp[t][1] * shp[t][2] for t in ext)
+    by += sum(4 * batch * shp[n][0] * shp[n][1] * shp[n][2] for n in names)
+    return by
+
+
+# ------------------------------------------------------------------ timing
+
+def time_steps(I, g, q, ins, outs, stream, warmup, steps, torch):
+    ip = [t.data_ptr() for t in ins]
+    op = [t.data_ptr() for t in outs]
+    for _ in range(warmup):
+        I.ios_run(g.handle, q, ip, op, stream)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    s = torch.cuda.current_stream()
+    e0.record(s)
+    for _ in range(steps):
+        I.ios_run(g.handle, q, ip, op, stream)
+    e1.record(s)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps          # us per step
+
+
+def stage_times(I, g, q, ins, outs, stream, reps):
+    """Per-stage GPU ns (median over reps) from HIP events recorded around
+    each stage launch on the launch stream."""
+    ip = [t.data_ptr() for t in ins]
+    op = [t.data_ptr() for t in outs]
+    n = len(I.ios_schedule_get(q))
+    rows = [I.ios_run_timed(g.handle, q, ip, op, stream, n) for _ in range(reps)]
+    return [statistics.median(r[k] for r in rows) for k in range(n)], rows
+
+
+def cpu_oracle(spec, ten, budget_s):
+    from oracle import evaluator as E
+    E.build()
+    E.outputs(spec, ten)                                 # warm (loads the library)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        E.outputs(spec, ten)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 50:
+            break
+    return el / n * 1e6, n
+
+
+def load_traffic(workload, sha):
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("kernel_sha") != sha:
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="inception")
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--r", type=int, default=3)
+    ap.add_argument("--s", type=int, default=8)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-baselines", action="store_true")
+    ap.add_argument("--report", default="", help="also write the full report (JSON) here")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the stage executor runs on a single MI355X and this "
+              "build has no multi-GPU path (batch sharding is a design note only).", file=sys.stderr)
+        sys.exit(2)
+
+    lib = os.path.join(ROOT, "paper_2011_01302_amd", "libios.so")
+    if not os.path.exists(lib):
+        import __graft_entry__
+        __graft_entry__._load_build_module().build()
+    import numpy as np
+    import torch
+
+    import paper_2011_01302_amd as I
+    import workloads as W
+
+    print(f"[bench] config={args.config} batch={args.batch} seed={args.seed}", file=sys.stderr, flush=True)
+    spec, ten = W.make(args.config, args.batch, args.seed)
+    dev = "cuda:0"
+    g = I.Graph(spec, ten)
+    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(dev) for t in spec["inputs"]]
+    shp = W.infer_shapes(spec)
+    outs = [torch.empty((args.batch,) + shp[o], device=dev) for o in spec["outputs"]]
+    stream = torch.cuda.current_stream().cuda_stream
+
+    # Algorithm 1 with on-device stage profiling
+    opts = I.ios_sched_opts_default()
+    opts.r, opts.s = args.r, args.s
+    t0 = time.perf_counter()
+    q, pred_ns = I.ios_schedule(g.handle, opts)
+    search_s = time.perf_counter() - t0
+    states, transitions, measured = I.ios_schedule_stats(q)
+    stages = I.ios_schedule_get(q)
+    print(f"[bench] search {search_s:.2f}s, {len(stages)} stages, predicted {pred_ns} ns",
+          file=sys.stderr, flush=True)
+
+    us = time_steps(I, g, q, ins, outs, stream, args.warmup, args.steps, torch)
+    assert I.ios_device_status(g.handle, stream) == 0
+    print(f"[bench] IOS {us:.2f} us/step", file=sys.stderr, flush=True)
+
+    # per-stage roofline on the stage kernel
+    work = unit_work(spec, args.batch)
+    st_ns, _ = stage_times(I, g, q, ins, outs, stream, max(20, min(args.steps, 100)))
+    stage_rows = []
+    tot_mfma = tot_valu = tot_bytes = 0
+    for (ids, strat), ns in zip(stages, st_ns):
+        names = g.names(ids)
+        f_m = sum(work[n][0] for n in names)
+        f_v = sum(work[n][1] for n in names)
+        by = stage_bytes(spec, args.batch, set(names)) + sum(work[n][2] for n in names)
+        tot_mfma += f_m
+        tot_valu += f_v
+        tot_bytes += by
+        t_roof = max(f_m / (PEAK_FP32_TFLOPS * 1e12), f_v / (PEAK_FP32_TFLOPS * 1e12),
+                     by / (PEAK_HBM_GBS * 1e9)) * 1e9
+        stage_rows.append({"units": names, "strategy": "merge" if strat else "concurrent",
+                           "ns": ns, "mfma_flop": f_m, "valu_flop": f_v, "bytes": by,
+                           "tflops": f_m / ns / 1e3 if ns else None,
+                           "frac_of_roofline": t_roof / ns if ns else None})
+    kern_ns = sum(st_ns)
+    n_launch = len(stages)
+    achieved = (tot_mfma / n_launch) / (kern_ns / n_launch) / 1e3     # TFLOP/s
+    sha = kernel_sha()
+    traffic = load_traffic(f"{args.config}_bs{args.batch}", sha)
+
+    result = {
+        "metric": "batch-1 network latency (us) + achieved fp32 TFLOP/s per stage vs MFMA peak",
+        "value": round(us, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(us / 1e3, 6), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{args.config} block (seeded synthetic, random-init weights)",
+                   "batch": args.batch, "seed": args.seed, "pruning": {"r": args.r, "s": args.s},
+                   "parallelism": "single GPU, inter-operator (IOS stages)"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 4), "peak": PEAK_FP32_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 5),
+                     "traffic": traffic, "kernel": "ios_stage_kernel",
+                     "mean_launch_ns": round(kern_ns / n_launch, 1),
+                     "mfma_flop_per_launch": tot_mfma / n_launch, "kernel_sha": sha},
+        "schedule": stage_rows,
+        "search": {"seconds": round(search_s, 3), "states": states, "transitions": transitions,
+                   "stages_measured": measured, "predicted_ns": pred_ns},
+        "throughput_img_per_s": round(args.batch / us * 1e6, 1),
+    }
+    if not args.no_baselines:
+        base = {}
+        for name, mode in (("sequential", I.IOS_SCHED_SEQUENTIAL), ("greedy", I.IOS_SCHED_GREEDY)):
+            o = I.ios_sched_opts_default()
+            o.mode = mode
+            qb, _ = I.ios_schedule(g.handle, o)
+            ub = time_steps(I, g, qb, ins, outs, stream, args.warmup, args.steps, torch)
+            base[name] = {"us": round(ub, 3), "launches": len(I.ios_schedule_get(qb)),
+                          "speedup_of_ios": round(ub / us, 3)}
+            I.ios_schedule_destroy(qb)
+            print(f"[bench] {name} {ub:.2f} us/step", file=sys.stderr, flush=True)
+        result["gpu_baselines"] = base
+    if not args.no_cpu:
+        cpu_us, n = cpu_oracle(spec, ten, args.cpu_seconds)
+        result["cpu_baseline"] = {"value": round(cpu_us, 1), "unit": "us", "cores": 1, "kind": "oracle",
+                                  "sample": f"{n} full evaluations of the {args.config} block at batch "
+                                            f"{args.batch} (fp64 direct loops, single thread)"}
+        print(f"[bench] cpu oracle {cpu_us:.0f} us/eval", file=sys.stderr, flush=True)
+    I.ios_schedule_destroy(q)
+    g.close()
+    line = json.dumps(result)
+    if args.report:
+        with open(args.report, "w") as f:
+            f.write(line + "\n")
+    print(line, flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -6,7 +6,7 @@ Every function below has the name of the C entry point it wraps (see
 search and every kernel run inside ``libios.so``.  PyTorch is used by callers
 for device memory and streams only.
 
-The library must have been built (``python -m paper_2011_01302_amd.build``);
+The library must have been built (``python paper_2011_01302_amd/build.py``);
 importing this package fails loudly when it is missing.
 """
 from __future__ import annotations
@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libios.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2011_01302_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2011_01302_amd/build.py`")
 
 _lib = ctypes.CDLL(LIB_PATH)
 

@@ -1,6 +1,6 @@
 """Build libios.so (host C++ + gfx950 HIP kernels) in-tree with hipcc.
 
-    python -m paper_2011_01302_amd.build
+    python paper_2011_01302_amd/build.py
 
 Objects go to ``_build/`` at the repository root; the shared library is
 written next to this file so that it travels with the source tree.

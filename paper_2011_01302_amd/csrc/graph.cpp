@@ -2,6 +2,7 @@
 // copies of weights (Sec. 3 "Computation Graph"; Sec. 4.2 block-wise
 // optimisation).
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <functional>
 
@@ -360,7 +361,14 @@ static T *upload(const std::vector<T> &v) {
   return p;
 }
 
+// Conv tile shape for an M x N output.  IOS_CONV_TILE=<0..3> in the
+// environment (read when a graph is finalized or a merged stage is built)
+// forces one shape for every conv, for tuning and for tests.
 int choose_conv_tile(int64_t M, int N) {
+  if (const char *e = std::getenv("IOS_CONV_TILE")) {
+    int v = std::atoi(e);
+    if (v >= 0 && v < TC_COUNT) return v;
+  }
   int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
   int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
   if (t64 >= 512) return TC_64x64;

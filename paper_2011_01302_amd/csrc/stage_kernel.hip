@@ -282,6 +282,10 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
   } else {
     t = blockIdx.x;
   }
+  if (t >= a.n_tiles) {   // only if the counters were not left at zero
+    if (tid == 0) __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
   const Tile tile = a.tiles[t];
   const int opi = __builtin_amdgcn_readfirstlane(tile.op);
   const int ti = __builtin_amdgcn_readfirstlane(tile.idx);

@@ -1,0 +1,296 @@
+"""GPU parity: the library's stage kernels against the fp64 oracle, through
+the C ABI, on the seeded workloads.  Activations must satisfy
+max|gpu - oracle| / max|oracle| <= 1e-4 per output tensor (fp32 path vs fp64
+reference); schedules found on the device must equal the oracle DP replayed
+on the dumped cost table, bit for bit."""
+import functools
+import json
+import os
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+torch = pytest.importorskip("torch")
+I = pytest.importorskip("paper_2011_01302_amd")
+from oracle import evaluator as E          # noqa: E402
+from oracle import schedule as O           # noqa: E402
+
+DEV = "cuda:0"
+
+
+@functools.lru_cache(maxsize=None)
+def case(config, batch=1, seed=0):
+    spec, ten = W.make(config, batch, seed)
+    return spec, ten
+
+
+@functools.lru_cache(maxsize=None)
+def reference(config, batch=1, seed=0):
+    spec, ten = case(config, batch, seed)
+    return E.outputs(spec, ten)
+
+
+def run(g, q, spec, ten, stream=0):
+    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(DEV) for t in spec["inputs"]]
+    shp = W.infer_shapes(spec)
+    outs = [torch.full((g.batch,) + shp[o], float("nan"), device=DEV) for o in spec["outputs"]]
+    I.ios_run(g.handle, q, [t.data_ptr() for t in ins], [o.data_ptr() for o in outs], stream)
+    torch.cuda.synchronize()
+    assert I.ios_device_status(g.handle, stream) == 0
+    return [o.cpu().numpy() for o in outs]
+
+
+def rel_err(got, ref):
+    return float(np.abs(got.astype(np.float64) - ref).max() / np.abs(ref).max())
+
+
+def check(outs, refs, what=""):
+    for got, ref in zip(outs, refs):
+        assert got.shape == ref.shape
+        assert np.isfinite(got).all(), what
+        e = rel_err(got, ref)
+        assert e <= TOL, f"{what}: relative error {e:.3e}"
+
+
+def sched(g, mode, cost=lambda b, m, ids, t: 1000):
+    o = I.ios_sched_opts_default()
+    o.mode = mode
+    q, _ = I.ios_schedule(g.handle, o, cost)
+    return q
+
+
+def block_stages(g):
+    """One concurrent stage holding a whole block (chains run inside it)."""
+    blocks = g.blocks()
+    return I.ios_schedule_from_stages(g.handle, blocks, [I.IOS_CONCURRENT] * len(blocks))
+
+
+@pytest.fixture(autouse=True)
+def _print_case(request):
+    print(f"\n[gpu-case] {request.node.name}", flush=True)
+    yield
+
+
+# ------------------------------------------------------------------ schedules x configs
+
+@pytest.mark.parametrize("config", W.CONFIG_NAMES)
+@pytest.mark.parametrize("kind", ["sequential", "greedy", "block_stage"])
+def test_parity_schedules(config, kind):
+    spec, ten = case(config)
+    g = I.Graph(spec, ten)
+    if kind == "sequential":
+        q = sched(g, I.IOS_SCHED_SEQUENTIAL)
+    elif kind == "greedy":
+        q = sched(g, I.IOS_SCHED_GREEDY)
+    else:
+        q = block_stages(g)
+    check(run(g, q, spec, ten), reference(config), f"{config}/{kind}")
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+def merge_schedule(g, spec, groups):
+    """Stages: each listed group (names) as a merge stage, every other unit
+    alone, in a valid order."""
+    names = [u["name"] for u in W.unit_ops(spec)]
+    grouped = {n for grp in groups for n in grp}
+    stages, strat, done = [], [], set()
+    for n in names:
+        if n in done:
+            continue
+        grp = next((gr for gr in groups if n in gr), None)
+        if grp:
+            stages.append([g.tid[x] for x in grp])
+            strat.append(I.IOS_MERGE)
+            done |= set(grp)
+        elif n not in grouped:
+            stages.append([g.tid[n]])
+            strat.append(I.IOS_CONCURRENT)
+            done.add(n)
+    return I.ios_schedule_from_stages(g.handle, stages, strat)
+
+
+@pytest.mark.parametrize("config,groups", [
+    ("tiny", [["A", "B1"]]),
+    ("inception", [["b1", "b2a", "b3a"]]),
+    ("inception", [["b1", "b3a"]]),
+    ("squeeze", [[f"m{m}e1", f"m{m}e3"] for m in range(1, 9)]),
+])
+def test_parity_operator_merge(config, groups):
+    spec, ten = case(config)
+    g = I.Graph(spec, ten)
+    q = merge_schedule(g, spec, groups)
+    check(run(g, q, spec, ten), reference(config), f"{config}/merge")
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3"])
+def test_parity_every_conv_tile_shape(tile, monkeypatch):
+    monkeypatch.setenv("IOS_CONV_TILE", tile)
+    for config in ["tiny", "inception", "squeeze"]:
+        spec, ten = case(config)
+        g = I.Graph(spec, ten)
+        q = sched(g, I.IOS_SCHED_GREEDY)
+        check(run(g, q, spec, ten), reference(config), f"{config}/tile{tile}")
+        I.ios_schedule_destroy(q)
+        q = merge_schedule(g, spec, [["A", "B1"]] if config == "tiny" else
+                           [["b1", "b2a", "b3a"]] if config == "inception" else
+                           [[f"m{m}e1", f"m{m}e3"] for m in range(1, 9)])
+        check(run(g, q, spec, ten), reference(config), f"{config}/merge/tile{tile}")
+        I.ios_schedule_destroy(q)
+        g.close()
+
+
+@pytest.mark.parametrize("config,seed", [("randwire", 1), ("nasnet", 1), ("nasnet", 2)])
+def test_parity_other_seeds(config, seed):
+    spec, ten = case(config, 1, seed)
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), reference(config, 1, seed), f"{config}/seed{seed}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
+# ------------------------------------------------------------------ DP on the device
+
+@pytest.mark.parametrize("config", ["tiny", "inception", "squeeze"])
+def test_device_dp_schedule_replays_in_oracle(config, tmp_path):
+    spec, ten = case(config)
+    g = I.Graph(spec, ten)
+    o = I.ios_sched_opts_default()
+    o.warmup, o.reps, o.repeats = 2, 5, 3
+    q, cost = I.ios_schedule(g.handle, o)
+    assert cost > 0
+    check(run(g, q, spec, ten), reference(config), f"{config}/dp")
+    path = tmp_path / "costs.jsonl"
+    I.ios_schedule_dump_costs(g.handle, str(path))
+    table = {}
+    for line in open(path):
+        r = json.loads(line)
+        table[(r["block"], r["mask"], 0)] = r["concurrent_ns"]
+        if r["merge_ns"] is not None:
+            table[(r["block"], r["mask"], 1)] = r["merge_ns"]
+    total, stages = 0, []
+    for b, blk in enumerate(O.blocks_of(spec)):
+        res = O.ios_dp(blk, lambda m, t: table[(b, m, t)], 3, 8)
+        total += res.cost
+        stages += [(sorted(blk.units[i]["name"] for i in O.bits(m)), t) for m, t in res.schedule]
+    lib = [(sorted(g.names(ids)), t) for ids, t in I.ios_schedule_get(q)]
+    assert lib == stages
+    assert total == cost
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+def test_profile_stage_and_errors():
+    spec, ten = case("inception")
+    g = I.Graph(spec, ten)
+    for u in W.unit_ops(spec):
+        assert I.ios_profile_stage(g.handle, [g.tid[u["name"]]], 0, 1, 3, 1) > 0
+    ids = [g.tid[n] for n in ("b1", "b2a", "b3a")]
+    assert I.ios_profile_stage(g.handle, ids, I.IOS_MERGE, 1, 3, 1) > 0
+    with pytest.raises(I.IosError) as e:
+        I.ios_profile_stage(g.handle, [g.tid["b1"], g.tid["b4"]], I.IOS_MERGE)
+    assert e.value.name == "IOS_E_NOT_MERGEABLE"
+    g.close()
+
+
+def test_run_timed_and_determinism():
+    spec, ten = case("inception")
+    g = I.Graph(spec, ten)
+    q = block_stages(g)
+    a = run(g, q, spec, ten)
+    b = run(g, q, spec, ten)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    ins = [torch.from_numpy(ten["x"]).to(DEV)]
+    out = torch.empty((1, 256, 35, 35), device=DEV)
+    ns = I.ios_run_timed(g.handle, q, [ins[0].data_ptr()], [out.data_ptr()])
+    assert len(ns) == 1 and ns[0] > 0
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+# ------------------------------------------------------------------ batches
+
+def sample_images(config, batch, images):
+    spec, ten = case(config, batch)
+    refs = {}
+    for i in images:
+        s1 = W.with_batch(spec, 1)
+        t1 = dict(ten)
+        for t in spec["inputs"]:
+            t1[t["name"]] = ten[t["name"]][i:i + 1]
+        refs[i] = E.outputs(s1, t1)
+    return spec, ten, refs
+
+
+@pytest.mark.parametrize("config,batch", [("inception", 16), ("squeeze", 32), ("nasnet", 4)])
+def test_parity_batched_sampled_images(config, batch):
+    spec, ten, refs = sample_images(config, batch, [0, batch - 1])
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY)):
+        outs = run(g, q, spec, ten)
+        for i, ref in refs.items():
+            check([o[i:i + 1] for o in outs], ref, f"{config}/bs{batch}/img{i}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
+def test_parity_batched_full_small():
+    spec, ten = case("inception", 3)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    q = block_stages(g)
+    check(run(g, q, spec, ten), ref, "inception/bs3")
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+# ------------------------------------------------------------------ ragged shapes
+
+def ragged_spec(batch):
+    conv = lambda n, i, co, k, s, p, post=1: {"name": n, "kind": "conv", "in": [i], "cout": co,
+                                             "kh": k[0], "kw": k[1], "sh": s, "sw": s, "ph": p[0],
+                                             "pw": p[1], "pre_relu": 0, "post_relu": post}
+    ops = [conv("c1", "x", 20, (3, 3), 1, (1, 1)),
+           conv("c2", "x", 7, (5, 5), 1, (2, 2)),
+           conv("c3", "x", 9, (3, 1), 1, (1, 0)),
+           conv("c4", "x", 5, (1, 3), 1, (0, 1)),
+           conv("c5", "x", 11, (3, 3), 2, (1, 1), post=0),
+           {"name": "s1", "kind": "sepconv", "in": ["c1", "c1"], "cout": 21, "kh": 3, "kw": 3,
+            "sh": 1, "sw": 1, "ph": 1, "pw": 1, "pre_relu": 1, "post_relu": 0},
+           {"name": "s2", "kind": "sepconv", "in": ["s1"], "cout": 13, "kh": 5, "kw": 5,
+            "sh": 1, "sw": 1, "ph": 2, "pw": 2, "pre_relu": 1, "post_relu": 0},
+           {"name": "mp", "kind": "maxpool", "in": ["x"], "kh": 3, "kw": 3, "sh": 2, "sw": 2,
+            "ph": 1, "pw": 1},
+           {"name": "ap", "kind": "avgpool", "in": ["s2"], "kh": 3, "kw": 3, "sh": 1, "sw": 1,
+            "ph": 1, "pw": 1},
+           {"name": "ad", "kind": "add", "in": ["ap", "s2", "s2"]},
+           {"name": "mn", "kind": "mean", "in": ["c2", "c2", "c2"]},
+           {"name": "cat", "kind": "concat", "in": ["c3", "c4"]},
+           {"name": "cat2", "kind": "concat", "in": ["c5", "mp"]}]
+    return {"name": "ragged", "batch": batch, "inputs": [{"name": "x", "c": 13, "h": 9, "w": 11}],
+            "ops": ops, "outputs": ["ad", "mn", "cat", "cat2"]}
+
+
+@pytest.mark.parametrize("batch", [1, 2])
+def test_parity_ragged_shapes(batch):
+    spec = ragged_spec(batch)
+    ten = W.make_tensors(spec, 3)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g),
+              I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in ("c1", "c2", "c3", "c4")],
+                                                    [g.tid[n] for n in ("c5", "s1", "s2", "mp", "ap",
+                                                                        "ad", "mn")]],
+                                         [I.IOS_MERGE, I.IOS_CONCURRENT])):
+        check(run(g, q, spec, ten), ref, "ragged")
+        I.ios_schedule_destroy(q)
+    g.close()

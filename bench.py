@@ -162,6 +162,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-baselines", action="store_true")
     ap.add_argument("--report", default="", help="also write the full report (JSON) here")
+    ap.add_argument("--dump-costs", default="", help="write the search's stage-latency table here")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the stage executor runs on a single MI355X and this "
@@ -194,6 +195,8 @@ def main():
     q, pred_ns = I.ios_schedule(g.handle, opts)
     search_s = time.perf_counter() - t0
     states, transitions, measured = I.ios_schedule_stats(q)
+    if args.dump_costs:
+        I.ios_schedule_dump_costs(g.handle, args.dump_costs)
     stages = I.ios_schedule_get(q)
     print(f"[bench] search {search_s:.2f}s, {len(stages)} stages, predicted {pred_ns} ns",
           file=sys.stderr, flush=True)

@@ -82,7 +82,6 @@ void ios_graph_destroy(ios_graph *g) {
   }
   CompiledStage &s = g->scratch;
   if (s.d_ops) hipFree(s.d_ops);
-  if (s.d_tiles) hipFree(s.d_tiles);
   if (s.d_ctr) hipFree(s.d_ctr);
   if (s.d_mw) hipFree(s.d_mw);
   if (s.d_mb) hipFree(s.d_mb);

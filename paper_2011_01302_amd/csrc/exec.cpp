@@ -14,6 +14,7 @@
 // GenerateStage measures a stage by launching it repeatedly between HIP
 // events (Sec. 4.1).
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <numeric>
 
@@ -110,11 +111,10 @@ void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool scratch) {
 void free_stage(CompiledStage *cs) {
   if (!cs->owns) return;
   if (cs->d_ops) hipFree(cs->d_ops);
-  if (cs->d_tiles) hipFree(cs->d_tiles);
   if (cs->d_ctr) hipFree(cs->d_ctr);
   if (cs->d_mw) hipFree(cs->d_mw);
   if (cs->d_mb) hipFree(cs->d_mb);
-  cs->d_ops = nullptr; cs->d_tiles = nullptr; cs->d_ctr = nullptr;
+  cs->d_ops = nullptr; cs->d_ctr = nullptr;
   cs->d_mw = nullptr; cs->d_mb = nullptr;
 }
 
@@ -148,7 +148,12 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.Cout = total;
     d.CinP = round_up(o0.cin, 4);
     d.Npad = round_up(total, 64);
-    d.tcfg = choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total);
+    // tile shape: forced one, else the measured choice of the largest conv
+    int largest = ops[0];
+    for (int i : ops)
+      if (op_flops(g, g->ops[i]) > op_flops(g, g->ops[largest])) largest = i;
+    d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total)
+                                           : g->ops[largest].tcfg;
     set_inputs(g, o0, d, sm);
     // packed [KH*KW][CinP][Npad]: each op's taps placed centred
     mw.assign((size_t)KH * KW * d.CinP * d.Npad, 0.f);
@@ -232,8 +237,10 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     }
     d.n_tiles = d.tiles_m * d.tiles_n;
   }
-  // tile order: producers before consumers (depth), longer tiles first
+  // tile order: producers before consumers (depth), longer tiles first; the
+  // ops are stored in that order so that each owns a contiguous tile range
   int n = (int)dops.size();
+  if (n > kMaxStageOps) fail(IOS_E_UNSUPPORTED, "more than 64 operators in one stage");
   std::vector<int> depth(n, 0);
   for (int i = 0; i < n; ++i)
     for (int k = 0; k < dops[i].n_deps; ++k) depth[i] = std::max(depth[i], depth[dops[i].dep[k]] + 1);
@@ -243,19 +250,27 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     if (depth[a] != depth[b]) return depth[a] < depth[b];
     return tile_work(dops[a]) > tile_work(dops[b]);
   });
-  std::vector<Tile> tiles;
-  bool ticket = false;
+  std::vector<int> pos(n);
+  for (int i = 0; i < n; ++i) pos[order[i]] = i;
+  std::vector<DevOp> sorted;
+  std::vector<int32_t> start{0};
+  bool ticket = false, light = true;
   int lds = 0;
   for (int i : order) {
-    for (int t = 0; t < dops[i].n_tiles; ++t) tiles.push_back(Tile{i, t});
-    ticket |= dops[i].n_deps > 0;
-    lds = std::max(lds, op_lds_bytes(dops[i]));
+    DevOp d = dops[i];
+    for (int k = 0; k < d.n_deps; ++k) d.dep[k] = pos[d.dep[k]];
+    sorted.push_back(d);
+    start.push_back(start.back() + d.n_tiles);
+    ticket |= d.n_deps > 0;
+    light &= d.kind != DK_CONV || d.tcfg == TC_16x16_K8;
+    lds = std::max(lds, op_lds_bytes(d));
   }
-  cs->ops = dops;
-  cs->tiles = tiles;
+  cs->ops = sorted;
+  cs->op_start = start;
   cs->slot_buf = sm.bufs;
   cs->lds_bytes = lds;
   cs->ticket = ticket;
+  cs->light = light;
   cs->owns = !scratch;
   // device copies
   if (!mw.empty()) {
@@ -266,9 +281,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     cs->ops[0].wpk = cs->d_mw;
     cs->ops[0].bias = cs->d_mb;
   }
-  size_t d0 = 0, d1 = 0, d2 = 0;
+  size_t d0 = 0, d2 = 0;
   grow_upload(&cs->d_ops, scratch ? &g->scratch_ops_cap : &d0, cs->ops, scratch);
-  grow_upload(&cs->d_tiles, scratch ? &g->scratch_tiles_cap : &d1, cs->tiles, scratch);
   std::vector<int32_t> ctr(2 + n, 0);
   grow_upload(&cs->d_ctr, scratch ? &g->scratch_ctr_cap : &d2, ctr, scratch);
 }
@@ -278,14 +292,14 @@ void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<fl
   StageArgs a{};
   for (size_t i = 0; i < cs.slot_buf.size(); ++i) a.slot[i] = buf_ptr[cs.slot_buf[i]];
   a.ops = cs.d_ops;
-  a.tiles = cs.d_tiles;
+  for (size_t i = 0; i < cs.op_start.size(); ++i) a.op_start[i] = cs.op_start[i];
   a.ctr = cs.d_ctr;
   a.err = g->d_err;
-  a.n_tiles = (int)cs.tiles.size();
+  a.n_tiles = cs.op_start.back();
   a.n_ops = (int)cs.ops.size();
   a.use_ticket = cs.ticket ? 1 : 0;
   a.spin_limit = 1 << 24;
-  hip_check(launch_stage(a, cs.lds_bytes, stream), "stage launch");
+  hip_check(launch_stage(a, cs.lds_bytes, cs.light, stream), "stage launch");
 }
 
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,

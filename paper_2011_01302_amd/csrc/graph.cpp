@@ -371,9 +371,10 @@ int choose_conv_tile(int64_t M, int N) {
   }
   int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
   int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
-  if (t64 >= 512) return TC_64x64;
-  if (t32 >= 256) return TC_32x32_K4;
-  return TC_16x16_K4;
+  if (t64 >= 2048) return TC_128x64;
+  if (t64 >= 512) return TC_64x64_K2;
+  if (t32 >= 256) return TC_32x32_K8;
+  return TC_16x16_K8;
 }
 
 void finalize_graph(ios_graph *g) {
@@ -439,6 +440,22 @@ void ensure_device(ios_graph *g) {
   }
   hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
   g->device_ready = true;
+  // Tile shape of every conv, chosen by measuring the conv alone with each
+  // shape (unless IOS_CONV_TILE forces one).
+  if (!std::getenv("IOS_CONV_TILE")) {
+    for (int oi : g->units) {
+      Op &op = g->ops[oi];
+      if (op.d.kind != IOS_CONV) continue;
+      int best = op.tcfg;
+      int64_t best_ns = INT64_MAX;
+      for (int cfg = 0; cfg < TC_COUNT; ++cfg) {
+        op.tcfg = cfg;
+        int64_t ns = profile_stage(g, {oi}, IOS_CONCURRENT, 2, 10, 3);
+        if (ns < best_ns) { best_ns = ns; best = cfg; }
+      }
+      op.tcfg = best;
+    }
+  }
 }
 
 }  // namespace ios

@@ -19,7 +19,9 @@ constexpr int kMaxIn = 16;        // inputs of one operator
 constexpr int kMaxRoutes = 8;     // destinations of one (merged) conv: s <= 8 ops
 constexpr int kMaxDeps = 16;      // in-stage producers one operator waits for
 constexpr int kMaxSlots = 64;     // distinct buffers touched by one stage
-constexpr int kThreads = 256;     // threads per workgroup (4 wave64)
+constexpr int kThreads = 512;     // threads per workgroup (8 wave64)
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxStageOps = 64;  // operators of one stage (a block holds at most 64 units)
 constexpr int kMaxUnitsPerBlock = 64;
 constexpr int kMaxChannels = 256; // SEPCONV channels (in and out) kept in LDS
 constexpr int64_t kInf = INT64_MAX;
@@ -34,23 +36,25 @@ enum DevKind : int32_t {
   DK_MEAN = 5,
 };
 
-// Conv tile shapes.  A workgroup has 4 waves arranged WM x WN x WK; each
+// Conv tile shapes.  A workgroup has 8 waves arranged WM x WN x WK; each
 // wave owns FM x FN blocks of 16x16 outputs and 1/WK of the reduction.
 enum TileCfg : int32_t {
-  TC_16x16_K4 = 0,   // FM1 FN1 WM1 WN1 WK4
-  TC_32x32_K4 = 1,   // FM2 FN2 WM1 WN1 WK4
-  TC_64x64 = 2,      // FM2 FN2 WM2 WN2 WK1
-  TC_32x64_K2 = 3,   // FM2 FN2 WM1 WN2 WK2
-  TC_COUNT = 4,
+  TC_16x16_K8 = 0,   // FM1 FN1 WM1 WN1 WK8
+  TC_32x32_K8 = 1,   // FM2 FN2 WM1 WN1 WK8
+  TC_32x64_K4 = 2,   // FM2 FN2 WM1 WN2 WK4
+  TC_64x64_K2 = 3,   // FM2 FN2 WM2 WN2 WK2
+  TC_128x64 = 4,     // FM2 FN2 WM4 WN2 WK1
+  TC_COUNT = 5,
 };
 
 struct TileShape { int fm, fn, wm, wn, wk; };
 inline TileShape tile_shape(int cfg) {
   switch (cfg) {
-    case TC_16x16_K4: return {1, 1, 1, 1, 4};
-    case TC_32x32_K4: return {2, 2, 1, 1, 4};
-    case TC_64x64: return {2, 2, 2, 2, 1};
-    default: return {2, 2, 1, 2, 2};
+    case TC_16x16_K8: return {1, 1, 1, 1, 8};
+    case TC_32x32_K8: return {2, 2, 1, 1, 8};
+    case TC_32x64_K4: return {2, 2, 1, 2, 4};
+    case TC_64x64_K2: return {2, 2, 2, 2, 2};
+    default: return {2, 2, 4, 2, 1};
   }
 }
 inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
@@ -86,15 +90,10 @@ struct DevOp {
   const float *dw;             // SEP: depthwise [Cin][kh*kw]
 };
 
-struct Tile {
-  int32_t op;    // stage-local op index
-  int32_t idx;   // tile index inside the op
-};
-
 struct StageArgs {
   float *slot[kMaxSlots];
-  const DevOp *ops;
-  const Tile *tiles;
+  const DevOp *ops;    // in tile order: op i owns tiles [op_start[i], op_start[i+1])
+  int32_t op_start[kMaxStageOps + 1];
   int32_t *ctr;        // [0] ticket, [1] finished, [2 + i] tiles done of op i
   int32_t *err;        // device error word
   int32_t n_tiles;
@@ -104,7 +103,8 @@ struct StageArgs {
 };
 
 // Launch one stage (defined in the HIP translation unit).
-hipError_t launch_stage(const StageArgs &args, int lds_bytes, hipStream_t stream);
+// `light`: every conv of the stage uses the 16x16 tile (smaller register file).
+hipError_t launch_stage(const StageArgs &args, int lds_bytes, bool light, hipStream_t stream);
 // Dynamic LDS a tile of `op` needs.
 int op_lds_bytes(const DevOp &op);
 
@@ -139,7 +139,7 @@ struct Op {
   int block = -1, local = -1;    // block and bit inside the block
   int cin = 0, h = 0, wd = 0, ho = 0, wo = 0;
   // device copies (units only)
-  int CinP = 0, Npad = 0, tcfg = TC_32x32_K4;
+  int CinP = 0, Npad = 0, tcfg = TC_32x32_K8;
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
 };
 
@@ -150,14 +150,14 @@ struct Block {
 };
 
 struct CompiledStage {
-  std::vector<DevOp> ops;
-  std::vector<Tile> tiles;
+  std::vector<DevOp> ops;        // in tile order (producers before consumers)
+  std::vector<int32_t> op_start; // tile ranges, size ops + 1
   std::vector<int> slot_buf;     // slot -> buffer index
   int lds_bytes = 0;
   bool ticket = false;
+  bool light = true;             // every conv uses the 16x16 tile
   // device copies (owned unless `scratch`)
   DevOp *d_ops = nullptr;
-  Tile *d_tiles = nullptr;
   int32_t *d_ctr = nullptr;
   float *d_mw = nullptr, *d_mb = nullptr;   // merged weights / bias
   bool owns = true;
@@ -183,8 +183,7 @@ struct ios_graph {
   int32_t *d_err = nullptr;
   // profiling scratch (reused by every candidate stage)
   ios::CompiledStage scratch;
-  size_t scratch_ops_cap = 0, scratch_tiles_cap = 0, scratch_ctr_cap = 0, scratch_w_cap = 0,
-         scratch_b_cap = 0;
+  size_t scratch_ops_cap = 0, scratch_ctr_cap = 0, scratch_w_cap = 0, scratch_b_cap = 0;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   // last search's cost table, per block: mask -> latencies
   std::vector<std::map<uint64_t, ios::CostRow>> cost_table;

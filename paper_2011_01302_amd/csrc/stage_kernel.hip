@@ -1,9 +1,10 @@
 // The stage kernel: one launch executes every operator of one schedule stage
-// (Sec. 3, "Stage" and "Parallelization Strategy").  Each workgroup (256
-// threads = 4 wave64) runs one tile from the stage's tile table:
+// (Sec. 3, "Stage" and "Parallelization Strategy").  Each workgroup (512
+// threads = 8 wave64) runs one tile; the stage's operators are stored in tile
+// order and each owns a contiguous range of workgroup (tile) indices:
 //   DK_CONV   implicit-GEMM convolution, M = output pixels, N = output
 //             channels, K = taps x input channels (tap-major), on
-//             v_mfma_f32_16x16x4_f32; the 4 waves split M, N and/or K and
+//             v_mfma_f32_16x16x4_f32; the 8 waves split M, N and/or K and
 //             reduce their partial sums through LDS; bias + ReLU are applied
 //             in the epilogue, which writes each output channel to its
 //             destination (a merged conv has several destinations).
@@ -23,10 +24,33 @@ namespace ios {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+// s_waitcnt operand with vmcnt = 0 and the other counters at their maxima
+// (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] in [15:14])
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 __device__ __forceinline__ floatx4 mfma16x16x4(float a, float b, floatx4 c) {
   // D[16x16] += A[16x4] * B[4x16]; lane l supplies A[l%16][l/16] and
   // B[l/16][l%16]; lane l, element j holds D[4*(l/16)+j][l%16].
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Pointers into the global address space (plain pointers are generic and
+// would make the compiler emit flat loads).
+typedef __attribute__((address_space(1))) const float gcfloat;
+__device__ __forceinline__ gcfloat *gp(const float *p) { return (gcfloat *)p; }
+
+// Activation accesses.  COH = true for outputs consumed by another tile of
+// the same launch: agent-coherent (sc1) stores, performed beyond the
+// XCD-private caches, so no L2 writeback is needed before signalling.
+template <bool COH>
+__device__ __forceinline__ float ld(const float *p) {
+  if constexpr (COH) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else return *p;
+}
+template <bool COH>
+__device__ __forceinline__ void st(float *p, float v) {
+  if constexpr (COH) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else *p = v;
 }
 
 __device__ __forceinline__ float *route_ptr(const StageArgs &a, const DevOp &op, int n, int img,
@@ -39,8 +63,8 @@ __device__ __forceinline__ float *route_ptr(const StageArgs &a, const DevOp &op,
 
 // ------------------------------------------------------------------ conv
 
-template <int FM, int FN, int WM, int WN, int WK>
-__device__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
+template <int FM, int FN, int WM, int WN, int WK, bool COH>
+__device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN * WN, LDM = BM + 1;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wk = wave % WK, wmn = wave / WK, wm = wmn % WM, wn = wmn / WM;
@@ -49,6 +73,15 @@ __device__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds
   const int H = op.H, W = op.W, HW = H * W;
   const int row16 = lane & 15, kq = lane >> 4;
   const float *__restrict__ xin = a.slot[op.in_slot[0]];
+
+  // epilogue outputs of this thread; their biases are loaded up front
+  constexpr int EPT = (BM * BN + kThreads - 1) / kThreads;
+  float bpre[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    int idx = tid + e * kThreads, n = tn * BN + idx / BM;
+    bpre[e] = (idx < BM * BN && n < op.Cout) ? op.bias[n] : 0.f;
+  }
 
   int base[FM], ih0[FM], iw0[FM];
   bool mv[FM];
@@ -69,49 +102,93 @@ __device__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  // The reduction runs over chunks of U k-steps (4U input channels of one
+  // tap).  Chunks are split evenly over the WK waves; each wave keeps two
+  // or three chunks in registers, loading ahead while its MFMAs consume.
+  constexpr int U = (FM * FN == 1) ? 8 : 4;
   const int CinP = op.CinP, Cin = op.Cin, Npad = op.Npad, kw = op.kw;
   const int spt = CinP >> 2;                       // k-steps of 4 per tap
-  const int total = op.kh * kw * spt;
-  const int s0 = total * wk / WK, s1 = total * (wk + 1) / WK;
-  int tap = s0 / spt, ci = (s0 - tap * spt) * 4;
-  const float *__restrict__ wp =
-      op.wpk + (size_t)(tap * CinP + ci + kq) * Npad + tn * BN + wn * 16 * FN + row16;
+  const int cpt = (spt + U - 1) / U;               // chunks per tap
+  const int total = op.kh * kw * cpt;
+  const int c0 = total * wk / WK, c1 = total * (wk + 1) / WK;
+  gcfloat *__restrict__ xg = gp(xin);
+  gcfloat *__restrict__ wbase = gp(op.wpk) + tn * BN + wn * 16 * FN + row16;
   const bool relu_in = op.pre_relu != 0;
 
-  int aoff[FM];
-  bool aval[FM];
-  auto setup = [&](int tp) {
-    int u = tp / kw, v = tp - u * kw;
+  // chunks are loaded in order c0, c0+1, ...: walk (tap row u, tap col v,
+  // chunk-in-tap cc) incrementally instead of dividing
+  int it_tap = c0 / cpt, it_cc = c0 - (c0 / cpt) * cpt;
+  int it_u = it_tap / kw, it_v = it_tap - it_u * kw;
+
+  float a0[U][FM], b0[U][FN], a1[U][FM], b1[U][FN], a2[FM * FN == 1 ? U : 1][FM], b2[FM * FN == 1 ? U : 1][FN];
+  // Loads are unconditional, from an in-bounds address (offset 0 when the
+  // tap falls in the padding or the channel is past Cin), and the value is
+  // then replaced by 0: no branches around the loads.
+  auto load = [&](float (&A)[U][FM], float (&B)[U][FN]) {
+    int aoff[FM];
+    bool aval[FM];
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
-      int ih = ih0[fm] + u, iw = iw0[fm] + v;
+      int ih = ih0[fm] + it_u, iw = iw0[fm] + it_v;
       aval[fm] = mv[fm] && ih >= 0 && ih < H && iw >= 0 && iw < W;
-      aoff[fm] = aval[fm] ? base[fm] + ih * W + iw : 0;
+      aoff[fm] = base[fm] + ih * W + iw;
+    }
+    const int cb = it_cc * 4 * U + kq;
+    gcfloat *__restrict__ wrow = wbase + (size_t)(it_tap * CinP + cb) * Npad;
+#pragma unroll
+    for (int st_ = 0; st_ < U; ++st_) {
+      const int c = cb + 4 * st_;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const bool ok = aval[fm] && c < Cin;
+        float x = xg[ok ? aoff[fm] + c * HW : 0];
+        x = ok ? x : 0.f;
+        A[st_][fm] = relu_in ? fmaxf(x, 0.f) : x;
+      }
+      // rows past CinP would belong to the next tap: read row 0 of this
+      // chunk instead (finite weights times a zero activation)
+      const int roff = c < CinP ? 4 * st_ * Npad : 0;
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) B[st_][fn] = wrow[roff + fn * 16];
+    }
+    if (++it_cc == cpt) {
+      it_cc = 0;
+      ++it_tap;
+      if (++it_v == kw) { it_v = 0; ++it_u; }
     }
   };
-  setup(tap);
-
-  for (int s = s0; s < s1; ++s) {
-    const int c = ci + kq;
-    const bool cv = c < Cin;
-    float av[FM], bv[FN];
+  auto compute = [&](const float (&A)[U][FM], const float (&B)[U][FN]) {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      float x = (aval[fm] && cv) ? xin[aoff[fm] + c * HW] : 0.f;
-      av[fm] = relu_in ? fmaxf(x, 0.f) : x;
+    for (int st_ = 0; st_ < U; ++st_)
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          acc[fm][fn] = mfma16x16x4(A[st_][fm], B[st_][fn], acc[fm][fn]);
+  };
+  if constexpr (FM * FN == 1) {
+    // three chunks in flight
+    if (c0 < c1) load(a0, b0);
+    if (c0 + 1 < c1) load(a1, b1);
+    for (int ch = c0; ch < c1; ch += 3) {
+      if (ch + 2 < c1) load(a2, b2);
+      compute(a0, b0);
+      if (ch + 1 >= c1) break;
+      if (ch + 3 < c1) load(a0, b0);
+      compute(a1, b1);
+      if (ch + 2 >= c1) break;
+      if (ch + 4 < c1) load(a1, b1);
+      compute(a2, b2);
     }
-#pragma unroll
-    for (int fn = 0; fn < FN; ++fn) bv[fn] = wp[fn * 16];
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(av[fm], bv[fn], acc[fm][fn]);
-    wp += 4 * Npad;
-    ci += 4;
-    if (ci == CinP) {
-      ci = 0;
-      ++tap;
-      if (s + 1 < s1) setup(tap);
+  } else {
+    // two chunks in flight (larger tiles hold more accumulators)
+    if (c0 < c1) load(a0, b0);
+    for (int ch = c0; ch < c1; ch += 2) {
+      if (ch + 1 < c1) load(a1, b1);
+      compute(a0, b0);
+      if (ch + 1 >= c1) break;
+      if (ch + 2 < c1) load(a0, b0);
+      compute(a1, b1);
     }
   }
 
@@ -127,23 +204,26 @@ __device__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds
         lds[(wk * BN + col) * LDM + row] = acc[fm][fn][j];
       }
   __syncthreads();
-  for (int idx = tid; idx < BM * BN; idx += kThreads) {
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    int idx = tid + e * kThreads;
     int col = idx / BM, row = idx - col * BM;
     int m = tm * BM + row, n = tn * BN + col;
-    if (m >= M || n >= op.Cout) continue;
-    float v = op.bias[n];
+    if (idx >= BM * BN || m >= M || n >= op.Cout) continue;
+    float v = bpre[e];
 #pragma unroll
     for (int w = 0; w < WK; ++w) v += lds[(w * BN + col) * LDM + row];
     if (op.post_relu) v = fmaxf(v, 0.f);
     int img = m / howo, pix = m - img * howo;
-    *route_ptr(a, op, n, img, pix, howo) = v;
+    st<COH>(route_ptr(a, op, n, img, pix, howo), v);
   }
 }
 
 // ------------------------------------------------------------------ sepconv
 
-__device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
-  constexpr int BM = kSepBM, LDM = BM + 1, MAXJ = kMaxChannels / 64;
+template <bool COH>
+__device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
+  constexpr int BM = kSepBM, LDM = BM + 1, MAXJ = kMaxChannels / 16 / kWaves;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Wo = op.Wo, howo = op.Ho * Wo, M = op.N * howo;
   const int H = op.H, W = op.W, HW = H * W;
@@ -165,7 +245,7 @@ __device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds)
           if (iw < 0 || iw >= W) continue;
           float s = 0.f;
           for (int i = 0; i < n_in; ++i)
-            s += a.slot[op.in_slot[i]][(img * op.in_ctot[i] + op.in_coff[i] + c) * HW + ih * W + iw];
+            s += ld<false>(a.slot[op.in_slot[i]] + (img * op.in_ctot[i] + op.in_coff[i] + c) * HW + ih * W + iw);
           if (op.pre_relu) s = fmaxf(s, 0.f);
           v = fmaf(wdw[u * kw + q], s, v);
         }
@@ -175,7 +255,7 @@ __device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds)
   }
   __syncthreads();
 
-  // phase 2: pointwise 1x1 on MFMA; wave w owns 16-column blocks w, w+4, ...
+  // phase 2: pointwise 1x1 on MFMA; wave w owns 16-column blocks w, w+8, ...
   const int NB = op.Npad >> 4;
   const int row16 = lane & 15, kq = lane >> 4;
   floatx4 acc[kSepFM][MAXJ];
@@ -190,7 +270,7 @@ __device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds)
     const float *wrow = op.wpk + (size_t)(c0 + kq) * op.Npad + row16;
 #pragma unroll
     for (int j = 0; j < MAXJ; ++j) {
-      int nb = wave + 4 * j;
+      int nb = wave + kWaves * j;
       if (nb < NB) {
         float b = wrow[nb * 16];
 #pragma unroll
@@ -201,7 +281,7 @@ __device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds)
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < MAXJ; ++j) {
-    int nb = wave + 4 * j;
+    int nb = wave + kWaves * j;
     if (nb < NB) {
 #pragma unroll
       for (int fm = 0; fm < kSepFM; ++fm)
@@ -217,21 +297,23 @@ __device__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds)
     float v = lds[n * LDM + mm] + op.bias[n];
     if (op.post_relu) v = fmaxf(v, 0.f);
     int img = m / howo, pix = m - img * howo;
-    *route_ptr(a, op, n, img, pix, howo) = v;
+    st<COH>(route_ptr(a, op, n, img, pix, howo), v);
   }
 }
 
 // ------------------------------------------------------------------ elementwise
 
-__device__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_max) {
+template <bool COH>
+__device__ __forceinline__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_max) {
   const int howo = op.Ho * op.Wo, C = op.Cout, chw = C * howo;
   const int total = op.N * chw, HW = op.H * op.W;
   const float *__restrict__ xin = a.slot[op.in_slot[0]];
   float *__restrict__ out = a.slot[op.route_slot[0]];
   const float inv = 1.0f / (float)(op.kh * op.kw);
+#pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) {
     int idx = t * kEltPerTile + e * kThreads + threadIdx.x;
-    if (idx >= total) break;
+    if (idx >= total) continue;
     int img = idx / chw, r = idx - img * chw, c = r / howo, pix = r - c * howo;
     int oh = pix / op.Wo, ow = pix - oh * op.Wo;
     const float *x = xin + (size_t)(img * op.in_ctot[0] + op.in_coff[0] + c) * HW;
@@ -242,33 +324,62 @@ __device__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_ma
       for (int q = 0; q < op.kw; ++q) {
         int iw = ow * op.sw + q - op.pw;
         if (iw < 0 || iw >= op.W) continue;
-        float v = x[ih * op.W + iw];
+        float v = ld<false>(x + ih * op.W + iw);
         acc = is_max ? fmaxf(acc, v) : acc + v;
       }
     }
     if (!is_max) acc *= inv;
-    out[(size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * howo + pix] = acc;
+    st<COH>(out + (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * howo + pix, acc);
   }
 }
 
-__device__ void sum_tile(const StageArgs &a, const DevOp &op, int t, bool mean) {
+template <bool COH>
+__device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, int t, bool mean) {
   const int hw = op.Ho * op.Wo, C = op.Cout, chw = C * hw;
   const int total = op.N * chw;
   float *__restrict__ out = a.slot[op.route_slot[0]];
+#pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) {
     int idx = t * kEltPerTile + e * kThreads + threadIdx.x;
-    if (idx >= total) break;
+    if (idx >= total) continue;
     int img = idx / chw, r = idx - img * chw, c = r / hw, pix = r - c * hw;
     float s = 0.f;
     for (int i = 0; i < op.n_in; ++i)
-      s += a.slot[op.in_slot[i]][(size_t)(img * op.in_ctot[i] + op.in_coff[i] + c) * hw + pix];
+      s += ld<false>(a.slot[op.in_slot[i]] + (size_t)(img * op.in_ctot[i] + op.in_coff[i] + c) * hw + pix);
     if (mean) s *= op.inv_n;
-    out[(size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * hw + pix] = s;
+    st<COH>(out + (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * hw + pix, s);
   }
 }
 
 // ------------------------------------------------------------------ kernel
 
+// LIGHT kernels support only the 16x16 conv tile, which keeps register use
+// (and so occupancy) at the level of the small tiles.
+template <bool COH, bool LIGHT>
+__device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, int ti, float *lds) {
+  switch (op.kind) {
+    case DK_CONV:
+      if constexpr (LIGHT) {
+        conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds);
+        break;
+      }
+      switch (op.tcfg) {
+        case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds); break;
+        case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(a, op, ti, lds); break;
+        case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(a, op, ti, lds); break;
+        case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(a, op, ti, lds); break;
+        default: conv_tile<2, 2, 4, 2, 1, COH>(a, op, ti, lds); break;
+      }
+      break;
+    case DK_SEP: sep_tile<COH>(a, op, ti, lds); break;
+    case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true); break;
+    case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false); break;
+    case DK_ADD: sum_tile<COH>(a, op, ti, false); break;
+    default: sum_tile<COH>(a, op, ti, true); break;
+  }
+}
+
+template <bool LIGHT>
 __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
   extern __shared__ float lds[];
   __shared__ int s_ticket;
@@ -286,18 +397,21 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
     if (tid == 0) __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
-  const Tile tile = a.tiles[t];
-  const int opi = __builtin_amdgcn_readfirstlane(tile.op);
-  const int ti = __builtin_amdgcn_readfirstlane(tile.idx);
+  int opi = 0;
+  while (opi + 1 < a.n_ops && t >= a.op_start[opi + 1]) ++opi;
+  const int ti = t - a.op_start[opi];
   const DevOp &op = a.ops[opi];
 
   if (op.n_deps) {
+    // one thread polls the producers' counters with coherent loads, then
+    // invalidates stale cache lines once; the workgroup reads the
+    // producers' outputs only after that (barrier)
     if (tid == 0) {
       for (int k = 0; k < op.n_deps; ++k) {
         const int d = op.dep[k];
         const int need = a.ops[d].n_tiles;
         int spins = 0;
-        while (__hip_atomic_load(&a.ctr[2 + d], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < need) {
+        while (__hip_atomic_load(&a.ctr[2 + d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
           __builtin_amdgcn_s_sleep(2);
           if (++spins > a.spin_limit) {
             __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -305,35 +419,30 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
           }
         }
       }
+      // drop lines of this CU / XCD that may predate the producers' stores
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
 
-  switch (op.kind) {
-    case DK_CONV:
-      switch (op.tcfg) {
-        case TC_16x16_K4: conv_tile<1, 1, 1, 1, 4>(a, op, ti, lds); break;
-        case TC_32x32_K4: conv_tile<2, 2, 1, 1, 4>(a, op, ti, lds); break;
-        case TC_64x64: conv_tile<2, 2, 2, 2, 1>(a, op, ti, lds); break;
-        default: conv_tile<2, 2, 1, 2, 2>(a, op, ti, lds); break;
-      }
-      break;
-    case DK_SEP: sep_tile(a, op, ti, lds); break;
-    case DK_POOL_MAX: pool_tile(a, op, ti, true); break;
-    case DK_POOL_AVG: pool_tile(a, op, ti, false); break;
-    case DK_ADD: sum_tile(a, op, ti, false); break;
-    default: sum_tile(a, op, ti, true); break;
-  }
+  if (op.n_deps || op.signal) run_tile<true, LIGHT>(a, op, ti, lds);
+  else run_tile<false, LIGHT>(a, op, ti, lds);
 
   if (op.signal) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    // The tile's outputs were written with agent-coherent stores.  Every wave
+    // waits until its stores have been performed, then one thread moves the
+    // op's counter; a consumer reads the outputs only after seeing the final
+    // count and invalidating its stale lines, so it sees every value.  This
+    // orders like a release/acquire pair without a per-tile L2 writeback.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
-    if (tid == 0)
-      __hip_atomic_fetch_add(&a.ctr[2 + opi], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_fetch_add(&a.ctr[2 + opi], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (a.use_ticket && tid == 0) {
-    int f = __hip_atomic_fetch_add(&a.ctr[1], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    // relaxed: a workgroup's counter polls have returned before this
+    // increment is issued, so the reset below cannot overtake them (an
+    // agent-scope acq_rel here would cost an L2 writeback + invalidate)
+    int f = __hip_atomic_fetch_add(&a.ctr[1], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (f == a.n_tiles - 1) {
       // last tile of the launch: every other workgroup has passed its waits;
       // leave the counters at zero for the next launch on the stream
@@ -357,8 +466,11 @@ int op_lds_bytes(const DevOp &op) {
   return 0;
 }
 
-hipError_t launch_stage(const StageArgs &args, int lds_bytes, hipStream_t stream) {
-  hipLaunchKernelGGL(ios_stage_kernel, dim3(args.n_tiles), dim3(kThreads), lds_bytes, stream, args);
+hipError_t launch_stage(const StageArgs &args, int lds_bytes, bool light, hipStream_t stream) {
+  if (light)
+    hipLaunchKernelGGL(ios_stage_kernel<true>, dim3(args.n_tiles), dim3(kThreads), lds_bytes, stream, args);
+  else
+    hipLaunchKernelGGL(ios_stage_kernel<false>, dim3(args.n_tiles), dim3(kThreads), lds_bytes, stream, args);
   return hipGetLastError();
 }
 

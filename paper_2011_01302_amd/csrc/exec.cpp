@@ -58,6 +58,7 @@ void set_inputs(const ios_graph *g, const Op &op, DevOp &d, SlotMap &sm) {
     d.in_slot[i] = sm.get(t.buf);
     d.in_coff[i] = t.coff;
     d.in_ctot[i] = g->bufs[t.buf].ctot;
+    d.in_bytes[i] = (int32_t)(g->bufs[t.buf].elems(g->batch) * sizeof(float));
   }
 }
 
@@ -177,6 +178,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       n0 += o.d.cout;
     }
     d.route_n0[d.n_routes] = total;
+    d.w_bytes = (int32_t)(mw.size() * sizeof(float));
     dops.push_back(d);
   } else if (strategy == IOS_CONCURRENT) {
     for (size_t i = 0; i < ops.size(); ++i) {
@@ -192,6 +194,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
         case IOS_CONV:
           d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad;
           d.wpk = o.d_wpk; d.bias = o.d_bias;
+          d.w_bytes = (int32_t)((size_t)o.d.kh * o.d.kw * o.CinP * o.Npad * sizeof(float));
           break;
         case IOS_SEPCONV:
           d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
@@ -231,8 +234,19 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     } else if (d.kind == DK_SEP) {
       d.tiles_m = cdiv(M, kSepBM);
       d.tiles_n = 1;
+    } else if (d.kind == DK_POOL_MAX || d.kind == DK_POOL_AVG) {
+      // output rows per tile: as many as fit (with halo) in the LDS budget
+      int rows = d.Ho;
+      while (rows > 1 && ((rows - 1) * d.sh + d.kh) * d.W > kPoolLdsFloats) --rows;
+      if (((rows - 1) * d.sh + d.kh) * d.W > kPoolLdsFloats)
+        fail(IOS_E_UNSUPPORTED, "pooling input rows too wide for the LDS tile");
+      d.rows_per_tile = rows;
+      d.tiles_per_plane = cdiv(d.Ho, rows);
+      d.tiles_m = d.N * d.Cout * d.tiles_per_plane;
+      d.tiles_n = 1;
     } else {
-      d.tiles_m = cdiv(M * d.Cout, kEltPerTile);
+      d.tiles_per_plane = cdiv((int64_t)d.Ho * d.Wo, kEltPerTile);
+      d.tiles_m = d.N * d.Cout * d.tiles_per_plane;
       d.tiles_n = 1;
     }
     d.n_tiles = d.tiles_m * d.tiles_n;

@@ -382,7 +382,8 @@ void finalize_graph(ios_graph *g) {
   assign_blocks(g);
   resolve_buffers(g);
   for (const auto &b : g->bufs)
-    if (b.elems(g->batch) >= (size_t)1 << 31) fail(IOS_E_UNSUPPORTED, "tensor of 2^31 or more elements");
+    if (b.elems(g->batch) * sizeof(float) >= (size_t)1 << 30)
+      fail(IOS_E_UNSUPPORTED, "tensor of 1 GiB or more");
   for (int oi : g->units) {
     Op &op = g->ops[oi];
     if (op.d.kind == IOS_CONV) {

@@ -63,14 +63,18 @@ inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * 
 // SEPCONV tile: 16 * kSepFM output pixels x every output channel.
 constexpr int kSepFM = 2;
 constexpr int kSepBM = 16 * kSepFM;
-// Elementwise tiles (pool / add / mean): outputs per workgroup.
+// Elementwise tiles: add / mean handle up to kEltPerTile contiguous outputs of
+// one channel plane; a pool tile handles a band of output rows of one plane
+// whose input rows (with halo) fit in kPoolLdsFloats of LDS.
 constexpr int kEltPerTile = 4 * kThreads;
+constexpr int kPoolLdsFloats = 8192;
 
 // One operator of a compiled stage, as the kernel sees it.
 struct DevOp {
   int32_t kind, tcfg;
   int32_t n_in;
   int32_t in_slot[kMaxIn], in_coff[kMaxIn], in_ctot[kMaxIn];
+  int32_t in_bytes[kMaxIn];    // size of each input's buffer (buffer-load range)
   int32_t N, Cin, H, W;        // input (batch, channels, height, width)
   int32_t Cout, Ho, Wo;        // output
   int32_t kh, kw, sh, sw, ph, pw;
@@ -85,6 +89,9 @@ struct DevOp {
   int32_t dep[kMaxDeps];       // stage-local indices of ops this op waits for
   int32_t signal;              // 1 if another op of the stage waits for this one
   float inv_n;                 // MEAN: 1 / n_in
+  int32_t rows_per_tile;       // POOL: output rows per tile
+  int32_t tiles_per_plane;     // POOL / ADD / MEAN: tiles per (image, channel) plane
+  int32_t w_bytes;             // size of wpk in bytes
   const float *wpk;            // CONV: [kh*kw][CinP][Npad]; SEP: pointwise [CinP][Npad]
   const float *bias;           // [Npad]
   const float *dw;             // SEP: depthwise [Cin][kh*kw]

@@ -39,6 +39,21 @@ __device__ __forceinline__ floatx4 mfma16x16x4(float a, float b, floatx4 c) {
 typedef __attribute__((address_space(1))) const float gcfloat;
 __device__ __forceinline__ gcfloat *gp(const float *p) { return (gcfloat *)p; }
 
+// Raw buffer loads: SGPR resource + 32-bit VGPR offset + SGPR offset, no
+// 64-bit address arithmetic per load; an offset at or past the resource's
+// size returns 0 (used for padding taps).
+constexpr int kBufFlags = 0x00020000;   // gfx9 descriptor word 3 (32-bit data)
+// Buffers are smaller than 1 GiB, so an offset of 2^30 or more reads 0; the
+// two "out of range" offsets below can be added without wrapping past 2^32.
+constexpr int kOOB = 1 << 30;           // masked pixel / padding tap
+constexpr int kOOBStep = (int)(1u << 31);  // k-step past the end of a tap
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, bytes, kBufFlags);
+}
+__device__ __forceinline__ float bld(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
 // Activation accesses.  COH = true for outputs consumed by another tile of
 // the same launch: agent-coherent (sc1) stores, performed beyond the
 // XCD-private caches, so no L2 writeback is needed before signalling.
@@ -66,7 +81,8 @@ __device__ __forceinline__ float *route_ptr(const StageArgs &a, const DevOp &op,
 template <int FM, int FN, int WM, int WN, int WK, bool COH>
 __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN * WN, LDM = BM + 1;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
   const int wk = wave % WK, wmn = wave / WK, wm = wmn % WM, wn = wmn / WM;
   const int tm = t / op.tiles_n, tn = t - tm * op.tiles_n;
   const int Wo = op.Wo, howo = op.Ho * Wo, M = op.N * howo;
@@ -111,9 +127,13 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
   const int cpt = (spt + U - 1) / U;               // chunks per tap
   const int total = op.kh * kw * cpt;
   const int c0 = total * wk / WK, c1 = total * (wk + 1) / WK;
-  gcfloat *__restrict__ xg = gp(xin);
-  gcfloat *__restrict__ wbase = gp(op.wpk) + tn * BN + wn * 16 * FN + row16;
+  const __amdgpu_buffer_rsrc_t xr = rsrc(xin, op.in_bytes[0]);
+  const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
+  const int HW16 = HW * 16;                        // bytes between k-steps (4 channels)
+  const int NP16 = Npad * 16;                      // bytes between k-steps of weights
+  const int wcol = (tn * BN + wn * 16 * FN + row16) * 4;
   const bool relu_in = op.pre_relu != 0;
+  const bool full_c = Cin == CinP;
 
   // chunks are loaded in order c0, c0+1, ...: walk (tap row u, tap col v,
   // chunk-in-tap cc) incrementally instead of dividing
@@ -121,35 +141,41 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
   int it_u = it_tap / kw, it_v = it_tap - it_u * kw;
 
   float a0[U][FM], b0[U][FN], a1[U][FM], b1[U][FN], a2[FM * FN == 1 ? U : 1][FM], b2[FM * FN == 1 ? U : 1][FN];
-  // Loads are unconditional, from an in-bounds address (offset 0 when the
-  // tap falls in the padding or the channel is past Cin), and the value is
-  // then replaced by 0: no branches around the loads.
+  // Per chunk each lane computes one activation offset per M-block (out of
+  // range for padding taps and masked pixels, so the load returns 0) and one
+  // weight offset; the k-step goes in the scalar offset, the 16-column block
+  // in the immediate.  Steps past the tap's channels are skipped uniformly.
   auto load = [&](float (&A)[U][FM], float (&B)[U][FN]) {
-    int aoff[FM];
-    bool aval[FM];
+    const int cb = it_cc * 4 * U + kq;             // this lane's first channel
+    int voff[FM];
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm) {
       int ih = ih0[fm] + it_u, iw = iw0[fm] + it_v;
-      aval[fm] = mv[fm] && ih >= 0 && ih < H && iw >= 0 && iw < W;
-      aoff[fm] = base[fm] + ih * W + iw;
+      bool ok = mv[fm] && ih >= 0 && ih < H && iw >= 0 && iw < W;
+      voff[fm] = ok ? (base[fm] + ih * W + iw + cb * HW) * 4 : kOOB;
     }
-    const int cb = it_cc * 4 * U + kq;
-    gcfloat *__restrict__ wrow = wbase + (size_t)(it_tap * CinP + cb) * Npad;
+    const int wvoff = (it_tap * CinP + cb) * (Npad * 4) + wcol;
+    const int nval = min(U, spt - it_cc * U);      // k-steps of this chunk inside the tap
+    if (full_c) {
 #pragma unroll
-    for (int st_ = 0; st_ < U; ++st_) {
-      const int c = cb + 4 * st_;
+      for (int st_ = 0; st_ < U; ++st_) {
+        const int sa = st_ < nval ? st_ * HW16 : kOOBStep;   // uniform
+        const int sb = st_ < nval ? st_ * NP16 : 0;          // weights row: any valid one
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm) {
-        const bool ok = aval[fm] && c < Cin;
-        float x = xg[ok ? aoff[fm] + c * HW : 0];
-        x = ok ? x : 0.f;
-        A[st_][fm] = relu_in ? fmaxf(x, 0.f) : x;
+        for (int fm = 0; fm < FM; ++fm) A[st_][fm] = bld(xr, voff[fm] + sa, 0);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) B[st_][fn] = bld(wr, wvoff + fn * 64, sb);
       }
-      // rows past CinP would belong to the next tap: read row 0 of this
-      // chunk instead (finite weights times a zero activation)
-      const int roff = c < CinP ? 4 * st_ * Npad : 0;
+    } else {
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) B[st_][fn] = wrow[roff + fn * 16];
+      for (int st_ = 0; st_ < U; ++st_) {
+        const bool cok = st_ < nval && cb + 4 * st_ < Cin;
+        const int sb = st_ < nval ? st_ * NP16 : 0;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) A[st_][fm] = bld(xr, cok ? voff[fm] + st_ * HW16 : kOOB, 0);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) B[st_][fn] = bld(wr, wvoff + fn * 64, sb);
+      }
     }
     if (++it_cc == cpt) {
       it_cc = 0;
@@ -158,13 +184,23 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
     }
   };
   auto compute = [&](const float (&A)[U][FM], const float (&B)[U][FN]) {
+    if (relu_in) {
 #pragma unroll
-    for (int st_ = 0; st_ < U; ++st_)
+      for (int st_ = 0; st_ < U; ++st_)
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
+        for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn)
-          acc[fm][fn] = mfma16x16x4(A[st_][fm], B[st_][fn], acc[fm][fn]);
+          for (int fn = 0; fn < FN; ++fn)
+            acc[fm][fn] = mfma16x16x4(fmaxf(A[st_][fm], 0.f), B[st_][fn], acc[fm][fn]);
+    } else {
+#pragma unroll
+      for (int st_ = 0; st_ < U; ++st_)
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+            acc[fm][fn] = mfma16x16x4(A[st_][fm], B[st_][fn], acc[fm][fn]);
+    }
   };
   if constexpr (FM * FN == 1) {
     // three chunks in flight
@@ -224,7 +260,8 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
 template <bool COH>
 __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
   constexpr int BM = kSepBM, LDM = BM + 1, MAXJ = kMaxChannels / 16 / kWaves;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
   const int Wo = op.Wo, howo = op.Ho * Wo, M = op.N * howo;
   const int H = op.H, W = op.W, HW = H * W;
   const int CinP = op.CinP, Cin = op.Cin, kh = op.kh, kw = op.kw, taps = kh * kw;
@@ -303,51 +340,71 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
 
 // ------------------------------------------------------------------ elementwise
 
+// One band of output rows of one (image, channel) plane: the input rows it
+// needs are staged in LDS with coalesced loads (each input value is read from
+// memory once), then every output is reduced from LDS.
 template <bool COH>
-__device__ __forceinline__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_max) {
-  const int howo = op.Ho * op.Wo, C = op.Cout, chw = C * howo;
-  const int total = op.N * chw, HW = op.H * op.W;
-  const float *__restrict__ xin = a.slot[op.in_slot[0]];
-  float *__restrict__ out = a.slot[op.route_slot[0]];
+__device__ __forceinline__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_max,
+                                          float *lds) {
+  const int tid = threadIdx.x;
+  const int C = op.Cout, H = op.H, W = op.W, Ho = op.Ho, Wo = op.Wo;
+  const int plane = t / op.tiles_per_plane, band = t - plane * op.tiles_per_plane;
+  const int img = plane / C, c = plane - img * C;
+  const int oh0 = band * op.rows_per_tile, oh1 = min(Ho, oh0 + op.rows_per_tile);
+  const int ih_lo = max(0, oh0 * op.sh - op.ph);
+  const int ih_hi = min(H, (oh1 - 1) * op.sh - op.ph + op.kh);
+  const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[0]], op.in_bytes[0]);
+  const int src = ((img * op.in_ctot[0] + op.in_coff[0] + c) * H + ih_lo) * W;
+  const int n_in = (ih_hi - ih_lo) * W;
+  for (int i = tid; i < n_in; i += kThreads) lds[i] = bld(xr, (src + i) * 4, 0);
+  __syncthreads();
+  float *__restrict__ out = a.slot[op.route_slot[0]] +
+                            (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * Ho * Wo;
   const float inv = 1.0f / (float)(op.kh * op.kw);
-#pragma unroll
-  for (int e = 0; e < kEltPerTile / kThreads; ++e) {
-    int idx = t * kEltPerTile + e * kThreads + threadIdx.x;
-    if (idx >= total) continue;
-    int img = idx / chw, r = idx - img * chw, c = r / howo, pix = r - c * howo;
-    int oh = pix / op.Wo, ow = pix - oh * op.Wo;
-    const float *x = xin + (size_t)(img * op.in_ctot[0] + op.in_coff[0] + c) * HW;
+  const int n_out = (oh1 - oh0) * Wo;
+  for (int i = tid; i < n_out; i += kThreads) {
+    const int oh = oh0 + i / Wo, ow = i - (i / Wo) * Wo;
     float acc = is_max ? -INFINITY : 0.f;
     for (int u = 0; u < op.kh; ++u) {
-      int ih = oh * op.sh + u - op.ph;
-      if (ih < 0 || ih >= op.H) continue;
+      const int ih = oh * op.sh + u - op.ph;
+      if (ih < ih_lo || ih >= ih_hi) continue;     // outside the image
       for (int q = 0; q < op.kw; ++q) {
-        int iw = ow * op.sw + q - op.pw;
-        if (iw < 0 || iw >= op.W) continue;
-        float v = ld<false>(x + ih * op.W + iw);
+        const int iw = ow * op.sw + q - op.pw;
+        if (iw < 0 || iw >= W) continue;
+        const float v = lds[(ih - ih_lo) * W + iw];
         acc = is_max ? fmaxf(acc, v) : acc + v;
       }
     }
     if (!is_max) acc *= inv;
-    st<COH>(out + (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * howo + pix, acc);
+    st<COH>(out + oh * Wo + ow, acc);
   }
 }
 
+// Up to kEltPerTile contiguous outputs of one (image, channel) plane.
 template <bool COH>
 __device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, int t, bool mean) {
-  const int hw = op.Ho * op.Wo, C = op.Cout, chw = C * hw;
-  const int total = op.N * chw;
-  float *__restrict__ out = a.slot[op.route_slot[0]];
+  const int hw = op.Ho * op.Wo, C = op.Cout;
+  const int plane = t / op.tiles_per_plane, chunk = t - plane * op.tiles_per_plane;
+  const int img = plane / C, c = plane - img * C;
+  const int p0 = chunk * kEltPerTile;
+  float *__restrict__ out = a.slot[op.route_slot[0]] +
+                            (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * hw;
+  float s[kEltPerTile / kThreads];
+#pragma unroll
+  for (int e = 0; e < kEltPerTile / kThreads; ++e) s[e] = 0.f;
+  for (int i = 0; i < op.n_in; ++i) {
+    const __amdgpu_buffer_rsrc_t r = rsrc(a.slot[op.in_slot[i]], op.in_bytes[i]);
+    const int base = (img * op.in_ctot[i] + op.in_coff[i] + c) * hw;
+#pragma unroll
+    for (int e = 0; e < kEltPerTile / kThreads; ++e) {
+      const int pix = p0 + e * kThreads + threadIdx.x;
+      s[e] += bld(r, pix < hw ? (base + pix) * 4 : kOOB, 0);
+    }
+  }
 #pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) {
-    int idx = t * kEltPerTile + e * kThreads + threadIdx.x;
-    if (idx >= total) continue;
-    int img = idx / chw, r = idx - img * chw, c = r / hw, pix = r - c * hw;
-    float s = 0.f;
-    for (int i = 0; i < op.n_in; ++i)
-      s += ld<false>(a.slot[op.in_slot[i]] + (size_t)(img * op.in_ctot[i] + op.in_coff[i] + c) * hw + pix);
-    if (mean) s *= op.inv_n;
-    st<COH>(out + (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * hw + pix, s);
+    const int pix = p0 + e * kThreads + threadIdx.x;
+    if (pix < hw) st<COH>(out + pix, mean ? s[e] * op.inv_n : s[e]);
   }
 }
 
@@ -372,8 +429,8 @@ __device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, in
       }
       break;
     case DK_SEP: sep_tile<COH>(a, op, ti, lds); break;
-    case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true); break;
-    case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false); break;
+    case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true, lds); break;
+    case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false, lds); break;
     case DK_ADD: sum_tile<COH>(a, op, ti, false); break;
     default: sum_tile<COH>(a, op, ti, true); break;
   }
@@ -400,7 +457,10 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
   int opi = 0;
   while (opi + 1 < a.n_ops && t >= a.op_start[opi + 1]) ++opi;
   const int ti = t - a.op_start[opi];
-  const DevOp &op = a.ops[opi];
+  // read-only for the whole launch: constant address space, so its fields
+  // are scalar (uniform) loads
+  typedef __attribute__((address_space(4))) const DevOp cDevOp;
+  const DevOp &op = *(const DevOp *)&((cDevOp *)a.ops)[opi];
 
   if (op.n_deps) {
     // one thread polls the producers' counters with coherent loads, then
@@ -409,7 +469,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
     if (tid == 0) {
       for (int k = 0; k < op.n_deps; ++k) {
         const int d = op.dep[k];
-        const int need = a.ops[d].n_tiles;
+        const int need = ((cDevOp *)a.ops)[d].n_tiles;
         int spins = 0;
         while (__hip_atomic_load(&a.ctr[2 + d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
           __builtin_amdgcn_s_sleep(2);
@@ -463,6 +523,8 @@ int op_lds_bytes(const DevOp &op) {
     int c = op.CinP > op.Npad ? op.CinP : op.Npad;
     return c * (kSepBM + 1) * (int)sizeof(float);
   }
+  if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
+    return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
   return 0;
 }
 

@@ -297,7 +297,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   }
   size_t d0 = 0, d2 = 0;
   grow_upload(&cs->d_ops, scratch ? &g->scratch_ops_cap : &d0, cs->ops, scratch);
-  std::vector<int32_t> ctr(2 + n, 0);
+  std::vector<int32_t> ctr(2 + kCtrStride * kCtrCopies, 0);
   grow_upload(&cs->d_ctr, scratch ? &g->scratch_ctr_cap : &d2, ctr, scratch);
 }
 

@@ -22,6 +22,10 @@ constexpr int kMaxSlots = 64;     // distinct buffers touched by one stage
 constexpr int kThreads = 512;     // threads per workgroup (8 wave64)
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxStageOps = 64;  // operators of one stage (a block holds at most 64 units)
+// Each op's completion counter is kept in kCtrCopies copies kCtrStride ints
+// apart (different memory channels); a waiting workgroup polls one copy.
+constexpr int kCtrCopies = 32;
+constexpr int kCtrStride = 64;    // >= kMaxStageOps
 constexpr int kMaxUnitsPerBlock = 64;
 constexpr int kMaxChannels = 256; // SEPCONV channels (in and out) kept in LDS
 constexpr int64_t kInf = INT64_MAX;
@@ -101,7 +105,7 @@ struct StageArgs {
   float *slot[kMaxSlots];
   const DevOp *ops;    // in tile order: op i owns tiles [op_start[i], op_start[i+1])
   int32_t op_start[kMaxStageOps + 1];
-  int32_t *ctr;        // [0] ticket, [1] finished, [2 + i] tiles done of op i
+  int32_t *ctr;        // [0] ticket, [1] finished, [2 + i + kCtrStride * r] tiles done of op i (copy r)
   int32_t *err;        // device error word
   int32_t n_tiles;
   int32_t n_ops;

@@ -463,16 +463,18 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
   const DevOp &op = *(const DevOp *)&((cDevOp *)a.ops)[opi];
 
   if (op.n_deps) {
-    // one thread polls the producers' counters with coherent loads, then
-    // invalidates stale cache lines once; the workgroup reads the
-    // producers' outputs only after that (barrier)
+    // one thread polls the producers' counters with coherent loads (its own
+    // copy of each, so the pollers of a stage spread over kCtrCopies memory
+    // channels), then invalidates stale cache lines once; the workgroup
+    // reads the producers' outputs only after that (barrier)
     if (tid == 0) {
+      int32_t *mine = a.ctr + 2 + kCtrStride * (blockIdx.x % kCtrCopies);
       for (int k = 0; k < op.n_deps; ++k) {
         const int d = op.dep[k];
         const int need = ((cDevOp *)a.ops)[d].n_tiles;
         int spins = 0;
-        while (__hip_atomic_load(&a.ctr[2 + d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
-          __builtin_amdgcn_s_sleep(2);
+        while (__hip_atomic_load(&mine[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
+          __builtin_amdgcn_s_sleep(4);
           if (++spins > a.spin_limit) {
             __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             break;
@@ -490,13 +492,14 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
 
   if (op.signal) {
     // The tile's outputs were written with agent-coherent stores.  Every wave
-    // waits until its stores have been performed, then one thread moves the
-    // op's counter; a consumer reads the outputs only after seeing the final
+    // waits until its stores have been performed, then one wave moves every
+    // copy of the op's counter; a consumer reads the outputs only after seeing the final
     // count and invalidating its stale lines, so it sees every value.  This
     // orders like a release/acquire pair without a per-tile L2 writeback.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
-    if (tid == 0) __hip_atomic_fetch_add(&a.ctr[2 + opi], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid < kCtrCopies)
+      __hip_atomic_fetch_add(&a.ctr[2 + opi + kCtrStride * tid], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (a.use_ticket && tid == 0) {
     // relaxed: a workgroup's counter polls have returned before this
@@ -506,8 +509,9 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
     if (f == a.n_tiles - 1) {
       // last tile of the launch: every other workgroup has passed its waits;
       // leave the counters at zero for the next launch on the stream
-      for (int i = 0; i < a.n_ops; ++i)
-        __hip_atomic_store(&a.ctr[2 + i], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int r = 0; r < kCtrCopies; ++r)
+        for (int i = 0; i < a.n_ops; ++i)
+          __hip_atomic_store(&a.ctr[2 + i + kCtrStride * r], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctr[0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctr[1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

@@ -146,6 +146,45 @@ def load_traffic(workload, sha):
     return d.get("traffic_bytes_per_launch")
 
 
+def _pmc_rows(d, counter):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r.get("Counter_Name") == counter:
+                rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def write_traffic(args, fetch_dir, write_dir):
+    """HBM bytes per stage launch of the timed loop, from rocprofv3 --pmc
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what the
+    same counter reads for the plain copy of --copy-mb MiB at the end of the
+    run.  The timed loop is the last steps x stages stage-kernel dispatches
+    before that copy."""
+    res = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _pmc_rows(d, counter)
+        copy = [v for _, k, v in rows if "ios_stage_kernel" not in k][-1]
+        stage = [v for _, k, v in rows if "ios_stage_kernel" in k]
+        meta = json.load(open(os.path.join(d, "bench.json")))
+        n = meta["steps"] * meta["stages"]
+        timed = stage[-n:]
+        copy_bytes = meta["copy_mb"] << 20
+        scale = copy_bytes / (copy * 1024.0)
+        res[counter] = {"kib_per_launch_raw": sum(timed) / len(timed), "copy_kib_raw": copy,
+                        "scale": scale, "bytes_per_launch": sum(timed) / len(timed) * 1024.0 * scale}
+    out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": kernel_sha(),
+           "fetch": res["FETCH_SIZE"], "write": res["WRITE_SIZE"],
+           "traffic_bytes_per_launch": res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"]}
+    path = os.path.join(ROOT, "profiles", f"traffic_{args.config}_bs{args.batch}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -163,11 +202,22 @@ def main():
     ap.add_argument("--no-baselines", action="store_true")
     ap.add_argument("--report", default="", help="also write the full report (JSON) here")
     ap.add_argument("--dump-costs", default="", help="write the search's stage-latency table here")
+    ap.add_argument("--no-stage-times", action="store_true",
+                    help="skip the per-stage event pass (the timed loop is then the last launches)")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="finish with one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
+                         "into profiles/traffic_<workload>.json and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the stage executor runs on a single MI355X and this "
               "build has no multi-GPU path (batch sharding is a design note only).", file=sys.stderr)
         sys.exit(2)
+
+    if args.traffic_from:
+        write_traffic(args, *args.traffic_from)
+        return
 
     lib = os.path.join(ROOT, "paper_2011_01302_amd", "libios.so")
     if not os.path.exists(lib):
@@ -204,6 +254,16 @@ def main():
     us = time_steps(I, g, q, ins, outs, stream, args.warmup, args.steps, torch)
     assert I.ios_device_status(g.handle, stream) == 0
     print(f"[bench] IOS {us:.2f} us/step", file=sys.stderr, flush=True)
+
+    if args.no_stage_times:
+        if args.copy_mb:
+            src = torch.ones(args.copy_mb << 18, device=dev)
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+        print(json.dumps({"value": round(us, 3), "unit": "us", "stages": len(stages),
+                          "steps": args.steps, "copy_mb": args.copy_mb}), flush=True)
+        return
 
     # per-stage roofline on the stage kernel
     work = unit_work(spec, args.batch)

@@ -188,6 +188,36 @@ def test_device_dp_schedule_replays_in_oracle(config, tmp_path):
     g.close()
 
 
+@pytest.mark.parametrize("config", ["randwire", "nasnet"])
+def test_device_dp_large_blocks_replay_in_oracle(config, tmp_path):
+    """RandWire (33 units, ~31k candidate stages) and NASNet (17 units, ~56k):
+    the search runs on the device with light profiling; the schedule must be
+    the oracle's on the dumped table and the outputs must match."""
+    spec, ten = case(config)
+    g = I.Graph(spec, ten)
+    o = I.ios_sched_opts_default()
+    o.warmup, o.reps, o.repeats = 1, 2, 1
+    q, cost = I.ios_schedule(g.handle, o)
+    check(run(g, q, spec, ten), reference(config), f"{config}/dp")
+    path = tmp_path / "costs.jsonl"
+    I.ios_schedule_dump_costs(g.handle, str(path))
+    table = {}
+    for line in open(path):
+        r = json.loads(line)
+        table[(r["mask"], 0)] = r["concurrent_ns"]
+        if r["merge_ns"] is not None:
+            table[(r["mask"], 1)] = r["merge_ns"]
+    blk = O.blocks_of(spec)[0]
+    res = O.ios_dp(blk, lambda m, t: table[(m, t)], 3, 8)
+    lib = [(sorted(g.names(ids)), t) for ids, t in I.ios_schedule_get(q)]
+    assert lib == [(sorted(blk.units[i]["name"] for i in O.bits(m)), t) for m, t in res.schedule]
+    assert res.cost == cost
+    states, transitions, _ = I.ios_schedule_stats(q)
+    assert (states, transitions) == (res.states, res.transitions)
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_profile_stage_and_errors():
     spec, ten = case("inception")
     g = I.Graph(spec, ten)

@@ -185,6 +185,69 @@ def write_traffic(args, fetch_dir, write_dir):
     print(json.dumps(out))
 
 
+# NASNet at batch 32 is left out: its ~56k candidate stages at that batch take
+# longer to profile than a benchmark run should.
+SUITE = [("tiny", 1), ("inception", 1), ("inception", 16), ("randwire", 1), ("nasnet", 1),
+         ("squeeze", 1), ("squeeze", 32), ("squeeze", 128)]
+
+
+def run_suite(args):
+    """Every configuration and batch size of the benchmark list: the DP
+    schedule (on-device profiling), the sequential and greedy schedules, all
+    on the same kernels and timed the same way."""
+    import numpy as np
+    import torch
+
+    import paper_2011_01302_amd as I
+    import workloads as W
+    report = []
+    for config, batch in SUITE:
+        spec, ten = W.make(config, batch, args.seed)
+        g = I.Graph(spec, ten)
+        dev = "cuda:0"
+        ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(dev) for t in spec["inputs"]]
+        shp = W.infer_shapes(spec)
+        outs = [torch.empty((batch,) + shp[o], device=dev) for o in spec["outputs"]]
+        stream = torch.cuda.current_stream().cuda_stream
+        row = {"config": config, "batch": batch}
+        work = unit_work(spec, batch)
+        row["gflop"] = round(sum(w[0] + w[1] for w in work.values()) / 1e9, 4)
+        for name, mode in (("ios", I.IOS_SCHED_DP), ("sequential", I.IOS_SCHED_SEQUENTIAL),
+                           ("greedy", I.IOS_SCHED_GREEDY)):
+            o = I.ios_sched_opts_default()
+            o.mode = mode
+            if config in ("randwire", "nasnet"):      # tens of thousands of candidate stages
+                o.warmup, o.reps, o.repeats = 1, 3, 1
+            print(f"[suite] {config} bs{batch} {name}: scheduling", file=sys.stderr, flush=True)
+            t0 = time.perf_counter()
+            q, pred = I.ios_schedule(g.handle, o)
+            search = time.perf_counter() - t0
+            steps = max(20, min(args.steps, int(2e5 / max(1.0, row["gflop"] * 1e3))))
+            us = time_steps(I, g, q, ins, outs, stream, 10, steps, torch)
+            assert I.ios_device_status(g.handle, stream) == 0
+            sched = I.ios_schedule_get(q)
+            entry = {"us": round(us, 2), "stages": len(sched), "predicted_us": round(pred / 1e3, 2),
+                     "search_s": round(search, 2)}
+            if mode == I.IOS_SCHED_DP:
+                st, tr, ms = I.ios_schedule_stats(q)
+                entry.update({"states": st, "transitions": tr, "stages_measured": ms,
+                              "schedule": [(g.names(ids), "merge" if t else "concurrent") for ids, t in sched]})
+            row[name] = entry
+            I.ios_schedule_destroy(q)
+        row["speedup_vs_sequential"] = round(row["sequential"]["us"] / row["ios"]["us"], 3)
+        row["speedup_vs_greedy"] = round(row["greedy"]["us"] / row["ios"]["us"], 3)
+        row["tflops"] = round(row["gflop"] / row["ios"]["us"] * 1e3, 2)
+        print(f"[suite] {config:9s} bs{batch:<4d} IOS {row['ios']['us']:9.2f} us ({row['ios']['stages']} stages)"
+              f"  seq {row['sequential']['us']:9.2f}  greedy {row['greedy']['us']:9.2f}"
+              f"  x{row['speedup_vs_sequential']:.2f} vs seq  {row['tflops']} TFLOP/s", file=sys.stderr, flush=True)
+        report.append(row)
+        g.close()
+        del ins, outs
+        torch.cuda.empty_cache()
+    with open(args.suite, "w") as f:
+        json.dump(report, f, indent=1)
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -206,6 +269,9 @@ def main():
                     help="skip the per-stage event pass (the timed loop is then the last launches)")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="finish with one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--suite", default="",
+                    help="instead of the headline line, measure every configuration and batch "
+                         "(IOS vs sequential vs greedy) and write a JSON report to this path")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
                          "into profiles/traffic_<workload>.json and exit")
@@ -223,6 +289,9 @@ def main():
     if not os.path.exists(lib):
         import __graft_entry__
         __graft_entry__._load_build_module().build()
+    if args.suite:
+        run_suite(args)
+        return
     import numpy as np
     import torch
 

@@ -199,6 +199,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
         case IOS_SEPCONV:
           d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
           d.wpk = o.d_wpk; d.bias = o.d_bias; d.dw = o.d_dw;
+          d.w_bytes = (int32_t)((size_t)o.CinP * o.Npad * sizeof(float));
           break;
         case IOS_POOL_MAX: d.kind = DK_POOL_MAX; break;
         case IOS_POOL_AVG: d.kind = DK_POOL_AVG; break;
@@ -232,7 +233,16 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.tiles_m = cdiv(M, tile_bm(d.tcfg));
       d.tiles_n = cdiv(d.Cout, tile_bn(d.tcfg));
     } else if (d.kind == DK_SEP) {
-      d.tiles_m = cdiv(M, kSepBM);
+      // tiles never straddle two images; a tile's kSepBM pixels span at most
+      // rows_out output rows, so rows_out + kh - 1 input rows are staged
+      const int howo = d.Ho * d.Wo;
+      const int rows_out = std::min(d.Ho, (kSepBM - 1) / d.Wo + 2);
+      d.rows_per_tile = std::min(d.H, rows_out + d.kh - 1);
+      d.chunk_c = 32;
+      while (d.chunk_c > 4 && sep_lds_floats(d) * 4 > kSepMaxLds) d.chunk_c /= 2;
+      if (sep_lds_floats(d) * 4 > kSepMaxLds) fail(IOS_E_UNSUPPORTED, "SEPCONV rows too wide for LDS");
+      d.tiles_per_plane = cdiv(howo, kSepBM);
+      d.tiles_m = d.N * d.tiles_per_plane;
       d.tiles_n = 1;
     } else if (d.kind == DK_POOL_MAX || d.kind == DK_POOL_AVG) {
       // output rows per tile: as many as fit (with halo) in the LDS budget

@@ -64,9 +64,10 @@ inline TileShape tile_shape(int cfg) {
 inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
 inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * s.wn; }
 
-// SEPCONV tile: 16 * kSepFM output pixels x every output channel.
-constexpr int kSepFM = 2;
-constexpr int kSepBM = 16 * kSepFM;
+// SEPCONV tile: kSepBM output pixels of one image x every output channel;
+// the input channels are walked in chunks whose rows (with halo) sit in LDS.
+constexpr int kSepBM = 16;
+constexpr int kSepMaxLds = 64 * 1024;   // bytes of LDS one SEPCONV tile may use
 // Elementwise tiles: add / mean handle up to kEltPerTile contiguous outputs of
 // one channel plane; a pool tile handles a band of output rows of one plane
 // whose input rows (with halo) fit in kPoolLdsFloats of LDS.
@@ -93,7 +94,8 @@ struct DevOp {
   int32_t dep[kMaxDeps];       // stage-local indices of ops this op waits for
   int32_t signal;              // 1 if another op of the stage waits for this one
   float inv_n;                 // MEAN: 1 / n_in
-  int32_t rows_per_tile;       // POOL: output rows per tile
+  int32_t rows_per_tile;       // POOL: output rows per tile; SEP: staged input rows
+  int32_t chunk_c;             // SEP: input channels per chunk
   int32_t tiles_per_plane;     // POOL / ADD / MEAN: tiles per (image, channel) plane
   int32_t w_bytes;             // size of wpk in bytes
   const float *wpk;            // CONV: [kh*kw][CinP][Npad]; SEP: pointwise [CinP][Npad]
@@ -118,6 +120,10 @@ struct StageArgs {
 hipError_t launch_stage(const StageArgs &args, int lds_bytes, bool light, hipStream_t stream);
 // Dynamic LDS a tile of `op` needs.
 int op_lds_bytes(const DevOp &op);
+// SEPCONV tile LDS (floats): staged rows + depthwise chunk + output tile.
+inline int sep_lds_floats(const DevOp &d) {
+  return d.chunk_c * d.rows_per_tile * d.W + d.chunk_c * (kSepBM + 1) + d.Npad * (kSepBM + 1);
+}
 
 // ------------------------------------------------------------------ host IR
 

@@ -27,6 +27,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 // s_waitcnt operand with vmcnt = 0 and the other counters at their maxima
 // (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8], vmcnt[5:4] in [15:14])
 constexpr int kWaitVmcnt0 = 0x0F70;
+constexpr int kXcds = 8;   // accelerator complex dies of an MI355X
 
 __device__ __forceinline__ floatx4 mfma16x16x4(float a, float b, floatx4 c) {
   // D[16x16] += A[16x4] * B[4x16]; lane l supplies A[l%16][l/16] and
@@ -257,84 +258,128 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
 
 // ------------------------------------------------------------------ sepconv
 
+// "Relu-SepConv" unit on kSepBM pixels of one image x all output channels.
+// Input channels are walked in chunks of chunk_c: (1) the chunk's input rows
+// (with halo) are staged in LDS as ReLU(sum of inputs), with coalesced
+// loads; (2) the depthwise filter turns them into a kSepBM x chunk_c tile in
+// LDS; (3) that tile is the next chunk of the pointwise GEMM's reduction on
+// MFMA (wave w owns 16-column blocks w, w+8, ...).
 template <bool COH>
 __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
   constexpr int BM = kSepBM, LDM = BM + 1, MAXJ = kMaxChannels / 16 / kWaves;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
-  const int Wo = op.Wo, howo = op.Ho * Wo, M = op.N * howo;
-  const int H = op.H, W = op.W, HW = H * W;
-  const int CinP = op.CinP, Cin = op.Cin, kh = op.kh, kw = op.kw, taps = kh * kw;
-  const int n_in = op.n_in;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = op.H, W = op.W, Wo = op.Wo, howo = op.Ho * Wo;
+  const int Cin = op.Cin, kh = op.kh, kw = op.kw, taps = kh * kw;
+  const int CC = op.chunk_c, ROWS = op.rows_per_tile;
+  const int img = t / op.tiles_per_plane, m0 = (t - img * op.tiles_per_plane) * BM;
+  const int m_last = min(howo, m0 + BM) - 1;
+  const int ih_lo = max(0, m0 / Wo - op.ph);
+  const int ih_hi = min(H, m_last / Wo - op.ph + kh);      // staged input rows [ih_lo, ih_hi)
+  const int nrows = ih_hi - ih_lo;
+  float *halo = lds;                                      // [CC][ROWS][W]
+  float *tb = lds + CC * ROWS * W;                         // [CC][LDM]: depthwise outputs
+  float *ob = tb + CC * LDM;                               // [Npad][LDM]: output tile
 
-  // phase 1: t[c][m] = sum_taps dw[c][tap] * ReLU(sum_i x_i[c][pixel + tap])
-  for (int idx = tid; idx < CinP * BM; idx += kThreads) {
-    int c = idx / BM, mm = idx - c * BM, m = t * BM + mm;
-    float v = 0.f;
-    if (c < Cin && m < M) {
-      int img = m / howo, r = m - img * howo, oh = r / Wo, ow = r - oh * Wo;
-      const float *wdw = op.dw + c * taps;
-      for (int u = 0; u < kh; ++u) {
-        int ih = oh + u - op.ph;
-        if (ih < 0 || ih >= H) continue;
-        for (int q = 0; q < kw; ++q) {
-          int iw = ow + q - op.pw;
-          if (iw < 0 || iw >= W) continue;
-          float s = 0.f;
-          for (int i = 0; i < n_in; ++i)
-            s += ld<false>(a.slot[op.in_slot[i]] + (img * op.in_ctot[i] + op.in_coff[i] + c) * HW + ih * W + iw);
-          if (op.pre_relu) s = fmaxf(s, 0.f);
-          v = fmaf(wdw[u * kw + q], s, v);
+  const int NB = op.Npad >> 4;
+  const int row16 = lane & 15, kq = lane >> 4;
+  const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
+
+  floatx4 acc[MAXJ];
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c0 = 0; c0 < op.CinP; c0 += CC) {
+    // pointwise weights of this chunk: loaded first, in flight during (1)-(2)
+    // (rows past CinP, in a last partial chunk, are outside the buffer: 0)
+    float bw[8][MAXJ];
+#pragma unroll
+    for (int s8 = 0; s8 < 8; ++s8) {
+      const int wrow = ((c0 + 4 * s8 + kq) * op.Npad + row16) * 4;
+#pragma unroll
+      for (int j = 0; j < MAXJ; ++j) {
+        const int nb = wave + kWaves * j;
+        bw[s8][j] = (4 * s8 < CC && nb < NB) ? bld(wr, wrow + nb * 64, 0) : 0.f;
+      }
+    }
+    // (1) stage ReLU(sum of inputs) for channels c0 .. c0+CC-1, rows [ih_lo, ih_hi),
+    //     eight loads in flight per thread
+    const int plane = nrows * W, nst = CC * plane;
+    for (int i0 = 0; i0 < nst; i0 += 8 * kThreads) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+      for (int k = 0; k < op.n_in; ++k) {
+        const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[k]], op.in_bytes[k]);
+        const int cbase = (img * op.in_ctot[k] + op.in_coff[k] + c0) * H + ih_lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int i = i0 + e * kThreads + tid;
+          const int cc = i / plane, rw = i - cc * plane;
+          const bool ok = i < nst && c0 + cc < Cin;
+          v[e] += bld(xr, ok ? ((cbase + cc * H) * W + rw) * 4 : kOOB, 0);
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int i = i0 + e * kThreads + tid;
+        if (i < nst) {
+          const int cc = i / plane, rw = i - cc * plane;
+          halo[cc * ROWS * W + rw] = op.pre_relu ? fmaxf(v[e], 0.f) : v[e];
         }
       }
     }
-    lds[c * LDM + mm] = v;
-  }
-  __syncthreads();
-
-  // phase 2: pointwise 1x1 on MFMA; wave w owns 16-column blocks w, w+8, ...
-  const int NB = op.Npad >> 4;
-  const int row16 = lane & 15, kq = lane >> 4;
-  floatx4 acc[kSepFM][MAXJ];
+    __syncthreads();
+    // (2) depthwise: one (channel, pixel) per thread when CC * BM <= threads
+    for (int i = tid; i < CC * BM; i += kThreads) {
+      const int cc = i / BM, mm = i - cc * BM;
+      const int m = m0 + mm, oh = m / Wo, ow = m - oh * Wo;
+      const int c = c0 + cc;
+      float v = 0.f;
+      if (c < Cin && m < howo) {
+        const float *wk = op.dw + c * taps;
+        const float *hb = halo + cc * ROWS * W;
+        for (int u = 0; u < kh; ++u) {
+          const int ih = oh + u - op.ph;
+          if (ih < ih_lo || ih >= ih_hi) continue;        // outside the image
+          for (int q = 0; q < kw; ++q) {
+            const int iw = ow + q - op.pw;
+            if (iw < 0 || iw >= W) continue;
+            v = fmaf(wk[u * kw + q], hb[(ih - ih_lo) * W + iw], v);
+          }
+        }
+      }
+      tb[cc * LDM + mm] = v;
+    }
+    __syncthreads();
+    // (3) pointwise chunk on MFMA
 #pragma unroll
-  for (int fm = 0; fm < kSepFM; ++fm)
+    for (int s8 = 0; s8 < 8; ++s8) {
+      if (4 * s8 < CC) {
+        const float av = tb[(4 * s8 + kq) * LDM + row16];
 #pragma unroll
-    for (int j = 0; j < MAXJ; ++j) acc[fm][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < CinP; c0 += 4) {
-    float av[kSepFM];
-#pragma unroll
-    for (int fm = 0; fm < kSepFM; ++fm) av[fm] = lds[(c0 + kq) * LDM + fm * 16 + row16];
-    const float *wrow = op.wpk + (size_t)(c0 + kq) * op.Npad + row16;
-#pragma unroll
-    for (int j = 0; j < MAXJ; ++j) {
-      int nb = wave + kWaves * j;
-      if (nb < NB) {
-        float b = wrow[nb * 16];
-#pragma unroll
-        for (int fm = 0; fm < kSepFM; ++fm) acc[fm][j] = mfma16x16x4(av[fm], b, acc[fm][j]);
+        for (int j = 0; j < MAXJ; ++j)
+          if (wave + kWaves * j < NB) acc[j] = mfma16x16x4(av, bw[s8][j], acc[j]);
       }
     }
+    __syncthreads();   // halo / tb are rewritten by the next chunk
   }
-  __syncthreads();
+  // output tile [n][m] in LDS, then coalesced stores with bias
 #pragma unroll
   for (int j = 0; j < MAXJ; ++j) {
-    int nb = wave + kWaves * j;
+    const int nb = wave + kWaves * j;
     if (nb < NB) {
 #pragma unroll
-      for (int fm = 0; fm < kSepFM; ++fm)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          lds[(nb * 16 + row16) * LDM + fm * 16 + 4 * kq + e] = acc[fm][j][e];
+      for (int e = 0; e < 4; ++e) ob[(nb * 16 + row16) * LDM + 4 * kq + e] = acc[j][e];
     }
   }
   __syncthreads();
   for (int idx = tid; idx < op.Cout * BM; idx += kThreads) {
-    int n = idx / BM, mm = idx - n * BM, m = t * BM + mm;
-    if (m >= M) continue;
-    float v = lds[n * LDM + mm] + op.bias[n];
+    const int n = idx / BM, mm = idx - n * BM, m = m0 + mm;
+    if (m >= howo) continue;
+    float v = ob[n * LDM + mm] + op.bias[n];
     if (op.post_relu) v = fmaxf(v, 0.f);
-    int img = m / howo, pix = m - img * howo;
-    st<COH>(route_ptr(a, op, n, img, pix, howo), v);
+    st<COH>(route_ptr(a, op, n, img, m, howo), v);
   }
 }
 
@@ -456,7 +501,16 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
   }
   int opi = 0;
   while (opi + 1 < a.n_ops && t >= a.op_start[opi + 1]) ++opi;
-  const int ti = t - a.op_start[opi];
+  int ti = t - a.op_start[opi];
+  if (!a.use_ticket) {
+    // Workgroup i runs on XCD i % 8.  Inside each op, give the op's
+    // workgroups on one XCD a contiguous range of its tiles, so neighbouring
+    // pixel tiles meet in the same L2 (a bijection on the op's tiles, so any
+    // placement stays correct; the op order across the stage is unchanged).
+    const int n = a.op_start[opi + 1] - a.op_start[opi];
+    const int q = n / kXcds, r = n - q * kXcds, x = ti % kXcds;
+    ti = x * q + min(x, r) + ti / kXcds;
+  }
   // read-only for the whole launch: constant address space, so its fields
   // are scalar (uniform) loads
   typedef __attribute__((address_space(4))) const DevOp cDevOp;
@@ -523,10 +577,7 @@ int op_lds_bytes(const DevOp &op) {
     TileShape s = tile_shape(op.tcfg);
     return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
   }
-  if (op.kind == DK_SEP) {
-    int c = op.CinP > op.Npad ? op.CinP : op.Npad;
-    return c * (kSepBM + 1) * (int)sizeof(float);
-  }
+  if (op.kind == DK_SEP) return sep_lds_floats(op) * (int)sizeof(float);
   if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
     return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
   return 0;

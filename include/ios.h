@@ -246,8 +246,7 @@ int ios_run_timed(ios_graph *g, ios_schedule_t *q, const float *const *d_inputs,
 
 /* Wait for `hip_stream` and read the graph's device error word: *flags
  * receives 0 if every stage kernel since the last call finished normally,
- * else a bit set (1 = an intra-stage dependency wait gave up, 2 = a
- * workgroup drew a ticket outside the tile table).  Clears it.
+ * else a bit set (1 = an intra-stage dependency wait gave up).  Clears it.
  * Errors: IOS_E_ARG, IOS_E_HIP. */
 int ios_device_status(ios_graph *g, void *hip_stream, int32_t *flags);
 

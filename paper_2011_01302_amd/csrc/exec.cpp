@@ -278,23 +278,30 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   for (int i = 0; i < n; ++i) pos[order[i]] = i;
   std::vector<DevOp> sorted;
   std::vector<int32_t> start{0};
-  bool ticket = false, light = true;
+  bool persistent = false, big_conv = false, has_sep = false;
   int lds = 0;
   for (int i : order) {
     DevOp d = dops[i];
     for (int k = 0; k < d.n_deps; ++k) d.dep[k] = pos[d.dep[k]];
     sorted.push_back(d);
     start.push_back(start.back() + d.n_tiles);
-    ticket |= d.n_deps > 0;
-    light &= d.kind != DK_CONV || d.tcfg == TC_16x16_K8;
+    persistent |= d.n_deps > 0;
+    big_conv |= d.kind == DK_CONV && d.tcfg != TC_16x16_K8;
+    has_sep |= d.kind == DK_SEP;
     lds = std::max(lds, op_lds_bytes(d));
   }
   cs->ops = sorted;
   cs->op_start = start;
   cs->slot_buf = sm.bufs;
   cs->lds_bytes = lds;
-  cs->ticket = ticket;
-  cs->light = light;
+  cs->persistent = persistent;
+  cs->variant = big_conv ? KV_FULL : has_sep ? KV_SEP : KV_LIGHT;
+  cs->grid = start.back();
+  if (persistent) {
+    int cap = stage_capacity(cs->variant, lds);
+    if (cap <= 0) fail(IOS_E_HIP, "cannot size the persistent launch of a stage with dependencies");
+    cs->grid = std::min(cs->grid, cap);
+  }
   cs->owns = !scratch;
   // device copies
   if (!mw.empty()) {
@@ -321,9 +328,9 @@ void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<fl
   a.err = g->d_err;
   a.n_tiles = cs.op_start.back();
   a.n_ops = (int)cs.ops.size();
-  a.use_ticket = cs.ticket ? 1 : 0;
+  a.persistent = cs.persistent ? 1 : 0;
   a.spin_limit = 1 << 24;
-  hip_check(launch_stage(a, cs.lds_bytes, cs.light, stream), "stage launch");
+  hip_check(launch_stage(a, cs.grid, cs.lds_bytes, cs.variant, stream), "stage launch");
 }
 
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,

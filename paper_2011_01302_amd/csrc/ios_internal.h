@@ -107,17 +107,21 @@ struct StageArgs {
   float *slot[kMaxSlots];
   const DevOp *ops;    // in tile order: op i owns tiles [op_start[i], op_start[i+1])
   int32_t op_start[kMaxStageOps + 1];
-  int32_t *ctr;        // [0] ticket, [1] finished, [2 + i + kCtrStride * r] tiles done of op i (copy r)
+  int32_t *ctr;        // [1] workgroups finished, [2 + i + kCtrStride * r] tiles done of op i (copy r)
   int32_t *err;        // device error word
   int32_t n_tiles;
   int32_t n_ops;
-  int32_t use_ticket;  // 1 when some op waits for another op of the stage
+  int32_t persistent;  // 1 when some op waits for another op of the stage (grid <= capacity)
   int32_t spin_limit;  // polls before a dependency wait gives up
 };
 
 // Launch one stage (defined in the HIP translation unit).
-// `light`: every conv of the stage uses the 16x16 tile (smaller register file).
-hipError_t launch_stage(const StageArgs &args, int lds_bytes, bool light, hipStream_t stream);
+// Kernel variant of a stage (see the stage kernel): the smallest one that
+// contains every tile kind the stage uses.
+enum KernelVariant { KV_LIGHT = 0, KV_SEP = 1, KV_FULL = 2 };
+hipError_t launch_stage(const StageArgs &args, int grid, int lds_bytes, int variant, hipStream_t stream);
+// Workgroups of `variant` with `lds_bytes` of LDS that fit on the device at once (0 if unknown).
+int stage_capacity(int variant, int lds_bytes);
 // Dynamic LDS a tile of `op` needs.
 int op_lds_bytes(const DevOp &op);
 // SEPCONV tile LDS (floats): staged rows + depthwise chunk + output tile.
@@ -171,8 +175,9 @@ struct CompiledStage {
   std::vector<int32_t> op_start; // tile ranges, size ops + 1
   std::vector<int> slot_buf;     // slot -> buffer index
   int lds_bytes = 0;
-  bool ticket = false;
-  bool light = true;             // every conv uses the 16x16 tile
+  bool persistent = false;       // some op waits for another: persistent launch
+  int grid = 0;                  // workgroups launched
+  int variant = 0;               // KernelVariant
   // device copies (owned unless `scratch`)
   DevOp *d_ops = nullptr;
   int32_t *d_ctr = nullptr;

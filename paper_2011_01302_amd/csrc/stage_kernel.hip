@@ -13,11 +13,8 @@
 //             all channels, then the pointwise 1x1 runs on MFMA from LDS.
 //   DK_POOL_* / DK_ADD / DK_MEAN   elementwise tiles on the vector ALUs.
 // Operators of one group run in order (Sec. 3: a group is executed
-// sequentially): when a stage has such chains, workgroups take tiles through
-// an atomic ticket in topological order and a consumer tile waits until every
-// tile of its producers has finished.  A workgroup only waits for tickets
-// smaller than its own, all held by workgroups already running, so the waits
-// always end.
+// sequentially): a consumer tile waits until every tile of its producers has
+// finished (see ios_stage_kernel for why the waits always end).
 #include "ios_internal.h"
 
 namespace ios {
@@ -455,25 +452,31 @@ __device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, in
 
 // ------------------------------------------------------------------ kernel
 
-// LIGHT kernels support only the 16x16 conv tile, which keeps register use
-// (and so occupancy) at the level of the small tiles.
-template <bool COH, bool LIGHT>
+// Kernel variants, chosen per stage by the host so that a stage only pays
+// the registers of the tile kinds it contains:
+//   KV_LIGHT  16x16 conv tiles, pooling, add / mean
+//   KV_SEP    KV_LIGHT + SEPCONV tiles
+//   KV_FULL   every tile kind and conv tile shape
+template <bool COH, int KV>
 __device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, int ti, float *lds) {
   switch (op.kind) {
     case DK_CONV:
-      if constexpr (LIGHT) {
+      if constexpr (KV != KV_FULL) {
         conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds);
         break;
+      } else {
+        switch (op.tcfg) {
+          case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds); break;
+          case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(a, op, ti, lds); break;
+          case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(a, op, ti, lds); break;
+          case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(a, op, ti, lds); break;
+          default: conv_tile<2, 2, 4, 2, 1, COH>(a, op, ti, lds); break;
+        }
+        break;
       }
-      switch (op.tcfg) {
-        case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds); break;
-        case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(a, op, ti, lds); break;
-        case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(a, op, ti, lds); break;
-        case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(a, op, ti, lds); break;
-        default: conv_tile<2, 2, 4, 2, 1, COH>(a, op, ti, lds); break;
-      }
+    case DK_SEP:
+      if constexpr (KV != KV_LIGHT) sep_tile<COH>(a, op, ti, lds);
       break;
-    case DK_SEP: sep_tile<COH>(a, op, ti, lds); break;
     case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true, lds); break;
     case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false, lds); break;
     case DK_ADD: sum_tile<COH>(a, op, ti, false); break;
@@ -481,28 +484,14 @@ __device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, in
   }
 }
 
-template <bool LIGHT>
-__global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
-  extern __shared__ float lds[];
-  __shared__ int s_ticket;
+// One tile: find its op, wait for in-stage producers, compute, signal.
+template <int KV>
+__device__ __forceinline__ void process_tile(const StageArgs &a, int t, bool remap, float *lds) {
   const int tid = threadIdx.x;
-  int t;
-  if (a.use_ticket) {
-    if (tid == 0)
-      s_ticket = __hip_atomic_fetch_add(&a.ctr[0], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    t = __builtin_amdgcn_readfirstlane(s_ticket);
-  } else {
-    t = blockIdx.x;
-  }
-  if (t >= a.n_tiles) {   // only if the counters were not left at zero
-    if (tid == 0) __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
   int opi = 0;
   while (opi + 1 < a.n_ops && t >= a.op_start[opi + 1]) ++opi;
   int ti = t - a.op_start[opi];
-  if (!a.use_ticket) {
+  if (remap) {
     // Workgroup i runs on XCD i % 8.  Inside each op, give the op's
     // workgroups on one XCD a contiguous range of its tiles, so neighbouring
     // pixel tiles meet in the same L2 (a bijection on the op's tiles, so any
@@ -541,32 +530,52 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
     __syncthreads();
   }
 
-  if (op.n_deps || op.signal) run_tile<true, LIGHT>(a, op, ti, lds);
-  else run_tile<false, LIGHT>(a, op, ti, lds);
+  if (op.n_deps || op.signal) run_tile<true, KV>(a, op, ti, lds);
+  else run_tile<false, KV>(a, op, ti, lds);
 
   if (op.signal) {
     // The tile's outputs were written with agent-coherent stores.  Every wave
     // waits until its stores have been performed, then one wave moves every
-    // copy of the op's counter; a consumer reads the outputs only after seeing the final
-    // count and invalidating its stale lines, so it sees every value.  This
-    // orders like a release/acquire pair without a per-tile L2 writeback.
+    // copy of the op's counter; a consumer reads the outputs only after
+    // seeing the final count and invalidating its stale lines, so it sees
+    // every value.  This orders like a release/acquire pair without a
+    // per-tile L2 writeback.
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
     if (tid < kCtrCopies)
       __hip_atomic_fetch_add(&a.ctr[2 + opi + kCtrStride * tid], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (a.use_ticket && tid == 0) {
-    // relaxed: a workgroup's counter polls have returned before this
-    // increment is issued, so the reset below cannot overtake them (an
-    // agent-scope acq_rel here would cost an L2 writeback + invalidate)
+}
+
+// A stage without in-stage dependencies runs one workgroup per tile.  A stage
+// with dependencies runs G workgroups, G no more than fit on the GPU at once
+// (occupancy of this kernel), so that all of them become resident even if
+// other kernels hold CUs for a while.  Workgroup w takes tiles w, w + G,
+// w + 2G, ... in tile order, which is topological: the smallest unfinished
+// tile has finished producers and an owner that has reached it, so every wait
+// ends, without a work queue or ticket atomics.  (A cooperative launch would
+// guarantee the residency too, but costs about 20 us per launch here.)
+template <int KV, bool PERSIST>
+__global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
+  extern __shared__ float lds[];
+  if constexpr (!PERSIST) {
+    process_tile<KV>(a, blockIdx.x, true, lds);
+    return;
+  }
+  for (int t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
+    process_tile<KV>(a, t, false, lds);
+    __syncthreads();   // the next tile reuses LDS
+  }
+  if (threadIdx.x == 0) {
+    // relaxed: this workgroup's counter polls have returned before the
+    // increment is issued, so the reset below cannot overtake them
     int f = __hip_atomic_fetch_add(&a.ctr[1], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (f == a.n_tiles - 1) {
-      // last tile of the launch: every other workgroup has passed its waits;
-      // leave the counters at zero for the next launch on the stream
+    if (f == (int)gridDim.x - 1) {
+      // last workgroup of the launch: leave the counters at zero for the
+      // next launch on the stream
       for (int r = 0; r < kCtrCopies; ++r)
         for (int i = 0; i < a.n_ops; ++i)
           __hip_atomic_store(&a.ctr[2 + i + kCtrStride * r], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.ctr[0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctr[1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -583,11 +592,46 @@ int op_lds_bytes(const DevOp &op) {
   return 0;
 }
 
-hipError_t launch_stage(const StageArgs &args, int lds_bytes, bool light, hipStream_t stream) {
-  if (light)
-    hipLaunchKernelGGL(ios_stage_kernel<true>, dim3(args.n_tiles), dim3(kThreads), lds_bytes, stream, args);
-  else
-    hipLaunchKernelGGL(ios_stage_kernel<false>, dim3(args.n_tiles), dim3(kThreads), lds_bytes, stream, args);
+static void *kernel_of(int variant, bool persist) {
+  if (persist) {
+    switch (variant) {
+      case KV_LIGHT: return (void *)ios_stage_kernel<KV_LIGHT, true>;
+      case KV_SEP: return (void *)ios_stage_kernel<KV_SEP, true>;
+      default: return (void *)ios_stage_kernel<KV_FULL, true>;
+    }
+  }
+  switch (variant) {
+    case KV_LIGHT: return (void *)ios_stage_kernel<KV_LIGHT, false>;
+    case KV_SEP: return (void *)ios_stage_kernel<KV_SEP, false>;
+    default: return (void *)ios_stage_kernel<KV_FULL, false>;
+  }
+}
+
+int stage_capacity(int variant, int lds_bytes) {
+  int dev = 0, per_cu = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)kernel_of(variant, true),
+                                                   kThreads, lds_bytes) != hipSuccess)
+    return 0;
+  return per_cu * prop.multiProcessorCount;
+}
+
+hipError_t launch_stage(const StageArgs &args, int grid, int lds_bytes, int variant, hipStream_t stream) {
+  const dim3 g(grid), block(kThreads);
+  if (args.persistent) {
+    switch (variant) {
+      case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, true>), g, block, lds_bytes, stream, args); break;
+      case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, true>), g, block, lds_bytes, stream, args); break;
+      default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, true>), g, block, lds_bytes, stream, args); break;
+    }
+    return hipGetLastError();
+  }
+  switch (variant) {
+    case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, false>), g, block, lds_bytes, stream, args); break;
+    case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, false>), g, block, lds_bytes, stream, args); break;
+    default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, false>), g, block, lds_bytes, stream, args); break;
+  }
   return hipGetLastError();
 }
 

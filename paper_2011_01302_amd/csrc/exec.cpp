@@ -88,7 +88,7 @@ double tile_work(const DevOp &d) {
       return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * d.kh * d.kw * d.CinP / s.wk;
     }
     case DK_SEP:
-      return (double)kSepBM * d.CinP * (d.kh * d.kw * d.n_in + d.Npad / 4.0);
+      return 16.0 * d.CinP * (d.sep_k * d.sep_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
     default:
       return (double)kEltPerTile * (d.kind <= DK_POOL_AVG ? d.kh * d.kw : d.n_in) / 4.0;
   }
@@ -200,6 +200,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
           d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
           d.wpk = o.d_wpk; d.bias = o.d_bias; d.dw = o.d_dw;
           d.w_bytes = (int32_t)((size_t)o.CinP * o.Npad * sizeof(float));
+          d.sep_k = sep_window(o.d.kh, o.d.kw);
+          d.sep_nbt = std::min(o.sep_nbt, o.Npad / 16);
+          d.dw_bytes = (int32_t)((size_t)o.CinP * sep_kkp(d.sep_k) * sizeof(float));
+          if (sep_lds_bytes(d.CinP, d.sep_k, d.sep_nbt) > kSepMaxLds)
+            fail(IOS_E_UNSUPPORTED, "SEPCONV tile exceeds its LDS budget");
           break;
         case IOS_POOL_MAX: d.kind = DK_POOL_MAX; break;
         case IOS_POOL_AVG: d.kind = DK_POOL_AVG; break;
@@ -233,17 +238,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.tiles_m = cdiv(M, tile_bm(d.tcfg));
       d.tiles_n = cdiv(d.Cout, tile_bn(d.tcfg));
     } else if (d.kind == DK_SEP) {
-      // tiles never straddle two images; a tile's kSepBM pixels span at most
-      // rows_out output rows, so rows_out + kh - 1 input rows are staged
-      const int howo = d.Ho * d.Wo;
-      const int rows_out = std::min(d.Ho, (kSepBM - 1) / d.Wo + 2);
-      d.rows_per_tile = std::min(d.H, rows_out + d.kh - 1);
-      d.chunk_c = 32;
-      while (d.chunk_c > 4 && sep_lds_floats(d) * 4 > kSepMaxLds) d.chunk_c /= 2;
-      if (sep_lds_floats(d) * 4 > kSepMaxLds) fail(IOS_E_UNSUPPORTED, "SEPCONV rows too wide for LDS");
-      d.tiles_per_plane = cdiv(howo, kSepBM);
-      d.tiles_m = d.N * d.tiles_per_plane;
-      d.tiles_n = 1;
+      // tiles: (image, output row, 16-pixel block of the row) x groups of
+      // sep_nbt 16-channel output blocks
+      d.sep_bpr = cdiv(d.Wo, 16);
+      d.tiles_m = d.N * d.Ho * d.sep_bpr;
+      d.tiles_n = cdiv(d.Npad / 16, d.sep_nbt);
     } else if (d.kind == DK_POOL_MAX || d.kind == DK_POOL_AVG) {
       // output rows per tile: as many as fit (with halo) in the LDS budget
       int rows = d.Ho;

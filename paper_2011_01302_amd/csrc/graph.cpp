@@ -124,8 +124,10 @@ int add_op(ios_graph *g, const ios_op_desc *d, const int32_t *in_ids, int n_in,
         op.w.assign(weights, weights + nw);
         op.b.assign((size_t)d->cout, 0.f);
         if (bias) std::memcpy(op.b.data(), bias, sizeof(float) * d->cout);
-        if (kind == IOS_SEPCONV && (t0.c > kMaxChannels || d->cout > kMaxChannels))
-          fail(IOS_E_UNSUPPORTED, "SEPCONV supports at most 256 channels");
+        if (kind == IOS_SEPCONV && t0.c > kMaxChannels)
+          fail(IOS_E_UNSUPPORTED, "SEPCONV supports at most 256 input channels");
+        if (kind == IOS_SEPCONV && sep_window(d->kh, d->kw) == 0)
+          fail(IOS_E_UNSUPPORTED, "SEPCONV depthwise window larger than 5x5");
       }
       break;
     }
@@ -364,6 +366,21 @@ static T *upload(const std::vector<T> &v) {
 // Conv tile shape for an M x N output.  IOS_CONV_TILE=<0..3> in the
 // environment (read when a graph is finalized or a merged stage is built)
 // forces one shape for every conv, for tuning and for tests.
+// Largest number of 16-channel output blocks a SEPCONV tile can take (LDS).
+static int max_sep_nbt(const Op &op) {
+  const int K = sep_window(op.d.kh, op.d.kw);
+  int n = std::min(kSepMaxNB, op.Npad / 16);
+  while (n > 1 && sep_lds_bytes(op.CinP, K, n) > kSepMaxLds) --n;
+  return n;
+}
+
+// Output blocks per SEPCONV tile before measurement (IOS_SEP_NBT forces it).
+static int choose_sep_nbt(const Op &op) {
+  int v = 2;
+  if (const char *e = std::getenv("IOS_SEP_NBT")) v = std::atoi(e);
+  return std::max(1, std::min(v, max_sep_nbt(op)));
+}
+
 int choose_conv_tile(int64_t M, int N) {
   if (const char *e = std::getenv("IOS_CONV_TILE")) {
     int v = std::atoi(e);
@@ -393,6 +410,7 @@ void finalize_graph(ios_graph *g) {
     } else if (op.d.kind == IOS_SEPCONV) {
       op.CinP = round_up(op.cin, 4);
       op.Npad = round_up(op.d.cout, 16);
+      op.sep_nbt = choose_sep_nbt(op);
     }
   }
   g->cost_table.assign(g->blocks.size(), {});
@@ -426,8 +444,14 @@ void ensure_device(ios_graph *g) {
       op.d_wpk = upload(wpk);
       op.d_bias = upload(bias);
     } else if (op.d.kind == IOS_SEPCONV) {
-      int taps = op.d.kh * op.d.kw;
-      std::vector<float> dw(op.w.begin(), op.w.begin() + (size_t)op.cin * taps);
+      // depthwise taps at the top left of a K x K window (the rest zero),
+      // KKP floats per channel, channels past cin zero
+      const int taps = op.d.kh * op.d.kw, K = sep_window(op.d.kh, op.d.kw), kkp = sep_kkp(K);
+      std::vector<float> dw((size_t)op.CinP * kkp, 0.f);
+      for (int c = 0; c < op.cin; ++c)
+        for (int u = 0; u < op.d.kh; ++u)
+          for (int v = 0; v < op.d.kw; ++v)
+            dw[(size_t)c * kkp + u * K + v] = op.w[(size_t)c * taps + u * op.d.kw + v];
       std::vector<float> pw((size_t)op.CinP * op.Npad, 0.f);
       const float *src = op.w.data() + (size_t)op.cin * taps;
       for (int co = 0; co < op.d.cout; ++co)
@@ -455,6 +479,21 @@ void ensure_device(ios_graph *g) {
         if (ns < best_ns) { best_ns = ns; best = cfg; }
       }
       op.tcfg = best;
+    }
+  }
+  // Output blocks per SEPCONV tile, likewise measured (unless IOS_SEP_NBT).
+  if (!std::getenv("IOS_SEP_NBT")) {
+    for (int oi : g->units) {
+      Op &op = g->ops[oi];
+      if (op.d.kind != IOS_SEPCONV) continue;
+      int best = op.sep_nbt;
+      int64_t best_ns = INT64_MAX;
+      for (int nbt = 1; nbt <= max_sep_nbt(op); ++nbt) {
+        op.sep_nbt = nbt;
+        int64_t ns = profile_stage(g, {oi}, IOS_CONCURRENT, 2, 10, 3);
+        if (ns < best_ns) { best_ns = ns; best = nbt; }
+      }
+      op.sep_nbt = best;
     }
   }
 }

@@ -27,7 +27,7 @@ constexpr int kMaxStageOps = 64;  // operators of one stage (a block holds at mo
 constexpr int kCtrCopies = 32;
 constexpr int kCtrStride = 64;    // >= kMaxStageOps
 constexpr int kMaxUnitsPerBlock = 64;
-constexpr int kMaxChannels = 256; // SEPCONV channels (in and out) kept in LDS
+constexpr int kMaxChannels = 256; // SEPCONV input channels (8 waves x 8 k-steps of 4)
 constexpr int64_t kInf = INT64_MAX;
 
 // Kinds of work a stage kernel tile can do.
@@ -64,10 +64,28 @@ inline TileShape tile_shape(int cfg) {
 inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
 inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * s.wn; }
 
-// SEPCONV tile: kSepBM output pixels of one image x every output channel;
-// the input channels are walked in chunks whose rows (with halo) sit in LDS.
-constexpr int kSepBM = 16;
+// SEPCONV tile: 16 output pixels of one output row x sep_nbt blocks of 16
+// output channels (sep_nbt <= kSepMaxNB).  The depthwise window is padded to
+// K x K, K = 3 or 5 (sep_k); its weights are packed [CinP][sep_kkp(K)].
+constexpr int kSepMaxNB = 4;
 constexpr int kSepMaxLds = 64 * 1024;   // bytes of LDS one SEPCONV tile may use
+inline int sep_window(int kh, int kw) {
+  int k = kh > kw ? kh : kw;
+  return k <= 3 ? 3 : k <= 5 ? 5 : 0;
+}
+__host__ __device__ inline int sep_kkp(int K) { return (K * K + 3) & ~3; }
+// LDS of one wave of a SEPCONV tile (floats, a multiple of 64): depthwise and
+// pointwise weights of its k-steps, plus 64 floats so that no 64-lane copy
+// can reach the next wave's region; the tile's LDS also holds the
+// [wave][16 nbt columns][17] partial sums afterwards.
+__host__ __device__ inline int sep_wave_floats(int CinP, int K, int nbt) {
+  const int ksw = (CinP / 4 + 7) / 8;
+  return ((ksw * 4 * (sep_kkp(K) + 16 * nbt) + 63) & ~63) + 64;
+}
+__host__ __device__ inline int sep_lds_bytes(int CinP, int K, int nbt) {
+  const int w = 8 * sep_wave_floats(CinP, K, nbt), r = 8 * kSepMaxNB * 16 * 17;
+  return (w > r ? w : r) * 4;
+}
 // Elementwise tiles: add / mean handle up to kEltPerTile contiguous outputs of
 // one channel plane; a pool tile handles a band of output rows of one plane
 // whose input rows (with halo) fit in kPoolLdsFloats of LDS.
@@ -94,13 +112,16 @@ struct DevOp {
   int32_t dep[kMaxDeps];       // stage-local indices of ops this op waits for
   int32_t signal;              // 1 if another op of the stage waits for this one
   float inv_n;                 // MEAN: 1 / n_in
-  int32_t rows_per_tile;       // POOL: output rows per tile; SEP: staged input rows
-  int32_t chunk_c;             // SEP: input channels per chunk
+  int32_t rows_per_tile;       // POOL: output rows per tile
   int32_t tiles_per_plane;     // POOL / ADD / MEAN: tiles per (image, channel) plane
+  int32_t sep_k;               // SEP: depthwise window K (3, 5 or 7)
+  int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
+  int32_t sep_bpr;             // SEP: 16-pixel blocks per output row
   int32_t w_bytes;             // size of wpk in bytes
+  int32_t dw_bytes;            // SEP: size of dw in bytes
   const float *wpk;            // CONV: [kh*kw][CinP][Npad]; SEP: pointwise [CinP][Npad]
   const float *bias;           // [Npad]
-  const float *dw;             // SEP: depthwise [Cin][kh*kw]
+  const float *dw;             // SEP: depthwise [CinP][sep_kkp(K)], kh x kw taps at the top left of K x K
 };
 
 struct StageArgs {
@@ -124,10 +145,6 @@ hipError_t launch_stage(const StageArgs &args, int grid, int lds_bytes, int vari
 int stage_capacity(int variant, int lds_bytes);
 // Dynamic LDS a tile of `op` needs.
 int op_lds_bytes(const DevOp &op);
-// SEPCONV tile LDS (floats): staged rows + depthwise chunk + output tile.
-inline int sep_lds_floats(const DevOp &d) {
-  return d.chunk_c * d.rows_per_tile * d.W + d.chunk_c * (kSepBM + 1) + d.Npad * (kSepBM + 1);
-}
 
 // ------------------------------------------------------------------ host IR
 
@@ -161,6 +178,7 @@ struct Op {
   int cin = 0, h = 0, wd = 0, ho = 0, wo = 0;
   // device copies (units only)
   int CinP = 0, Npad = 0, tcfg = TC_32x32_K8;
+  int sep_nbt = 1;               // SEPCONV: output blocks of 16 channels per tile
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
 };
 

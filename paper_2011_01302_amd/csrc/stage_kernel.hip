@@ -9,12 +9,14 @@
 //             in the epilogue, which writes each output channel to its
 //             destination (a merged conv has several destinations).
 //   DK_SEP    "Relu-SepConv" unit (Table 2): the sum of the inputs, ReLU and
-//             the depthwise kxk filter are computed into LDS for 32 pixels x
-//             all channels, then the pointwise 1x1 runs on MFMA from LDS.
+//             the depthwise kxk filter are computed in registers, laid out as
+//             the A operand of the pointwise 1x1, which runs on MFMA.
 //   DK_POOL_* / DK_ADD / DK_MEAN   elementwise tiles on the vector ALUs.
 // Operators of one group run in order (Sec. 3: a group is executed
 // sequentially): a consumer tile waits until every tile of its producers has
 // finished (see ios_stage_kernel for why the waits always end).
+#include <utility>
+
 #include "ios_internal.h"
 
 namespace ios {
@@ -255,128 +257,205 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
 
 // ------------------------------------------------------------------ sepconv
 
-// "Relu-SepConv" unit on kSepBM pixels of one image x all output channels.
-// Input channels are walked in chunks of chunk_c: (1) the chunk's input rows
-// (with halo) are staged in LDS as ReLU(sum of inputs), with coalesced
-// loads; (2) the depthwise filter turns them into a kSepBM x chunk_c tile in
-// LDS; (3) that tile is the next chunk of the pointwise GEMM's reduction on
-// MFMA (wave w owns 16-column blocks w, w+8, ...).
-template <bool COH>
+// Cross-lane moves inside each row of 16 lanes (DPP): lane i of a row takes
+// the value of lane i + N (from_right) or lane i - N (from_left) of the same
+// row, and 0 where that lane lies outside the row.
+template <int N>
+__device__ __forceinline__ float from_right(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                0x100 + N, 0xF, 0xF, true));
+}
+template <int N>
+__device__ __forceinline__ float from_left(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                0x110 + N, 0xF, 0xF, true));
+}
+
+// Taps 1 .. K-1 of one window row: tap v of pixel j is column j + v of the
+// row segment, i.e. lane j + v's first value or lane j + v - 16's second.
+template <int... V>
+__device__ __forceinline__ float dw_taps(const float *w, float xa, float xb, float d,
+                                         std::integer_sequence<int, V...>) {
+  ((d = fmaf(w[V + 1], from_right<V + 1>(xa) + from_left<15 - V>(xb), d)), ...);
+  return d;
+}
+
+// Direct global -> LDS load of one float per active lane: lane i of the wave
+// writes l[i] (l wave-uniform), no VGPR involved.  The compiler does not see
+// this write: readers must wait for vmcnt(0) themselves (lds_dma_wait).
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float *l, int voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)l, 4, voff, 0, 0, 0);
+}
+__device__ __forceinline__ void lds_dma_wait() {
+  __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// "Relu-SepConv" unit (sum of inputs -> ReLU -> depthwise -> pointwise) on 16
+// output pixels of one output row x sep_nbt blocks of 16 output channels.
+//
+// Lane l = 16 g + j of a wave computes the depthwise output of pixel j for
+// channel 4 ks + g: exactly the A operand lane l gives the 16x16x4 MFMA at
+// k-step ks, so depthwise results never leave registers.  Per window row a
+// lane loads two inputs, columns j and 16 + j of the row segment the 16
+// pixels read; the K taps of pixel j are then gathered from lanes j .. j+K-1
+// of its row with DPP shifts.  The 8 waves split the input channels (k-steps
+// of 4); each wave copies the depthwise and pointwise weights of its own
+// channels straight into a private LDS region, and the waves' partial
+// pointwise sums are added in LDS.  Every input value of a batch of KB
+// k-steps is loaded before any is used (one memory round trip per batch);
+// with several inputs the next input's loads are in flight while the current
+// one is added.
+template <int K, bool SINGLE, bool COH>
 __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
-  constexpr int BM = kSepBM, LDM = BM + 1, MAXJ = kMaxChannels / 16 / kWaves;
+  constexpr int KB = SINGLE ? (K == 3 ? 8 : 6) : (K == 3 ? 4 : 2);   // k-steps per batch
+  constexpr int KKP = (K * K + 3) & ~3;               // floats per channel of depthwise weights
+  constexpr int NBT = kSepMaxNB;
+  constexpr int LDR = 16 + 1;                         // reduction buffer row pitch
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int H = op.H, W = op.W, Wo = op.Wo, howo = op.Ho * Wo;
-  const int Cin = op.Cin, kh = op.kh, kw = op.kw, taps = kh * kw;
-  const int CC = op.chunk_c, ROWS = op.rows_per_tile;
-  const int img = t / op.tiles_per_plane, m0 = (t - img * op.tiles_per_plane) * BM;
-  const int m_last = min(howo, m0 + BM) - 1;
-  const int ih_lo = max(0, m0 / Wo - op.ph);
-  const int ih_hi = min(H, m_last / Wo - op.ph + kh);      // staged input rows [ih_lo, ih_hi)
-  const int nrows = ih_hi - ih_lo;
-  float *halo = lds;                                      // [CC][ROWS][W]
-  float *tb = lds + CC * ROWS * W;                         // [CC][LDM]: depthwise outputs
-  float *ob = tb + CC * LDM;                               // [Npad][LDM]: output tile
+  const int j = lane & 15, g = lane >> 4;
+  const int tm = t / op.tiles_n, tn = t - tm * op.tiles_n;
+  const int H = op.H, W = op.W, Ho = op.Ho, Wo = op.Wo, howo = Ho * Wo;
+  const int bpr = op.sep_bpr, per_img = Ho * bpr;
+  const int img = tm / per_img, rr = tm - img * per_img;
+  const int oh = rr / bpr, ow0 = (rr - oh * bpr) * 16;
+  const int NKS = op.CinP >> 2;
+  const int ks0 = NKS * wave / kWaves, nks = NKS * (wave + 1) / kWaves - ks0;
+  const int nb0 = tn * op.sep_nbt, nbc = min(op.sep_nbt, (op.Npad >> 4) - nb0);
+  const int pitch = nbc * 16;                         // pointwise weights row in LDS
+  const int Cin = op.Cin, kh = op.kh, ph = op.ph;
 
-  const int NB = op.Npad >> 4;
-  const int row16 = lane & 15, kq = lane >> 4;
-  const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
-
-  floatx4 acc[MAXJ];
-#pragma unroll
-  for (int j = 0; j < MAXJ; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  for (int c0 = 0; c0 < op.CinP; c0 += CC) {
-    // pointwise weights of this chunk: loaded first, in flight during (1)-(2)
-    // (rows past CinP, in a last partial chunk, are outside the buffer: 0)
-    float bw[8][MAXJ];
-#pragma unroll
-    for (int s8 = 0; s8 < 8; ++s8) {
-      const int wrow = ((c0 + 4 * s8 + kq) * op.Npad + row16) * 4;
-#pragma unroll
-      for (int j = 0; j < MAXJ; ++j) {
-        const int nb = wave + kWaves * j;
-        bw[s8][j] = (4 * s8 < CC && nb < NB) ? bld(wr, wrow + nb * 64, 0) : 0.f;
-      }
-    }
-    // (1) stage ReLU(sum of inputs) for channels c0 .. c0+CC-1, rows [ih_lo, ih_hi),
-    //     eight loads in flight per thread
-    const int plane = nrows * W, nst = CC * plane;
-    for (int i0 = 0; i0 < nst; i0 += 8 * kThreads) {
-      float v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      for (int k = 0; k < op.n_in; ++k) {
-        const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[k]], op.in_bytes[k]);
-        const int cbase = (img * op.in_ctot[k] + op.in_coff[k] + c0) * H + ih_lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int i = i0 + e * kThreads + tid;
-          const int cc = i / plane, rw = i - cc * plane;
-          const bool ok = i < nst && c0 + cc < Cin;
-          v[e] += bld(xr, ok ? ((cbase + cc * H) * W + rw) * 4 : kOOB, 0);
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int i = i0 + e * kThreads + tid;
-        if (i < nst) {
-          const int cc = i / plane, rw = i - cc * plane;
-          halo[cc * ROWS * W + rw] = op.pre_relu ? fmaxf(v[e], 0.f) : v[e];
-        }
-      }
-    }
-    __syncthreads();
-    // (2) depthwise: one (channel, pixel) per thread when CC * BM <= threads
-    for (int i = tid; i < CC * BM; i += kThreads) {
-      const int cc = i / BM, mm = i - cc * BM;
-      const int m = m0 + mm, oh = m / Wo, ow = m - oh * Wo;
-      const int c = c0 + cc;
-      float v = 0.f;
-      if (c < Cin && m < howo) {
-        const float *wk = op.dw + c * taps;
-        const float *hb = halo + cc * ROWS * W;
-        for (int u = 0; u < kh; ++u) {
-          const int ih = oh + u - op.ph;
-          if (ih < ih_lo || ih >= ih_hi) continue;        // outside the image
-          for (int q = 0; q < kw; ++q) {
-            const int iw = ow + q - op.pw;
-            if (iw < 0 || iw >= W) continue;
-            v = fmaf(wk[u * kw + q], hb[(ih - ih_lo) * W + iw], v);
-          }
-        }
-      }
-      tb[cc * LDM + mm] = v;
-    }
-    __syncthreads();
-    // (3) pointwise chunk on MFMA
-#pragma unroll
-    for (int s8 = 0; s8 < 8; ++s8) {
-      if (4 * s8 < CC) {
-        const float av = tb[(4 * s8 + kq) * LDM + row16];
-#pragma unroll
-        for (int j = 0; j < MAXJ; ++j)
-          if (wave + kWaves * j < NB) acc[j] = mfma16x16x4(av, bw[s8][j], acc[j]);
-      }
-    }
-    __syncthreads();   // halo / tb are rewritten by the next chunk
-  }
-  // output tile [n][m] in LDS, then coalesced stores with bias
-#pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    const int nb = wave + kWaves * j;
-    if (nb < NB) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ob[(nb * 16 + row16) * LDM + 4 * kq + e] = acc[j][e];
+  // (1) this wave's weights -> its LDS region: depthwise [4 nks][KKP], then
+  //     pointwise rows 4 ks0 .. 4 (ks0 + nks) - 1, columns of this tile
+  float *wl = lds + wave * sep_wave_floats(op.CinP, K, op.sep_nbt);
+  float *pl = wl + nks * 4 * KKP;
+  {
+    const __amdgpu_buffer_rsrc_t dr = rsrc(op.dw, op.dw_bytes);
+    const int nd = nks * 4 * KKP, src = ks0 * 4 * KKP;
+    for (int e = 0; e < nd; e += 64)
+      if (e + lane < nd) lds_dma(dr, wl + e, (src + e + lane) * 4);
+    const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
+    const int np = nks * 4 * pitch;
+    for (int e = 0; e < np; e += 64) {
+      const int i = e + lane, row = i / pitch, col = i - row * pitch;
+      if (i < np) lds_dma(wr, pl + e, ((4 * ks0 + row) * op.Npad + nb0 * 16 + col) * 4);
     }
   }
+
+  // (2) input loads.  Lane column colA = ow0 - pw + j (and colA + 16 for the
+  //     K - 1 lanes whose second value is needed); out-of-image rows and
+  //     columns and channels past Cin read 0 (zero padding).
+  const int colA = ow0 - op.pw + j, colB = colA + 16;
+  const bool okA = colA >= 0 && colA < W, okB = j < K - 1 && colB >= 0 && colB < W;
+  auto issue = [&](int b, int k, float (&X)[KB][K][2]) {
+    const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[k]], op.in_bytes[k]);
+    const int cb = img * op.in_ctot[k] + op.in_coff[k] + 4 * ks0 + g;
+#pragma unroll
+    for (int s = 0; s < KB; ++s) {
+      const int kr = b * KB + s;                      // k-step relative to ks0
+      const bool cok = 4 * (ks0 + kr) + g < Cin;
+#pragma unroll
+      for (int u = 0; u < K; ++u) {
+        const int ih = oh + u - ph;
+        if (kr < nks && u < kh && ih >= 0 && ih < H) {   // uniform
+          const int row = ((cb + 4 * kr) * H + ih) * W;
+          X[s][u][0] = bld(xr, cok && okA ? (row + colA) * 4 : kOOB, 0);
+          X[s][u][1] = bld(xr, cok && okB ? (row + colB) * 4 : kOOB, 0);
+        } else {
+          X[s][u][0] = 0.f;
+          X[s][u][1] = 0.f;
+        }
+      }
+    }
+  };
+
+  floatx4 acc[NBT];
+#pragma unroll
+  for (int nb = 0; nb < NBT; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const bool relu_in = op.pre_relu != 0;
+  // depthwise filter of batch b from the summed inputs S, then its MFMAs
+  // (weights from LDS: the caller has waited for the copies)
+  auto finish = [&](int b, float (&S)[KB][K][2]) {
+#pragma unroll
+    for (int s = 0; s < KB; ++s) {
+      const int kr = b * KB + s;
+      if (kr >= nks) break;
+      const float *wc = wl + (kr * 4 + g) * KKP;
+      float d = 0.f;
+#pragma unroll
+      for (int u = 0; u < K; ++u) {
+        float xa = S[s][u][0], xb = S[s][u][1];
+        if (relu_in) { xa = fmaxf(xa, 0.f); xb = fmaxf(xb, 0.f); }
+        d = fmaf(wc[u * K], xa, d);
+        d = dw_taps(wc + u * K, xa, xb, d, std::make_integer_sequence<int, K - 1>{});
+      }
+      const float *bp = pl + (4 * kr + g) * pitch + j;
+#pragma unroll
+      for (int nb = 0; nb < NBT; ++nb)
+        if (nb < nbc) acc[nb] = mfma16x16x4(d, bp[nb * 16], acc[nb]);
+    }
+  };
+
+  if constexpr (SINGLE) {
+    float X[KB][K][2];
+    for (int b = 0; b * KB < nks; ++b) {
+      issue(b, 0, X);
+      lds_dma_wait();
+      finish(b, X);
+    }
+  } else {
+    float S[KB][K][2], X0[KB][K][2], X1[KB][K][2];
+    const int n_in = op.n_in;
+    for (int b = 0; b * KB < nks; ++b) {
+      issue(b, 0, X0);
+      for (int k = 0; k < n_in; k += 2) {
+        if (k + 1 < n_in) issue(b, k + 1, X1);
+#pragma unroll
+        for (int s = 0; s < KB; ++s)
+#pragma unroll
+          for (int u = 0; u < K; ++u)
+#pragma unroll
+            for (int p = 0; p < 2; ++p) S[s][u][p] = k == 0 ? X0[s][u][p] : S[s][u][p] + X0[s][u][p];
+        if (k + 1 >= n_in) break;
+        if (k + 2 < n_in) issue(b, k + 2, X0);
+#pragma unroll
+        for (int s = 0; s < KB; ++s)
+#pragma unroll
+          for (int u = 0; u < K; ++u)
+#pragma unroll
+            for (int p = 0; p < 2; ++p) S[s][u][p] += X1[s][u][p];
+      }
+      lds_dma_wait();
+      finish(b, S);
+    }
+  }
+  // a wave with no k-steps still waits for nothing in flight
+  lds_dma_wait();
+
+  // (3) partial sums of the 8 waves -> LDS [wave][column][pixel] (the region
+  //     held the weights: every wave must be done with them)
   __syncthreads();
-  for (int idx = tid; idx < op.Cout * BM; idx += kThreads) {
-    const int n = idx / BM, mm = idx - n * BM, m = m0 + mm;
-    if (m >= howo) continue;
-    float v = ob[n * LDM + mm] + op.bias[n];
+#pragma unroll
+  for (int nb = 0; nb < NBT; ++nb)
+    if (nb < nbc) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) lds[(wave * NBT * 16 + nb * 16 + j) * LDR + 4 * g + e] = acc[nb][e];
+    }
+  __syncthreads();
+  const int NC = nbc * 16;
+  for (int idx = tid; idx < NC * 16; idx += kThreads) {
+    const int col = idx >> 4, px = idx & 15;
+    const int n = nb0 * 16 + col, ow = ow0 + px;
+    if (ow >= Wo || n >= op.Cout) continue;
+    float v = op.bias[n];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v += lds[(w * NBT * 16 + col) * LDR + px];
     if (op.post_relu) v = fmaxf(v, 0.f);
-    st<COH>(route_ptr(a, op, n, img, m, howo), v);
+    st<COH>(route_ptr(a, op, n, img, oh * Wo + ow, howo), v);
   }
 }
 
@@ -475,7 +554,14 @@ __device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, in
         break;
       }
     case DK_SEP:
-      if constexpr (KV != KV_LIGHT) sep_tile<COH>(a, op, ti, lds);
+      if constexpr (KV != KV_LIGHT) {
+        const bool one = op.n_in == 1;
+        if (op.sep_k == 3) {
+          if (one) sep_tile<3, true, COH>(a, op, ti, lds); else sep_tile<3, false, COH>(a, op, ti, lds);
+        } else {
+          if (one) sep_tile<5, true, COH>(a, op, ti, lds); else sep_tile<5, false, COH>(a, op, ti, lds);
+        }
+      }
       break;
     case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true, lds); break;
     case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false, lds); break;
@@ -586,7 +672,7 @@ int op_lds_bytes(const DevOp &op) {
     TileShape s = tile_shape(op.tcfg);
     return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
   }
-  if (op.kind == DK_SEP) return sep_lds_floats(op) * (int)sizeof(float);
+  if (op.kind == DK_SEP) return sep_lds_bytes(op.CinP, op.sep_k, op.sep_nbt);
   if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
     return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
   return 0;

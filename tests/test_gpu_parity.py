@@ -298,6 +298,10 @@ def ragged_spec(batch):
             "sh": 1, "sw": 1, "ph": 1, "pw": 1, "pre_relu": 1, "post_relu": 0},
            {"name": "s2", "kind": "sepconv", "in": ["s1"], "cout": 13, "kh": 5, "kw": 5,
             "sh": 1, "sw": 1, "ph": 2, "pw": 2, "pre_relu": 1, "post_relu": 0},
+           {"name": "s3", "kind": "sepconv", "in": ["x"], "cout": 6, "kh": 1, "kw": 3,
+            "sh": 1, "sw": 1, "ph": 0, "pw": 1, "pre_relu": 1, "post_relu": 0},
+           {"name": "s4", "kind": "sepconv", "in": ["x", "x", "x"], "cout": 17, "kh": 5, "kw": 5,
+            "sh": 1, "sw": 1, "ph": 1, "pw": 1, "pre_relu": 1, "post_relu": 0},
            {"name": "mp", "kind": "maxpool", "in": ["x"], "kh": 3, "kw": 3, "sh": 2, "sw": 2,
             "ph": 1, "pw": 1},
            {"name": "ap", "kind": "avgpool", "in": ["s2"], "kh": 3, "kw": 3, "sh": 1, "sw": 1,
@@ -307,7 +311,7 @@ def ragged_spec(batch):
            {"name": "cat", "kind": "concat", "in": ["c3", "c4"]},
            {"name": "cat2", "kind": "concat", "in": ["c5", "mp"]}]
     return {"name": "ragged", "batch": batch, "inputs": [{"name": "x", "c": 13, "h": 9, "w": 11}],
-            "ops": ops, "outputs": ["ad", "mn", "cat", "cat2"]}
+            "ops": ops, "outputs": ["ad", "mn", "cat", "cat2", "s3", "s4"]}
 
 
 @pytest.mark.parametrize("batch", [1, 2])
@@ -318,9 +322,29 @@ def test_parity_ragged_shapes(batch):
     g = I.Graph(spec, ten)
     for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g),
               I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in ("c1", "c2", "c3", "c4")],
-                                                    [g.tid[n] for n in ("c5", "s1", "s2", "mp", "ap",
-                                                                        "ad", "mn")]],
+                                                    [g.tid[n] for n in ("c5", "s1", "s2", "s3", "s4", "mp",
+                                                                        "ap", "ad", "mn")]],
                                          [I.IOS_MERGE, I.IOS_CONCURRENT])):
         check(run(g, q, spec, ten), ref, "ragged")
         I.ios_schedule_destroy(q)
+    g.close()
+
+
+@pytest.mark.parametrize("nbt", ["1", "2", "3", "4"])
+def test_parity_every_sepconv_block_count(nbt, monkeypatch):
+    # output blocks of 16 channels per SEPCONV tile, forced instead of measured
+    monkeypatch.setenv("IOS_SEP_NBT", nbt)
+    for config in ["randwire", "nasnet"]:
+        spec, ten = case(config)
+        g = I.Graph(spec, ten)
+        for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY)):
+            check(run(g, q, spec, ten), reference(config), f"{config}/nbt{nbt}")
+            I.ios_schedule_destroy(q)
+        g.close()
+    spec = ragged_spec(2)
+    ten = W.make_tensors(spec, 4)
+    g = I.Graph(spec, ten)
+    q = sched(g, I.IOS_SCHED_GREEDY)
+    check(run(g, q, spec, ten), E.outputs(spec, ten), f"ragged/nbt{nbt}")
+    I.ios_schedule_destroy(q)
     g.close()

@@ -21,6 +21,17 @@ LIB_PATH = os.path.join(_HERE, "libios.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2011_01302_amd/build.py`")
 
+# One HIP runtime per process.  PyTorch-ROCm ships its own libamdhip64 and
+# links it by the unversioned name; if libios.so were loaded first it would
+# pull in the system runtime, torch would then load its copy as a second
+# runtime, and the two would not share the GPU (the second reports "no
+# ROCm-capable device").  Loading torch first makes libios bind to torch's
+# runtime by soname.
+try:
+    import torch  # noqa: F401
+except ImportError:   # no torch: libios uses the system HIP runtime
+    pass
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ------------------------------------------------------------------ constants

@@ -30,7 +30,8 @@ SOURCES = ["graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_kernel.hip"]
 def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(BUILD, src + ".o")
-    cmd = [HIPCC] + COMMON + (DEVICE if src.endswith(".hip") else ["-D__HIP_PLATFORM_AMD__"]) + \
+    # host sources are plain C++ against the HIP runtime headers (no device pass)
+    cmd = [HIPCC] + COMMON + (DEVICE if src.endswith(".hip") else ["-x", "c++", "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__"]) + \
         ["-c", path, "-o", obj]
     subprocess.check_call(cmd)
     return obj

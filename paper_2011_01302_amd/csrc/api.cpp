@@ -81,7 +81,7 @@ void ios_graph_destroy(ios_graph *g) {
     if (op.d_dw) hipFree(op.d_dw);
   }
   CompiledStage &s = g->scratch;
-  if (s.d_ops) hipFree(s.d_ops);
+  if (s.d_table) hipFree(s.d_table);
   if (s.d_ctr) hipFree(s.d_ctr);
   if (s.d_mw) hipFree(s.d_mw);
   if (s.d_mb) hipFree(s.d_mb);

@@ -85,7 +85,7 @@ double tile_work(const DevOp &d) {
   switch (d.kind) {
     case DK_CONV: {
       TileShape s = tile_shape(d.tcfg);
-      return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * d.kh * d.kw * d.CinP / s.wk;
+      return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * 16.0 * d.NG / s.wk;
     }
     case DK_SEP:
       return 16.0 * d.CinP * (d.sep_k * d.sep_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
@@ -109,13 +109,31 @@ void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool scratch) {
 
 }  // namespace
 
+void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out,
+                       int *ng, int *nb) {
+  const int taps = kh * kw, spt = (cin + 3) / 4, ks_total = taps * spt;
+  const int groups = (ks_total + 3) / 4, blocks = (cout + 15) / 16;
+  out.assign((size_t)blocks * groups * 256, 0.f);
+  for (int b = 0; b < blocks; ++b)
+    for (int g = 0; g < groups; ++g)
+      for (int kq = 0; kq < 4; ++kq)
+        for (int j = 0; j < 16; ++j)
+          for (int s = 0; s < 4; ++s) {
+            const int ks = 4 * g + s, tap = ks / spt, c = (ks - tap * spt) * 4 + kq, n = 16 * b + j;
+            if (ks >= ks_total || c >= cin || n >= cout) continue;
+            out[(((size_t)b * groups + g) * 64 + kq * 16 + j) * 4 + s] = w[((size_t)n * cin + c) * taps + tap];
+          }
+  *ng = groups;
+  *nb = blocks;
+}
+
 void free_stage(CompiledStage *cs) {
   if (!cs->owns) return;
-  if (cs->d_ops) hipFree(cs->d_ops);
+  if (cs->d_table) hipFree(cs->d_table);
   if (cs->d_ctr) hipFree(cs->d_ctr);
   if (cs->d_mw) hipFree(cs->d_mw);
   if (cs->d_mb) hipFree(cs->d_mb);
-  cs->d_ops = nullptr; cs->d_ctr = nullptr;
+  cs->d_table = nullptr; cs->d_ctr = nullptr;
   cs->d_mw = nullptr; cs->d_mb = nullptr;
 }
 
@@ -148,17 +166,10 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.pw = o0.d.pad_w + (KW - o0.d.kw) / 2;
     d.Cout = total;
     d.CinP = round_up(o0.cin, 4);
-    d.Npad = round_up(total, 64);
-    // tile shape: forced one, else the measured choice of the largest conv
-    int largest = ops[0];
-    for (int i : ops)
-      if (op_flops(g, g->ops[i]) > op_flops(g, g->ops[largest])) largest = i;
-    d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total)
-                                           : g->ops[largest].tcfg;
-    set_inputs(g, o0, d, sm);
-    // packed [KH*KW][CinP][Npad]: each op's taps placed centred
-    mw.assign((size_t)KH * KW * d.CinP * d.Npad, 0.f);
-    mb.assign(d.Npad, 0.f);
+    // merged kernel [total][cin][KH][KW]: each op's kernel centred, stacked
+    // along output channels in ascending unit id (the concat order)
+    std::vector<float> wm((size_t)total * o0.cin * KH * KW, 0.f);
+    mb.assign(round_up(total, 16), 0.f);
     int n0 = 0;
     d.n_routes = (int)ops.size();
     for (size_t r = 0; r < ops.size(); ++r) {
@@ -168,15 +179,23 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
         mb[n0 + co] = o.b[co];
         for (int ci = 0; ci < o.cin; ++ci)
           for (int u = 0; u < o.d.kh; ++u)
-            for (int v = 0; v < o.d.kw; ++v) {
-              int tap = (u + dh) * KW + (v + dwc);
-              mw[((size_t)tap * d.CinP + ci) * d.Npad + n0 + co] =
+            for (int v = 0; v < o.d.kw; ++v)
+              wm[(((size_t)(n0 + co) * o0.cin + ci) * KH + u + dh) * KW + v + dwc] =
                   o.w[(((size_t)co * o.cin + ci) * o.d.kh + u) * o.d.kw + v];
-            }
       }
       set_route(g, d, (int)r, n0, o.out, sm);
       n0 += o.d.cout;
     }
+    int nb = 0;
+    pack_conv_weights(wm.data(), total, o0.cin, KH, KW, mw, &d.NG, &nb);
+    d.Npad = nb * 16;
+    // tile shape: forced one, else the measured choice of the largest conv
+    int largest = ops[0];
+    for (int i : ops)
+      if (op_flops(g, g->ops[i]) > op_flops(g, g->ops[largest])) largest = i;
+    d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total)
+                                           : g->ops[largest].tcfg;
+    set_inputs(g, o0, d, sm);
     d.route_n0[d.n_routes] = total;
     d.w_bytes = (int32_t)(mw.size() * sizeof(float));
     dops.push_back(d);
@@ -192,9 +211,9 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.route_n0[1] = d.Cout;
       switch (o.d.kind) {
         case IOS_CONV:
-          d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad;
+          d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad; d.NG = o.NG;
           d.wpk = o.d_wpk; d.bias = o.d_bias;
-          d.w_bytes = (int32_t)((size_t)o.d.kh * o.d.kw * o.CinP * o.Npad * sizeof(float));
+          d.w_bytes = (int32_t)((size_t)(o.Npad / 16) * o.NG * 256 * sizeof(float));
           break;
         case IOS_SEPCONV:
           d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
@@ -285,19 +304,23 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     sorted.push_back(d);
     start.push_back(start.back() + d.n_tiles);
     persistent |= d.n_deps > 0;
-    big_conv |= d.kind == DK_CONV && d.tcfg != TC_16x16_K8;
+    big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg);
     has_sep |= d.kind == DK_SEP;
     lds = std::max(lds, op_lds_bytes(d));
   }
   cs->ops = sorted;
   cs->op_start = start;
   cs->slot_buf = sm.bufs;
-  cs->lds_bytes = lds;
+  // table: header, op_start, DevOps (the kernel copies it to LDS)
+  const int devop_off = (4 + n + 1 + 3) & ~3;
+  const int table_words = devop_off + n * kDevOpWords;
+  cs->lds_bytes = (kSlotWords + table_words) * (int)sizeof(int32_t) + lds;
+  if (cs->lds_bytes > kMaxLdsBytes) fail(IOS_E_UNSUPPORTED, "stage needs more LDS than a workgroup has");
   cs->persistent = persistent;
   cs->variant = big_conv ? KV_FULL : has_sep ? KV_SEP : KV_LIGHT;
   cs->grid = start.back();
   if (persistent) {
-    int cap = stage_capacity(cs->variant, lds);
+    int cap = stage_capacity(cs->variant, cs->lds_bytes);
     if (cap <= 0) fail(IOS_E_HIP, "cannot size the persistent launch of a stage with dependencies");
     cs->grid = std::min(cs->grid, cap);
   }
@@ -311,8 +334,14 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     cs->ops[0].wpk = cs->d_mw;
     cs->ops[0].bias = cs->d_mb;
   }
+  cs->table.assign(table_words, 0);
+  cs->table[0] = n;
+  cs->table[1] = start.back();
+  cs->table[2] = devop_off;
+  for (int i = 0; i <= n; ++i) cs->table[4 + i] = start[i];
+  std::memcpy(&cs->table[devop_off], cs->ops.data(), sizeof(DevOp) * n);
   size_t d0 = 0, d2 = 0;
-  grow_upload(&cs->d_ops, scratch ? &g->scratch_ops_cap : &d0, cs->ops, scratch);
+  grow_upload(&cs->d_table, scratch ? &g->scratch_ops_cap : &d0, cs->table, scratch);
   std::vector<int32_t> ctr(2 + kCtrStride * kCtrCopies, 0);
   grow_upload(&cs->d_ctr, scratch ? &g->scratch_ctr_cap : &d2, ctr, scratch);
 }
@@ -320,16 +349,14 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
 void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
                      hipStream_t stream) {
   StageArgs a{};
-  for (size_t i = 0; i < cs.slot_buf.size(); ++i) a.slot[i] = buf_ptr[cs.slot_buf[i]];
-  a.ops = cs.d_ops;
-  for (size_t i = 0; i < cs.op_start.size(); ++i) a.op_start[i] = cs.op_start[i];
+  a.n_slots = (int)cs.slot_buf.size();
+  for (int i = 0; i < a.n_slots; ++i) a.slot[i] = buf_ptr[cs.slot_buf[i]];
   a.ctr = cs.d_ctr;
   a.err = g->d_err;
-  a.n_tiles = cs.op_start.back();
-  a.n_ops = (int)cs.ops.size();
-  a.persistent = cs.persistent ? 1 : 0;
   a.spin_limit = 1 << 24;
-  hip_check(launch_stage(a, cs.grid, cs.lds_bytes, cs.variant, stream), "stage launch");
+  hip_check(launch_stage(cs.d_table, (int)cs.table.size(), a, cs.persistent, cs.grid, cs.lds_bytes,
+                         cs.variant, stream),
+            "stage launch");
 }
 
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,

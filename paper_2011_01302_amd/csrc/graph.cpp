@@ -109,6 +109,8 @@ int add_op(ios_graph *g, const ios_op_desc *d, const int32_t *in_ids, int n_in,
         fail(IOS_E_ARG, "bad kernel / stride / padding");
       if (kind == IOS_SEPCONV && (d->stride_h != 1 || d->stride_w != 1))
         fail(IOS_E_UNSUPPORTED, "SEPCONV needs stride 1");
+      if (kind == IOS_CONV && (d->kh > 16 || d->kw > 16))
+        fail(IOS_E_UNSUPPORTED, "conv windows larger than 16x16");
       if (kind == IOS_POOL_MAX && (d->pad_h >= d->kh || d->pad_w >= d->kw))
         fail(IOS_E_ARG, "max-pool padding must be smaller than the window");
       oh = out_size(t0.h, d->kh, d->stride_h, d->pad_h);
@@ -342,19 +344,6 @@ static void resolve_buffers(ios_graph *g) {
 
 static int round_up(int a, int b) { return (a + b - 1) / b * b; }
 
-// Packed conv weights: [kh*kw][CinP][Npad], k = tap * CinP + ci (tap-major),
-// zero for ci >= Cin and n >= Cout.
-static void pack_conv(const Op &op, std::vector<float> &wpk, std::vector<float> &bias) {
-  int taps = op.d.kh * op.d.kw, CinP = op.CinP, Npad = op.Npad;
-  wpk.assign((size_t)taps * CinP * Npad, 0.f);
-  for (int co = 0; co < op.d.cout; ++co)
-    for (int ci = 0; ci < op.cin; ++ci)
-      for (int t = 0; t < taps; ++t)
-        wpk[((size_t)t * CinP + ci) * Npad + co] = op.w[((size_t)co * op.cin + ci) * taps + t];
-  bias.assign(Npad, 0.f);
-  std::copy(op.b.begin(), op.b.end(), bias.begin());
-}
-
 template <class T>
 static T *upload(const std::vector<T> &v) {
   T *p = nullptr;
@@ -363,9 +352,6 @@ static T *upload(const std::vector<T> &v) {
   return p;
 }
 
-// Conv tile shape for an M x N output.  IOS_CONV_TILE=<0..3> in the
-// environment (read when a graph is finalized or a merged stage is built)
-// forces one shape for every conv, for tuning and for tests.
 // Largest number of 16-channel output blocks a SEPCONV tile can take (LDS).
 static int max_sep_nbt(const Op &op) {
   const int K = sep_window(op.d.kh, op.d.kw);
@@ -381,6 +367,9 @@ static int choose_sep_nbt(const Op &op) {
   return std::max(1, std::min(v, max_sep_nbt(op)));
 }
 
+// Conv tile shape for an M x N output before measurement.  IOS_CONV_TILE=<0..5>
+// in the environment (read when a graph is finalized or a merged stage is
+// built) forces one shape for every conv, for tuning and for tests.
 int choose_conv_tile(int64_t M, int N) {
   if (const char *e = std::getenv("IOS_CONV_TILE")) {
     int v = std::atoi(e);
@@ -391,7 +380,7 @@ int choose_conv_tile(int64_t M, int N) {
   if (t64 >= 2048) return TC_128x64;
   if (t64 >= 512) return TC_64x64_K2;
   if (t32 >= 256) return TC_32x32_K8;
-  return TC_16x16_K8;
+  return TC_16x32_K8;
 }
 
 void finalize_graph(ios_graph *g) {
@@ -405,7 +394,7 @@ void finalize_graph(ios_graph *g) {
     Op &op = g->ops[oi];
     if (op.d.kind == IOS_CONV) {
       op.CinP = round_up(op.cin, 4);
-      op.Npad = round_up(op.d.cout, 64);
+      op.Npad = round_up(op.d.cout, 16);
       op.tcfg = choose_conv_tile((int64_t)g->batch * op.ho * op.wo, op.d.cout);
     } else if (op.d.kind == IOS_SEPCONV) {
       op.CinP = round_up(op.cin, 4);
@@ -439,8 +428,10 @@ void ensure_device(ios_graph *g) {
   for (int oi : g->units) {
     Op &op = g->ops[oi];
     if (op.d.kind == IOS_CONV) {
-      std::vector<float> wpk, bias;
-      pack_conv(op, wpk, bias);
+      std::vector<float> wpk, bias(op.Npad, 0.f);
+      int nb = 0;
+      pack_conv_weights(op.w.data(), op.d.cout, op.cin, op.d.kh, op.d.kw, wpk, &op.NG, &nb);
+      std::copy(op.b.begin(), op.b.end(), bias.begin());
       op.d_wpk = upload(wpk);
       op.d_bias = upload(bias);
     } else if (op.d.kind == IOS_SEPCONV) {

@@ -44,23 +44,27 @@ enum DevKind : int32_t {
 // wave owns FM x FN blocks of 16x16 outputs and 1/WK of the reduction.
 enum TileCfg : int32_t {
   TC_16x16_K8 = 0,   // FM1 FN1 WM1 WN1 WK8
-  TC_32x32_K8 = 1,   // FM2 FN2 WM1 WN1 WK8
-  TC_32x64_K4 = 2,   // FM2 FN2 WM1 WN2 WK4
-  TC_64x64_K2 = 3,   // FM2 FN2 WM2 WN2 WK2
-  TC_128x64 = 4,     // FM2 FN2 WM4 WN2 WK1
-  TC_COUNT = 5,
+  TC_16x32_K8 = 1,   // FM1 FN2 WM1 WN1 WK8
+  TC_32x32_K8 = 2,   // FM2 FN2 WM1 WN1 WK8
+  TC_32x64_K4 = 3,   // FM2 FN2 WM1 WN2 WK4
+  TC_64x64_K2 = 4,   // FM2 FN2 WM2 WN2 WK2
+  TC_128x64 = 5,     // FM2 FN2 WM4 WN2 WK1
+  TC_COUNT = 6,
 };
 
 struct TileShape { int fm, fn, wm, wn, wk; };
 inline TileShape tile_shape(int cfg) {
   switch (cfg) {
     case TC_16x16_K8: return {1, 1, 1, 1, 8};
+    case TC_16x32_K8: return {1, 2, 1, 1, 8};
     case TC_32x32_K8: return {2, 2, 1, 1, 8};
     case TC_32x64_K4: return {2, 2, 1, 2, 4};
     case TC_64x64_K2: return {2, 2, 2, 2, 2};
     default: return {2, 2, 4, 2, 1};
   }
 }
+// Tile shapes the light kernel variant contains (one 16-pixel block per wave).
+inline bool tile_is_light(int cfg) { return cfg == TC_16x16_K8 || cfg == TC_16x32_K8; }
 inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
 inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * s.wn; }
 
@@ -93,7 +97,7 @@ constexpr int kEltPerTile = 4 * kThreads;
 constexpr int kPoolLdsFloats = 8192;
 
 // One operator of a compiled stage, as the kernel sees it.
-struct DevOp {
+struct alignas(16) DevOp {
   int32_t kind, tcfg;
   int32_t n_in;
   int32_t in_slot[kMaxIn], in_coff[kMaxIn], in_ctot[kMaxIn];
@@ -103,7 +107,8 @@ struct DevOp {
   int32_t kh, kw, sh, sw, ph, pw;
   int32_t pre_relu, post_relu;
   int32_t CinP;                // Cin rounded up to 4 (reduction per tap)
-  int32_t Npad;                // row length of the packed weights
+  int32_t Npad;                // SEP: row length of the pointwise weights; CONV: 16 x blocks
+  int32_t NG;                  // CONV: groups of 4 k-steps (K = taps x CinP = 16 NG, padded)
   int32_t tiles_m, tiles_n, n_tiles;
   int32_t n_routes;            // output column ranges -> destination buffers
   int32_t route_n0[kMaxRoutes + 1];
@@ -119,31 +124,42 @@ struct DevOp {
   int32_t sep_bpr;             // SEP: 16-pixel blocks per output row
   int32_t w_bytes;             // size of wpk in bytes
   int32_t dw_bytes;            // SEP: size of dw in bytes
-  const float *wpk;            // CONV: [kh*kw][CinP][Npad]; SEP: pointwise [CinP][Npad]
+  const float *wpk;            // CONV: see pack_conv_weights; SEP: pointwise [CinP][Npad]
   const float *bias;           // [Npad]
   const float *dw;             // SEP: depthwise [CinP][sep_kkp(K)], kh x kw taps at the top left of K x K
 };
 
+// A compiled stage's table in device memory (int32 words): a header
+// {n_ops, n_tiles, devop_off, 0}, op_start[n_ops + 1] (op i owns tiles
+// [op_start[i], op_start[i+1]) in tile order), zero padding to a multiple of
+// 4 words, then DevOp[n_ops] from word devop_off.  Every workgroup copies the
+// table and the launch's buffer pointers to LDS when it starts (one memory
+// round trip for all of its metadata).
+constexpr int kDevOpWords = (int)(sizeof(DevOp) / 4);
+constexpr int kSlotWords = 2 * kMaxSlots;   // LDS words holding the buffer pointers
+constexpr int kMaxLdsBytes = 160 * 1024;    // LDS of one workgroup (gfx950)
+
+// Kernel arguments besides the table: per-launch buffer pointers and the
+// intra-stage signalling state.
 struct StageArgs {
-  float *slot[kMaxSlots];
-  const DevOp *ops;    // in tile order: op i owns tiles [op_start[i], op_start[i+1])
-  int32_t op_start[kMaxStageOps + 1];
   int32_t *ctr;        // [1] workgroups finished, [2 + i + kCtrStride * r] tiles done of op i (copy r)
   int32_t *err;        // device error word
-  int32_t n_tiles;
-  int32_t n_ops;
-  int32_t persistent;  // 1 when some op waits for another op of the stage (grid <= capacity)
   int32_t spin_limit;  // polls before a dependency wait gives up
+  int32_t n_slots;
+  float *slot[kMaxSlots];
 };
 
 // Launch one stage (defined in the HIP translation unit).
 // Kernel variant of a stage (see the stage kernel): the smallest one that
 // contains every tile kind the stage uses.
 enum KernelVariant { KV_LIGHT = 0, KV_SEP = 1, KV_FULL = 2 };
-hipError_t launch_stage(const StageArgs &args, int grid, int lds_bytes, int variant, hipStream_t stream);
+// table / table_words: the compiled stage's table (a multiple of 4 words);
+// lds_bytes: the dynamic LDS, slots and table included.
+hipError_t launch_stage(const int32_t *table, int table_words, const StageArgs &args, bool persistent,
+                        int grid, int lds_bytes, int variant, hipStream_t stream);
 // Workgroups of `variant` with `lds_bytes` of LDS that fit on the device at once (0 if unknown).
 int stage_capacity(int variant, int lds_bytes);
-// Dynamic LDS a tile of `op` needs.
+// Dynamic LDS a tile of `op` needs (besides the slots and the table).
 int op_lds_bytes(const DevOp &op);
 
 // ------------------------------------------------------------------ host IR
@@ -177,7 +193,7 @@ struct Op {
   int block = -1, local = -1;    // block and bit inside the block
   int cin = 0, h = 0, wd = 0, ho = 0, wo = 0;
   // device copies (units only)
-  int CinP = 0, Npad = 0, tcfg = TC_32x32_K8;
+  int CinP = 0, Npad = 0, NG = 0, tcfg = TC_16x32_K8;
   int sep_nbt = 1;               // SEPCONV: output blocks of 16 channels per tile
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
 };
@@ -196,8 +212,9 @@ struct CompiledStage {
   bool persistent = false;       // some op waits for another: persistent launch
   int grid = 0;                  // workgroups launched
   int variant = 0;               // KernelVariant
+  std::vector<int32_t> table;    // header, op_start, DevOps (see kDevOpWords)
   // device copies (owned unless `scratch`)
-  DevOp *d_ops = nullptr;
+  int32_t *d_table = nullptr;
   int32_t *d_ctr = nullptr;
   float *d_mw = nullptr, *d_mb = nullptr;   // merged weights / bias
   bool owns = true;
@@ -257,6 +274,14 @@ bool stage_mergeable(const ios_graph *g, const std::vector<int> &ops);
 int64_t op_flops(const ios_graph *g, const Op &op);
 
 // exec.cpp
+// Conv weights w[cout][cin][kh][kw] in the layout the conv tile loads: for
+// each block of 16 output channels nb and group g of 4 k-steps (k-step ks =
+// tap * CinP/4 + channel/4, tap-major), 64 lanes x 4 floats, lane kq*16 + j
+// holding rows 4*(4g+s) + kq (s = 0..3) of column 16 nb + j, i.e. the B
+// operands of four consecutive 16x16x4 MFMAs.  Zero-padded to CinP and to 16
+// channels.  Sets *ng = groups, *nb = blocks.
+void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out,
+                       int *ng, int *nb);
 void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
                    bool scratch);
 void free_stage(CompiledStage *cs);

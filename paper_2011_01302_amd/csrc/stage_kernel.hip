@@ -43,10 +43,10 @@ __device__ __forceinline__ gcfloat *gp(const float *p) { return (gcfloat *)p; }
 // 64-bit address arithmetic per load; an offset at or past the resource's
 // size returns 0 (used for padding taps).
 constexpr int kBufFlags = 0x00020000;   // gfx9 descriptor word 3 (32-bit data)
-// Buffers are smaller than 1 GiB, so an offset of 2^30 or more reads 0; the
-// two "out of range" offsets below can be added without wrapping past 2^32.
+// Buffers are smaller than 1 GiB, so a per-lane offset of 2^30 or more reads
+// 0.  The range check covers the per-lane (VGPR) offset only, never the
+// scalar one: every offset that may leave the buffer goes in the VGPR offset.
 constexpr int kOOB = 1 << 30;           // masked pixel / padding tap
-constexpr int kOOBStep = (int)(1u << 31);  // k-step past the end of a tap
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, bytes, kBufFlags);
 }
@@ -68,27 +68,94 @@ __device__ __forceinline__ void st(float *p, float v) {
   else *p = v;
 }
 
-__device__ __forceinline__ float *route_ptr(const StageArgs &a, const DevOp &op, int n, int img,
+// Operator descriptors and buffer pointers live in LDS (the workgroup copies
+// them there when it starts).  U() reads a field that is the same for every
+// lane and moves it to a scalar register, so that descriptors, loop bounds
+// and buffer resources stay uniform.
+template <class T>
+__device__ __forceinline__ T U(const T &v) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8, "4- or 8-byte fields");
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+  } else {
+    const uint64_t x = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((int)(uint32_t)(x >> 32));
+    return __builtin_bit_cast(T, ((uint64_t)hi << 32) | lo);
+  }
+}
+
+// A descriptor's fields in scalar registers: lane i reads words i, 64 + i,
+// ... of the LDS copy, then v_readlane moves word w from lane w % 64 to
+// a scalar register (fields the caller never reads are dropped by the
+// compiler).  Every lane reading every word would be 64x the LDS traffic.
+// Arrays indexed by a run-time value are read from the LDS copy instead
+// (U(op.arr[k])), which keeps this copy in registers.
+__device__ __forceinline__ DevOp op_scalars(const DevOp &op) {
+  constexpr int NW = (kDevOpWords + 63) / 64;   // words per lane
+  const int *src = (const int *)&op;
+  const int lane = threadIdx.x & 63;
+  int v[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j) v[j] = lane + 64 * j < kDevOpWords ? src[lane + 64 * j] : 0;
+  DevOp o;
+  int *d = (int *)&o;
+#pragma unroll
+  for (int i = 0; i < kDevOpWords; ++i) d[i] = __builtin_amdgcn_readlane(v[i / 64], i & 63);
+  return o;
+}
+
+// The launch's buffer pointers (slot -> pointer), staged in LDS.  [] takes a
+// slot index that is the same for every lane (LDS read + readfirstlane, which
+// stays correct where some lanes are switched off, unlike v_readlane of a
+// lane that may be inactive); .p[] takes one that may differ between lanes.
+struct Slots {
+  float *const *p;
+  __device__ __forceinline__ float *operator[](int i) const { return U(p[i]); }
+};
+
+// Destination of output column n (the column differs between lanes, so a
+// merged conv's route arrays are read per lane; a single route is uniform).
+__device__ __forceinline__ float *route_ptr(const Slots &sl, const DevOp &op, const DevOp &o, int n, int img,
                                             int pix, int howo) {
+  const int nr = o.n_routes;
+  if (nr == 1)
+    return sl[o.route_slot[0]] +
+           ((size_t)img * o.route_ctot[0] + o.route_coff[0] + n) * howo + pix;
   int r = 0;
-  while (r + 1 < op.n_routes && n >= op.route_n0[r + 1]) ++r;
-  return a.slot[op.route_slot[r]] +
+  while (r + 1 < nr && n >= op.route_n0[r + 1]) ++r;
+  return sl.p[op.route_slot[r]] +
          ((size_t)img * op.route_ctot[r] + op.route_coff[r] + (n - op.route_n0[r])) * howo + pix;
 }
 
 // ------------------------------------------------------------------ conv
 
+__device__ __forceinline__ floatx4 bld4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Implicit-GEMM convolution tile: BM output pixels x BN output channels.
+// The reduction runs over k-steps of 4 input channels of one tap (tap-major),
+// in groups of 4 k-steps; the WK waves of a column split the groups evenly.
+// Per k-step a lane gathers one activation per 16-pixel block (pixel
+// lane % 16, channel 4 * step + lane / 16; padding taps and masked pixels
+// read 0 through the buffer range check), and per group one 16-byte load
+// brings the B operands of four consecutive MFMAs (pack_conv_weights).  A
+// wave keeps two chunks of CG groups in registers: the loads of chunk c + 1
+// are in flight while chunk c runs on the MFMA unit, and every load is issued
+// on a straight path so that each wait only covers the chunk it needs (a
+// wave with a single chunk skips the groups past its range instead).
 template <int FM, int FN, int WM, int WN, int WK, bool COH>
-__device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
+__device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN * WN, LDM = BM + 1;
+  constexpr int CG = FM * FN >= 2 ? 2 : 4;     // groups per register chunk
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
   const int wk = wave % WK, wmn = wave / WK, wm = wmn % WM, wn = wmn / WM;
-  const int tm = t / op.tiles_n, tn = t - tm * op.tiles_n;
-  const int Wo = op.Wo, howo = op.Ho * Wo, M = op.N * howo;
-  const int H = op.H, W = op.W, HW = H * W;
+  const int tm = t / o.tiles_n, tn = t - tm * o.tiles_n;
+  const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo;
+  const int H = o.H, W = o.W, HW = H * W;
   const int row16 = lane & 15, kq = lane >> 4;
-  const float *__restrict__ xin = a.slot[op.in_slot[0]];
 
   // epilogue outputs of this thread; their biases are loaded up front
   constexpr int EPT = (BM * BN + kThreads - 1) / kThreads;
@@ -96,20 +163,26 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
     int idx = tid + e * kThreads, n = tn * BN + idx / BM;
-    bpre[e] = (idx < BM * BN && n < op.Cout) ? op.bias[n] : 0.f;
+    bpre[e] = (idx < BM * BN && n < o.Cout) ? o.bias[n] : 0.f;
   }
 
-  int base[FM], ih0[FM], iw0[FM];
-  bool mv[FM];
+  // per 16-pixel block: offset of this lane's pixel (channel kq, tap 0,0)
+  // and the taps whose input row / column lies inside the image
+  const int kh = o.kh, kw = o.kw;
+  int pix[FM], rv[FM], cv[FM];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
-    int m = tm * BM + wm * 16 * FM + fm * 16 + row16;
-    mv[fm] = m < M;
-    int mm = mv[fm] ? m : 0;
-    int img = mm / howo, r = mm - img * howo, oh = r / Wo, ow = r - oh * Wo;
-    ih0[fm] = oh * op.sh - op.ph;
-    iw0[fm] = ow * op.sw - op.pw;
-    base[fm] = (img * op.in_ctot[0] + op.in_coff[0]) * HW;
+    const int m = tm * BM + wm * 16 * FM + fm * 16 + row16;
+    const bool ok = m < M;
+    const int mm = ok ? m : 0;
+    const int img = mm / howo, r = mm - img * howo, oh = r / Wo, ow = r - oh * Wo;
+    const int ih0 = oh * o.sh - o.ph, iw0 = ow * o.sw - o.pw;
+    pix[fm] = (img * o.in_ctot[0] + o.in_coff[0] + kq) * HW + ih0 * W + iw0;
+    int rb = 0, cb = 0;
+    for (int u = 0; u < kh; ++u) rb |= (ok && ih0 + u >= 0 && ih0 + u < H) << u;
+    for (int v = 0; v < kw; ++v) cb |= (iw0 + v >= 0 && iw0 + v < W) << v;
+    rv[fm] = rb;
+    cv[fm] = cb;
   }
 
   floatx4 acc[FM][FN];
@@ -118,113 +191,100 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // The reduction runs over chunks of U k-steps (4U input channels of one
-  // tap).  Chunks are split evenly over the WK waves; each wave keeps two
-  // or three chunks in registers, loading ahead while its MFMAs consume.
-  constexpr int U = (FM * FN == 1) ? 8 : 4;
-  const int CinP = op.CinP, Cin = op.Cin, Npad = op.Npad, kw = op.kw;
-  const int spt = CinP >> 2;                       // k-steps of 4 per tap
-  const int cpt = (spt + U - 1) / U;               // chunks per tap
-  const int total = op.kh * kw * cpt;
-  const int c0 = total * wk / WK, c1 = total * (wk + 1) / WK;
-  const __amdgpu_buffer_rsrc_t xr = rsrc(xin, op.in_bytes[0]);
-  const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
+  const int spt = o.CinP >> 2, KS = kh * kw * spt, NG = o.NG;
+  const int g0 = NG * wk / WK, g1 = NG * (wk + 1) / WK;
+  const int nc = (g1 - g0 + CG - 1) / CG;
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
   const int HW16 = HW * 16;                        // bytes between k-steps (4 channels)
-  const int NP16 = Npad * 16;                      // bytes between k-steps of weights
-  const int wcol = (tn * BN + wn * 16 * FN + row16) * 4;
-  const bool relu_in = op.pre_relu != 0;
-  const bool full_c = Cin == CinP;
+  const bool relu_in = o.pre_relu != 0;
+  const bool full_c = o.Cin == o.CinP;
+  const int cmax = o.Cin - kq;                    // channel 4 * cs + kq exists iff 4 * cs < cmax
+  // byte offset of each 16-column block's groups, -1 for blocks past the
+  // packed ones (columns past Cout)
+  const int nblk = o.Npad >> 4;
+  int nbo[FN];
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int nb = (tn * WN + wn) * FN + fn;
+    nbo[fn] = nb < nblk ? nb * NG * 1024 : -1;
+  }
 
-  // chunks are loaded in order c0, c0+1, ...: walk (tap row u, tap col v,
-  // chunk-in-tap cc) incrementally instead of dividing
-  int it_tap = c0 / cpt, it_cc = c0 - (c0 / cpt) * cpt;
-  int it_u = it_tap / kw, it_v = it_tap - it_u * kw;
-
-  float a0[U][FM], b0[U][FN], a1[U][FM], b1[U][FN], a2[FM * FN == 1 ? U : 1][FM], b2[FM * FN == 1 ? U : 1][FN];
-  // Per chunk each lane computes one activation offset per M-block (out of
-  // range for padding taps and masked pixels, so the load returns 0) and one
-  // weight offset; the k-step goes in the scalar offset, the 16-column block
-  // in the immediate.  Steps past the tap's channels are skipped uniformly.
-  auto load = [&](float (&A)[U][FM], float (&B)[U][FN]) {
-    const int cb = it_cc * 4 * U + kq;             // this lane's first channel
-    int voff[FM];
+  // walk of (tap row u, tap column v, channel step cs) over the k-steps, in
+  // load order, starting at this wave's first group; toff[fm] is the byte
+  // offset of this lane's input for the current tap (kOOB outside the image)
+  int w_tap = (4 * g0) / spt;
+  int w_cs = 4 * g0 - w_tap * spt;
+  int w_u = w_tap / kw, w_v = w_tap - (w_tap / kw) * kw;
+  int toff[FM];
+  auto set_tap = [&]() {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      int ih = ih0[fm] + it_u, iw = iw0[fm] + it_v;
-      bool ok = mv[fm] && ih >= 0 && ih < H && iw >= 0 && iw < W;
-      voff[fm] = ok ? (base[fm] + ih * W + iw + cb * HW) * 4 : kOOB;
-    }
-    const int wvoff = (it_tap * CinP + cb) * (Npad * 4) + wcol;
-    const int nval = min(U, spt - it_cc * U);      // k-steps of this chunk inside the tap
-    if (full_c) {
-#pragma unroll
-      for (int st_ = 0; st_ < U; ++st_) {
-        const int sa = st_ < nval ? st_ * HW16 : kOOBStep;   // uniform
-        const int sb = st_ < nval ? st_ * NP16 : 0;          // weights row: any valid one
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm) A[st_][fm] = bld(xr, voff[fm] + sa, 0);
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) B[st_][fn] = bld(wr, wvoff + fn * 64, sb);
-      }
-    } else {
-#pragma unroll
-      for (int st_ = 0; st_ < U; ++st_) {
-        const bool cok = st_ < nval && cb + 4 * st_ < Cin;
-        const int sb = st_ < nval ? st_ * NP16 : 0;
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm) A[st_][fm] = bld(xr, cok ? voff[fm] + st_ * HW16 : kOOB, 0);
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) B[st_][fn] = bld(wr, wvoff + fn * 64, sb);
-      }
-    }
-    if (++it_cc == cpt) {
-      it_cc = 0;
-      ++it_tap;
-      if (++it_v == kw) { it_v = 0; ++it_u; }
-    }
+    for (int fm = 0; fm < FM; ++fm)
+      toff[fm] = (w_u < kh && ((rv[fm] >> w_u) & (cv[fm] >> w_v) & 1)) ? (pix[fm] + w_u * W + w_v) * 4 : kOOB;
   };
-  auto compute = [&](const float (&A)[U][FM], const float (&B)[U][FN]) {
-    if (relu_in) {
+  set_tap();
+
+  typedef float AChunk[4 * CG][FM];
+  typedef floatx4 BChunk[CG][FN];
+  auto load = [&](AChunk &A, BChunk &B, int gb, bool last) {
 #pragma unroll
-      for (int st_ = 0; st_ < U; ++st_)
+    for (int gi = 0; gi < CG; ++gi) {
+      const int g = gb + gi;
+      const bool gok = g < g1;                     // uniform
+      if (last && !gok) break;                     // nothing is loaded after this chunk
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bool kok = gok && 4 * g + s < KS;    // uniform
+        const bool cok = full_c || 4 * w_cs < cmax;
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm)
+          A[gi * 4 + s][fm] = bld(xr, kok && cok && toff[fm] != kOOB ? toff[fm] + w_cs * HW16 : kOOB, 0);
+        if (++w_cs == spt) {
+          w_cs = 0;
+          if (++w_v == kw) { w_v = 0; ++w_u; }
+          set_tap();
+        }
+      }
 #pragma unroll
-          for (int fn = 0; fn < FN; ++fn)
-            acc[fm][fn] = mfma16x16x4(fmaxf(A[st_][fm], 0.f), B[st_][fn], acc[fm][fn]);
-    } else {
-#pragma unroll
-      for (int st_ = 0; st_ < U; ++st_)
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-          for (int fn = 0; fn < FN; ++fn)
-            acc[fm][fn] = mfma16x16x4(A[st_][fm], B[st_][fn], acc[fm][fn]);
+      for (int fn = 0; fn < FN; ++fn)
+        B[gi][fn] = bld4(wr, gok && nbo[fn] >= 0 ? nbo[fn] + g * 1024 + lane * 16 : kOOB, 0);
     }
   };
-  if constexpr (FM * FN == 1) {
-    // three chunks in flight
-    if (c0 < c1) load(a0, b0);
-    if (c0 + 1 < c1) load(a1, b1);
-    for (int ch = c0; ch < c1; ch += 3) {
-      if (ch + 2 < c1) load(a2, b2);
-      compute(a0, b0);
-      if (ch + 1 >= c1) break;
-      if (ch + 3 < c1) load(a0, b0);
-      compute(a1, b1);
-      if (ch + 2 >= c1) break;
-      if (ch + 4 < c1) load(a1, b1);
-      compute(a2, b2);
+  auto compute = [&](const AChunk &A, const BChunk &B, int gb) {
+#pragma unroll
+    for (int gi = 0; gi < CG; ++gi) {
+      if (gb + gi >= g1) break;                    // uniform
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+          const float x = relu_in ? fmaxf(A[gi * 4 + s][fm], 0.f) : A[gi * 4 + s][fm];
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(x, B[gi][fn][s], acc[fm][fn]);
+        }
     }
-  } else {
-    // two chunks in flight (larger tiles hold more accumulators)
-    if (c0 < c1) load(a0, b0);
-    for (int ch = c0; ch < c1; ch += 2) {
-      if (ch + 1 < c1) load(a1, b1);
-      compute(a0, b0);
-      if (ch + 1 >= c1) break;
-      if (ch + 2 < c1) load(a0, b0);
-      compute(a1, b1);
+  };
+  AChunk A0, A1;
+  BChunk B0, B1;
+  if (nc == 1) {
+    load(A0, B0, g0, true);
+    compute(A0, B0, g0);
+  } else if (nc > 1) {
+    load(A0, B0, g0, false);
+    load(A1, B1, g0 + CG, false);
+    for (int c = 0;; c += 2) {
+      compute(A0, B0, g0 + c * CG);
+      if (c + 2 >= nc) {
+        compute(A1, B1, g0 + (c + 1) * CG);
+        break;
+      }
+      load(A0, B0, g0 + (c + 2) * CG, false);
+      compute(A1, B1, g0 + (c + 1) * CG);
+      if (c + 3 >= nc) {
+        compute(A0, B0, g0 + (c + 2) * CG);
+        break;
+      }
+      load(A1, B1, g0 + (c + 3) * CG, false);
     }
   }
 
@@ -245,13 +305,13 @@ __device__ __forceinline__ void conv_tile(const StageArgs &a, const DevOp &op, i
     int idx = tid + e * kThreads;
     int col = idx / BM, row = idx - col * BM;
     int m = tm * BM + row, n = tn * BN + col;
-    if (idx >= BM * BN || m >= M || n >= op.Cout) continue;
+    if (idx >= BM * BN || m >= M || n >= o.Cout) continue;
     float v = bpre[e];
 #pragma unroll
     for (int w = 0; w < WK; ++w) v += lds[(w * BN + col) * LDM + row];
-    if (op.post_relu) v = fmaxf(v, 0.f);
-    int img = m / howo, pix = m - img * howo;
-    st<COH>(route_ptr(a, op, n, img, pix, howo), v);
+    if (o.post_relu) v = fmaxf(v, 0.f);
+    int img = m / howo, pix_ = m - img * howo;
+    st<COH>(route_ptr(sl, op, o, n, img, pix_, howo), v);
   }
 }
 
@@ -309,7 +369,7 @@ __device__ __forceinline__ void lds_dma_wait() {
 // with several inputs the next input's loads are in flight while the current
 // one is added.
 template <int K, bool SINGLE, bool COH>
-__device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, int t, float *lds) {
+__device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
   constexpr int KB = SINGLE ? (K == 3 ? 8 : 6) : (K == 3 ? 4 : 2);   // k-steps per batch
   constexpr int KKP = (K * K + 3) & ~3;               // floats per channel of depthwise weights
   constexpr int NBT = kSepMaxNB;
@@ -317,42 +377,42 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15, g = lane >> 4;
-  const int tm = t / op.tiles_n, tn = t - tm * op.tiles_n;
-  const int H = op.H, W = op.W, Ho = op.Ho, Wo = op.Wo, howo = Ho * Wo;
-  const int bpr = op.sep_bpr, per_img = Ho * bpr;
+  const int tm = t / o.tiles_n, tn = t - tm * o.tiles_n;
+  const int H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo, howo = Ho * Wo;
+  const int bpr = o.sep_bpr, per_img = Ho * bpr;
   const int img = tm / per_img, rr = tm - img * per_img;
   const int oh = rr / bpr, ow0 = (rr - oh * bpr) * 16;
-  const int NKS = op.CinP >> 2;
+  const int NKS = o.CinP >> 2;
   const int ks0 = NKS * wave / kWaves, nks = NKS * (wave + 1) / kWaves - ks0;
-  const int nb0 = tn * op.sep_nbt, nbc = min(op.sep_nbt, (op.Npad >> 4) - nb0);
+  const int nb0 = tn * o.sep_nbt, nbc = min(o.sep_nbt, (o.Npad >> 4) - nb0);
   const int pitch = nbc * 16;                         // pointwise weights row in LDS
-  const int Cin = op.Cin, kh = op.kh, ph = op.ph;
+  const int Cin = o.Cin, kh = o.kh, ph = o.ph;
 
   // (1) this wave's weights -> its LDS region: depthwise [4 nks][KKP], then
   //     pointwise rows 4 ks0 .. 4 (ks0 + nks) - 1, columns of this tile
-  float *wl = lds + wave * sep_wave_floats(op.CinP, K, op.sep_nbt);
+  float *wl = lds + wave * sep_wave_floats(o.CinP, K, o.sep_nbt);
   float *pl = wl + nks * 4 * KKP;
   {
-    const __amdgpu_buffer_rsrc_t dr = rsrc(op.dw, op.dw_bytes);
+    const __amdgpu_buffer_rsrc_t dr = rsrc(o.dw, o.dw_bytes);
     const int nd = nks * 4 * KKP, src = ks0 * 4 * KKP;
     for (int e = 0; e < nd; e += 64)
       if (e + lane < nd) lds_dma(dr, wl + e, (src + e + lane) * 4);
-    const __amdgpu_buffer_rsrc_t wr = rsrc(op.wpk, op.w_bytes);
+    const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
     const int np = nks * 4 * pitch;
     for (int e = 0; e < np; e += 64) {
       const int i = e + lane, row = i / pitch, col = i - row * pitch;
-      if (i < np) lds_dma(wr, pl + e, ((4 * ks0 + row) * op.Npad + nb0 * 16 + col) * 4);
+      if (i < np) lds_dma(wr, pl + e, ((4 * ks0 + row) * o.Npad + nb0 * 16 + col) * 4);
     }
   }
 
   // (2) input loads.  Lane column colA = ow0 - pw + j (and colA + 16 for the
   //     K - 1 lanes whose second value is needed); out-of-image rows and
   //     columns and channels past Cin read 0 (zero padding).
-  const int colA = ow0 - op.pw + j, colB = colA + 16;
+  const int colA = ow0 - o.pw + j, colB = colA + 16;
   const bool okA = colA >= 0 && colA < W, okB = j < K - 1 && colB >= 0 && colB < W;
   auto issue = [&](int b, int k, float (&X)[KB][K][2]) {
-    const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[k]], op.in_bytes[k]);
-    const int cb = img * op.in_ctot[k] + op.in_coff[k] + 4 * ks0 + g;
+    const __amdgpu_buffer_rsrc_t xr = rsrc(sl[U(op.in_slot[k])], U(op.in_bytes[k]));
+    const int cb = img * U(op.in_ctot[k]) + U(op.in_coff[k]) + 4 * ks0 + g;
 #pragma unroll
     for (int s = 0; s < KB; ++s) {
       const int kr = b * KB + s;                      // k-step relative to ks0
@@ -376,7 +436,7 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
 #pragma unroll
   for (int nb = 0; nb < NBT; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const bool relu_in = op.pre_relu != 0;
+  const bool relu_in = o.pre_relu != 0;
   // depthwise filter of batch b from the summed inputs S, then its MFMAs
   // (weights from LDS: the caller has waited for the copies)
   auto finish = [&](int b, float (&S)[KB][K][2]) {
@@ -409,7 +469,7 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
     }
   } else {
     float S[KB][K][2], X0[KB][K][2], X1[KB][K][2];
-    const int n_in = op.n_in;
+    const int n_in = o.n_in;
     for (int b = 0; b * KB < nks; ++b) {
       issue(b, 0, X0);
       for (int k = 0; k < n_in; k += 2) {
@@ -450,12 +510,12 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
   for (int idx = tid; idx < NC * 16; idx += kThreads) {
     const int col = idx >> 4, px = idx & 15;
     const int n = nb0 * 16 + col, ow = ow0 + px;
-    if (ow >= Wo || n >= op.Cout) continue;
-    float v = op.bias[n];
+    if (ow >= Wo || n >= o.Cout) continue;
+    float v = o.bias[n];
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += lds[(w * NBT * 16 + col) * LDR + px];
-    if (op.post_relu) v = fmaxf(v, 0.f);
-    st<COH>(route_ptr(a, op, n, img, oh * Wo + ow, howo), v);
+    if (o.post_relu) v = fmaxf(v, 0.f);
+    st<COH>(route_ptr(sl, op, o, n, img, oh * Wo + ow, howo), v);
   }
 }
 
@@ -465,32 +525,32 @@ __device__ __forceinline__ void sep_tile(const StageArgs &a, const DevOp &op, in
 // needs are staged in LDS with coalesced loads (each input value is read from
 // memory once), then every output is reduced from LDS.
 template <bool COH>
-__device__ __forceinline__ void pool_tile(const StageArgs &a, const DevOp &op, int t, bool is_max,
+__device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, bool is_max,
                                           float *lds) {
   const int tid = threadIdx.x;
-  const int C = op.Cout, H = op.H, W = op.W, Ho = op.Ho, Wo = op.Wo;
-  const int plane = t / op.tiles_per_plane, band = t - plane * op.tiles_per_plane;
+  const int C = o.Cout, H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo;
+  const int plane = t / o.tiles_per_plane, band = t - plane * o.tiles_per_plane;
   const int img = plane / C, c = plane - img * C;
-  const int oh0 = band * op.rows_per_tile, oh1 = min(Ho, oh0 + op.rows_per_tile);
-  const int ih_lo = max(0, oh0 * op.sh - op.ph);
-  const int ih_hi = min(H, (oh1 - 1) * op.sh - op.ph + op.kh);
-  const __amdgpu_buffer_rsrc_t xr = rsrc(a.slot[op.in_slot[0]], op.in_bytes[0]);
-  const int src = ((img * op.in_ctot[0] + op.in_coff[0] + c) * H + ih_lo) * W;
+  const int oh0 = band * o.rows_per_tile, oh1 = min(Ho, oh0 + o.rows_per_tile);
+  const int ih_lo = max(0, oh0 * o.sh - o.ph);
+  const int ih_hi = min(H, (oh1 - 1) * o.sh - o.ph + o.kh);
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  const int src = ((img * o.in_ctot[0] + o.in_coff[0] + c) * H + ih_lo) * W;
   const int n_in = (ih_hi - ih_lo) * W;
   for (int i = tid; i < n_in; i += kThreads) lds[i] = bld(xr, (src + i) * 4, 0);
   __syncthreads();
-  float *__restrict__ out = a.slot[op.route_slot[0]] +
-                            (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * Ho * Wo;
-  const float inv = 1.0f / (float)(op.kh * op.kw);
+  float *__restrict__ out = sl[o.route_slot[0]] +
+                            (size_t)(img * o.route_ctot[0] + o.route_coff[0] + c) * Ho * Wo;
+  const float inv = 1.0f / (float)(o.kh * o.kw);
   const int n_out = (oh1 - oh0) * Wo;
   for (int i = tid; i < n_out; i += kThreads) {
     const int oh = oh0 + i / Wo, ow = i - (i / Wo) * Wo;
     float acc = is_max ? -INFINITY : 0.f;
-    for (int u = 0; u < op.kh; ++u) {
-      const int ih = oh * op.sh + u - op.ph;
+    for (int u = 0; u < o.kh; ++u) {
+      const int ih = oh * o.sh + u - o.ph;
       if (ih < ih_lo || ih >= ih_hi) continue;     // outside the image
-      for (int q = 0; q < op.kw; ++q) {
-        const int iw = ow * op.sw + q - op.pw;
+      for (int q = 0; q < o.kw; ++q) {
+        const int iw = ow * o.sw + q - o.pw;
         if (iw < 0 || iw >= W) continue;
         const float v = lds[(ih - ih_lo) * W + iw];
         acc = is_max ? fmaxf(acc, v) : acc + v;
@@ -503,19 +563,19 @@ __device__ __forceinline__ void pool_tile(const StageArgs &a, const DevOp &op, i
 
 // Up to kEltPerTile contiguous outputs of one (image, channel) plane.
 template <bool COH>
-__device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, int t, bool mean) {
-  const int hw = op.Ho * op.Wo, C = op.Cout;
-  const int plane = t / op.tiles_per_plane, chunk = t - plane * op.tiles_per_plane;
+__device__ __forceinline__ void sum_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, bool mean) {
+  const int hw = o.Ho * o.Wo, C = o.Cout;
+  const int plane = t / o.tiles_per_plane, chunk = t - plane * o.tiles_per_plane;
   const int img = plane / C, c = plane - img * C;
   const int p0 = chunk * kEltPerTile;
-  float *__restrict__ out = a.slot[op.route_slot[0]] +
-                            (size_t)(img * op.route_ctot[0] + op.route_coff[0] + c) * hw;
+  float *__restrict__ out = sl[o.route_slot[0]] +
+                            (size_t)(img * o.route_ctot[0] + o.route_coff[0] + c) * hw;
   float s[kEltPerTile / kThreads];
 #pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) s[e] = 0.f;
-  for (int i = 0; i < op.n_in; ++i) {
-    const __amdgpu_buffer_rsrc_t r = rsrc(a.slot[op.in_slot[i]], op.in_bytes[i]);
-    const int base = (img * op.in_ctot[i] + op.in_coff[i] + c) * hw;
+  for (int i = 0; i < o.n_in; ++i) {
+    const __amdgpu_buffer_rsrc_t r = rsrc(sl[U(op.in_slot[i])], U(op.in_bytes[i]));
+    const int base = (img * U(op.in_ctot[i]) + U(op.in_coff[i]) + c) * hw;
 #pragma unroll
     for (int e = 0; e < kEltPerTile / kThreads; ++e) {
       const int pix = p0 + e * kThreads + threadIdx.x;
@@ -525,7 +585,7 @@ __device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, in
 #pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) {
     const int pix = p0 + e * kThreads + threadIdx.x;
-    if (pix < hw) st<COH>(out + pix, mean ? s[e] * op.inv_n : s[e]);
+    if (pix < hw) st<COH>(out + pix, mean ? s[e] * o.inv_n : s[e]);
   }
 }
 
@@ -533,74 +593,74 @@ __device__ __forceinline__ void sum_tile(const StageArgs &a, const DevOp &op, in
 
 // Kernel variants, chosen per stage by the host so that a stage only pays
 // the registers of the tile kinds it contains:
-//   KV_LIGHT  16x16 conv tiles, pooling, add / mean
+//   KV_LIGHT  16x16 and 16x32 conv tiles, pooling, add / mean
 //   KV_SEP    KV_LIGHT + SEPCONV tiles
 //   KV_FULL   every tile kind and conv tile shape
 template <bool COH, int KV>
-__device__ __forceinline__ void run_tile(const StageArgs &a, const DevOp &op, int ti, float *lds) {
-  switch (op.kind) {
+__device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const DevOp &o, int ti, float *lds) {
+  switch (o.kind) {
     case DK_CONV:
       if constexpr (KV != KV_FULL) {
-        conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds);
+        if (o.tcfg == TC_16x16_K8) conv_tile<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds);
+        else conv_tile<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds);
         break;
       } else {
-        switch (op.tcfg) {
-          case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(a, op, ti, lds); break;
-          case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(a, op, ti, lds); break;
-          case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(a, op, ti, lds); break;
-          case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(a, op, ti, lds); break;
-          default: conv_tile<2, 2, 4, 2, 1, COH>(a, op, ti, lds); break;
+        switch (o.tcfg) {
+          case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_16x32_K8: conv_tile<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(sl, op, o, ti, lds); break;
+          case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(sl, op, o, ti, lds); break;
+          default: conv_tile<2, 2, 4, 2, 1, COH>(sl, op, o, ti, lds); break;
         }
         break;
       }
     case DK_SEP:
       if constexpr (KV != KV_LIGHT) {
-        const bool one = op.n_in == 1;
-        if (op.sep_k == 3) {
-          if (one) sep_tile<3, true, COH>(a, op, ti, lds); else sep_tile<3, false, COH>(a, op, ti, lds);
+        const bool one = o.n_in == 1;
+        if (o.sep_k == 3) {
+          if (one) sep_tile<3, true, COH>(sl, op, o, ti, lds); else sep_tile<3, false, COH>(sl, op, o, ti, lds);
         } else {
-          if (one) sep_tile<5, true, COH>(a, op, ti, lds); else sep_tile<5, false, COH>(a, op, ti, lds);
+          if (one) sep_tile<5, true, COH>(sl, op, o, ti, lds); else sep_tile<5, false, COH>(sl, op, o, ti, lds);
         }
       }
       break;
-    case DK_POOL_MAX: pool_tile<COH>(a, op, ti, true, lds); break;
-    case DK_POOL_AVG: pool_tile<COH>(a, op, ti, false, lds); break;
-    case DK_ADD: sum_tile<COH>(a, op, ti, false); break;
-    default: sum_tile<COH>(a, op, ti, true); break;
+    case DK_POOL_MAX: pool_tile<COH>(sl, op, o, ti, true, lds); break;
+    case DK_POOL_AVG: pool_tile<COH>(sl, op, o, ti, false, lds); break;
+    case DK_ADD: sum_tile<COH>(sl, op, o, ti, false); break;
+    default: sum_tile<COH>(sl, op, o, ti, true); break;
   }
 }
 
 // One tile: find its op, wait for in-stage producers, compute, signal.
+// `tab` is the stage table in LDS.
 template <int KV>
-__device__ __forceinline__ void process_tile(const StageArgs &a, int t, bool remap, float *lds) {
-  const int tid = threadIdx.x;
-  int opi = 0;
-  while (opi + 1 < a.n_ops && t >= a.op_start[opi + 1]) ++opi;
-  int ti = t - a.op_start[opi];
-  if (remap) {
-    // Workgroup i runs on XCD i % 8.  Inside each op, give the op's
-    // workgroups on one XCD a contiguous range of its tiles, so neighbouring
-    // pixel tiles meet in the same L2 (a bijection on the op's tiles, so any
-    // placement stays correct; the op order across the stage is unchanged).
-    const int n = a.op_start[opi + 1] - a.op_start[opi];
-    const int q = n / kXcds, r = n - q * kXcds, x = ti % kXcds;
-    ti = x * q + min(x, r) + ti / kXcds;
-  }
-  // read-only for the whole launch: constant address space, so its fields
-  // are scalar (uniform) loads
-  typedef __attribute__((address_space(4))) const DevOp cDevOp;
-  const DevOp &op = *(const DevOp *)&((cDevOp *)a.ops)[opi];
+__device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl, const int32_t *tab, int t,
+                                             bool remap, float *lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  // op_start is non-decreasing with op_start[0] = 0: the tile's op is the
+  // last one starting at or before t.  Lane i holds op_start[i] and word
+  // i % 4 of the header; the values are taken out with v_readlane.
+  const int hv = tab[lane & 3], ov = tab[4 + lane];
+  const int n_ops = __builtin_amdgcn_readlane(hv, 0);
+  const int opi = __popcll(__ballot(lane < n_ops && t >= ov)) - 1;
+  const int s0 = __builtin_amdgcn_readlane(ov, opi);
+  int ti = t - s0;
+  const DevOp *ops = (const DevOp *)(tab + __builtin_amdgcn_readlane(hv, 2));
+  const DevOp &op = ops[opi];
 
-  if (op.n_deps) {
+  const DevOp o = op_scalars(op);
+  const int n_deps = o.n_deps, signal = o.signal;
+  if (n_deps) {
     // one thread polls the producers' counters with coherent loads (its own
     // copy of each, so the pollers of a stage spread over kCtrCopies memory
     // channels), then invalidates stale cache lines once; the workgroup
     // reads the producers' outputs only after that (barrier)
     if (tid == 0) {
       int32_t *mine = a.ctr + 2 + kCtrStride * (blockIdx.x % kCtrCopies);
-      for (int k = 0; k < op.n_deps; ++k) {
+      for (int k = 0; k < n_deps; ++k) {
         const int d = op.dep[k];
-        const int need = ((cDevOp *)a.ops)[d].n_tiles;
+        const int need = ops[d].n_tiles;
         int spins = 0;
         while (__hip_atomic_load(&mine[d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need) {
           __builtin_amdgcn_s_sleep(4);
@@ -616,10 +676,10 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, int t, bool rem
     __syncthreads();
   }
 
-  if (op.n_deps || op.signal) run_tile<true, KV>(a, op, ti, lds);
-  else run_tile<false, KV>(a, op, ti, lds);
+  if (n_deps || signal) run_tile<true, KV>(sl, op, o, ti, lds);
+  else run_tile<false, KV>(sl, op, o, ti, lds);
 
-  if (op.signal) {
+  if (signal) {
     // The tile's outputs were written with agent-coherent stores.  Every wave
     // waits until its stores have been performed, then one wave moves every
     // copy of the op's counter; a consumer reads the outputs only after
@@ -633,6 +693,18 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, int t, bool rem
   }
 }
 
+// Dynamic LDS of a launch: the buffer pointers (kSlotWords words), the stage
+// table, then the tile's own scratch.  A workgroup fills the first two with
+// one round of loads before its first tile.
+__device__ __forceinline__ float *stage_prologue(const int4 *__restrict__ table, int table_words,
+                                                 const StageArgs &a, int32_t *meta) {
+  int4 *dst = (int4 *)(meta + kSlotWords);
+  for (int i = threadIdx.x; i < (table_words >> 2); i += kThreads) dst[i] = table[i];
+  if (threadIdx.x < 2 * a.n_slots) meta[threadIdx.x] = ((const int32_t *)a.slot)[threadIdx.x];
+  __syncthreads();
+  return (float *)(meta + kSlotWords + table_words);
+}
+
 // A stage without in-stage dependencies runs one workgroup per tile.  A stage
 // with dependencies runs G workgroups, G no more than fit on the GPU at once
 // (occupancy of this kernel), so that all of them become resident even if
@@ -641,15 +713,23 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, int t, bool rem
 // tile has finished producers and an owner that has reached it, so every wait
 // ends, without a work queue or ticket atomics.  (A cooperative launch would
 // guarantee the residency too, but costs about 20 us per launch here.)
+// The table pointer and size come first so that they can be preloaded into
+// scalar registers at dispatch.
 template <int KV, bool PERSIST>
-__global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
-  extern __shared__ float lds[];
+__global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restrict__ table, int table_words,
+                                                             StageArgs a) {
+  extern __shared__ int4 lds_base[];
+  int32_t *meta = (int32_t *)lds_base;
+  float *lds = stage_prologue(table, table_words, a, meta);
+  const Slots sl{(float *const *)meta};
+  const int32_t *tab = meta + kSlotWords;
   if constexpr (!PERSIST) {
-    process_tile<KV>(a, blockIdx.x, true, lds);
+    process_tile<KV>(a, sl, tab, blockIdx.x, true, lds);
     return;
   }
-  for (int t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
-    process_tile<KV>(a, t, false, lds);
+  const int n_tiles = U(tab[1]), n_ops = U(tab[0]);
+  for (int t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    process_tile<KV>(a, sl, tab, t, false, lds);
     __syncthreads();   // the next tile reuses LDS
   }
   if (threadIdx.x == 0) {
@@ -660,7 +740,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(StageArgs a) {
       // last workgroup of the launch: leave the counters at zero for the
       // next launch on the stream
       for (int r = 0; r < kCtrCopies; ++r)
-        for (int i = 0; i < a.n_ops; ++i)
+        for (int i = 0; i < n_ops; ++i)
           __hip_atomic_store(&a.ctr[2 + i + kCtrStride * r], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&a.ctr[1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -703,20 +783,31 @@ int stage_capacity(int variant, int lds_bytes) {
   return per_cu * prop.multiProcessorCount;
 }
 
-hipError_t launch_stage(const StageArgs &args, int grid, int lds_bytes, int variant, hipStream_t stream) {
+hipError_t launch_stage(const int32_t *table, int table_words, const StageArgs &args, bool persistent,
+                        int grid, int lds_bytes, int variant, hipStream_t stream) {
+  // dynamic LDS above the default limit must be allowed per kernel, once
+  static int allowed[2][3] = {};
+  int &al = allowed[persistent ? 1 : 0][variant];
+  if (lds_bytes > 64 * 1024 && lds_bytes > al) {
+    hipError_t e = hipFuncSetAttribute(kernel_of(variant, persistent),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
+    if (e != hipSuccess) return e;
+    al = kMaxLdsBytes;
+  }
   const dim3 g(grid), block(kThreads);
-  if (args.persistent) {
+  const int4 *t = (const int4 *)table;
+  if (persistent) {
     switch (variant) {
-      case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, true>), g, block, lds_bytes, stream, args); break;
-      case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, true>), g, block, lds_bytes, stream, args); break;
-      default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, true>), g, block, lds_bytes, stream, args); break;
+      case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, true>), g, block, lds_bytes, stream, t, table_words, args); break;
+      case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, true>), g, block, lds_bytes, stream, t, table_words, args); break;
+      default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, true>), g, block, lds_bytes, stream, t, table_words, args); break;
     }
     return hipGetLastError();
   }
   switch (variant) {
-    case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, false>), g, block, lds_bytes, stream, args); break;
-    case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, false>), g, block, lds_bytes, stream, args); break;
-    default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, false>), g, block, lds_bytes, stream, args); break;
+    case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, false>), g, block, lds_bytes, stream, t, table_words, args); break;
+    case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, false>), g, block, lds_bytes, stream, t, table_words, args); break;
+    default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, false>), g, block, lds_bytes, stream, t, table_words, args); break;
   }
   return hipGetLastError();
 }

@@ -130,7 +130,7 @@ def test_parity_operator_merge(config, groups):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4"])
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5"])
 def test_parity_every_conv_tile_shape(tile, monkeypatch):
     monkeypatch.setenv("IOS_CONV_TILE", tile)
     for config in ["tiny", "inception", "squeeze"]:

@@ -21,9 +21,10 @@ BUILD = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result"]
-# device code: gfx950 only, packed fp32 arithmetic disabled
+# device code: gfx950 only, packed fp32 arithmetic disabled; the stage kernel's
+# first three argument words (table pointer and size) preloaded into SGPRs
 DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
-          "-packed-fp32-ops", "-munsafe-fp-atomics"]
+          "-packed-fp32-ops", "-munsafe-fp-atomics", "-mllvm", "-amdgpu-kernarg-preload-count=3"]
 SOURCES = ["graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_kernel.hip"]
 
 

@@ -278,6 +278,16 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.tiles_n = 1;
     }
     d.n_tiles = d.tiles_m * d.tiles_n;
+    const auto fd = [](int v) { return make_fdiv((uint32_t)std::max(1, v)); };
+    d.fd_tn = fd(d.tiles_n);
+    d.fd_howo = fd(d.Ho * d.Wo);
+    d.fd_wo = fd(d.Wo);
+    d.fd_spt = fd(d.CinP / 4);
+    d.fd_kw = fd(d.kw);
+    d.fd_pimg = fd(d.Ho * d.sep_bpr);
+    d.fd_bpr = fd(d.sep_bpr);
+    d.fd_tpp = fd(d.tiles_per_plane);
+    d.fd_c = fd(d.Cout);
   }
   // tile order: producers before consumers (depth), longer tiles first; the
   // ops are stored in that order so that each owns a contiguous tile range

@@ -96,6 +96,16 @@ __host__ __device__ inline int sep_lds_bytes(int CinP, int K, int nbt) {
 constexpr int kEltPerTile = 4 * kThreads;
 constexpr int kPoolLdsFloats = 8192;
 
+// Division by a run-time constant d >= 1 as a multiply-high and a shift:
+// n / d == (umulhi(n, mul) + n) >> shr for 0 <= n < 2^31 (Granlund and
+// Montgomery, PLDI 1994), so that the kernel never expands an integer divide.
+struct FDiv { uint32_t mul, shr; };
+inline FDiv make_fdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  return {(uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1), l};
+}
+
 // One operator of a compiled stage, as the kernel sees it.
 struct alignas(16) DevOp {
   int32_t kind, tcfg;
@@ -124,6 +134,12 @@ struct alignas(16) DevOp {
   int32_t sep_bpr;             // SEP: 16-pixel blocks per output row
   int32_t w_bytes;             // size of wpk in bytes
   int32_t dw_bytes;            // SEP: size of dw in bytes
+  // divisors of the tile and pixel decompositions (see FDiv)
+  FDiv fd_tn;                  // tiles_n
+  FDiv fd_howo, fd_wo;         // Ho * Wo, Wo
+  FDiv fd_spt, fd_kw;          // CONV: k-steps per tap, kw
+  FDiv fd_pimg, fd_bpr;        // SEP: 16-pixel blocks per image, per row
+  FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
   const float *wpk;            // CONV: see pack_conv_weights; SEP: pointwise [CinP][Npad]
   const float *bias;           // [Npad]
   const float *dw;             // SEP: depthwise [CinP][sep_kkp(K)], kh x kw taps at the top left of K x K

@@ -130,6 +130,11 @@ __device__ __forceinline__ float *route_ptr(const Slots &sl, const DevOp &op, co
 
 // ------------------------------------------------------------------ conv
 
+// n / d for 0 <= n < 2^31 with f = FDiv of d.
+__device__ __forceinline__ int fdiv(int n, FDiv f) {
+  return (int)((__umulhi((uint32_t)n, f.mul) + (uint32_t)n) >> f.shr);
+}
+
 __device__ __forceinline__ floatx4 bld4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
@@ -152,7 +157,7 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave
   const int wk = wave % WK, wmn = wave / WK, wm = wmn % WM, wn = wmn / WM;
-  const int tm = t / o.tiles_n, tn = t - tm * o.tiles_n;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
   const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo;
   const int H = o.H, W = o.W, HW = H * W;
   const int row16 = lane & 15, kq = lane >> 4;
@@ -175,7 +180,7 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
     const int m = tm * BM + wm * 16 * FM + fm * 16 + row16;
     const bool ok = m < M;
     const int mm = ok ? m : 0;
-    const int img = mm / howo, r = mm - img * howo, oh = r / Wo, ow = r - oh * Wo;
+    const int img = fdiv(mm, o.fd_howo), r = mm - img * howo, oh = fdiv(r, o.fd_wo), ow = r - oh * Wo;
     const int ih0 = oh * o.sh - o.ph, iw0 = ow * o.sw - o.pw;
     pix[fm] = (img * o.in_ctot[0] + o.in_coff[0] + kq) * HW + ih0 * W + iw0;
     int rb = 0, cb = 0;
@@ -213,9 +218,9 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
   // walk of (tap row u, tap column v, channel step cs) over the k-steps, in
   // load order, starting at this wave's first group; toff[fm] is the byte
   // offset of this lane's input for the current tap (kOOB outside the image)
-  int w_tap = (4 * g0) / spt;
+  int w_tap = fdiv(4 * g0, o.fd_spt);
   int w_cs = 4 * g0 - w_tap * spt;
-  int w_u = w_tap / kw, w_v = w_tap - (w_tap / kw) * kw;
+  int w_u = fdiv(w_tap, o.fd_kw), w_v = w_tap - w_u * kw;
   int toff[FM];
   auto set_tap = [&]() {
 #pragma unroll
@@ -310,7 +315,7 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
 #pragma unroll
     for (int w = 0; w < WK; ++w) v += lds[(w * BN + col) * LDM + row];
     if (o.post_relu) v = fmaxf(v, 0.f);
-    int img = m / howo, pix_ = m - img * howo;
+    int img = fdiv(m, o.fd_howo), pix_ = m - img * howo;
     st<COH>(route_ptr(sl, op, o, n, img, pix_, howo), v);
   }
 }
@@ -377,11 +382,11 @@ __device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15, g = lane >> 4;
-  const int tm = t / o.tiles_n, tn = t - tm * o.tiles_n;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
   const int H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo, howo = Ho * Wo;
   const int bpr = o.sep_bpr, per_img = Ho * bpr;
-  const int img = tm / per_img, rr = tm - img * per_img;
-  const int oh = rr / bpr, ow0 = (rr - oh * bpr) * 16;
+  const int img = fdiv(tm, o.fd_pimg), rr = tm - img * per_img;
+  const int oh = fdiv(rr, o.fd_bpr), ow0 = (rr - oh * bpr) * 16;
   const int NKS = o.CinP >> 2;
   const int ks0 = NKS * wave / kWaves, nks = NKS * (wave + 1) / kWaves - ks0;
   const int nb0 = tn * o.sep_nbt, nbc = min(o.sep_nbt, (o.Npad >> 4) - nb0);
@@ -529,8 +534,8 @@ __device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, cons
                                           float *lds) {
   const int tid = threadIdx.x;
   const int C = o.Cout, H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo;
-  const int plane = t / o.tiles_per_plane, band = t - plane * o.tiles_per_plane;
-  const int img = plane / C, c = plane - img * C;
+  const int plane = fdiv(t, o.fd_tpp), band = t - plane * o.tiles_per_plane;
+  const int img = fdiv(plane, o.fd_c), c = plane - img * C;
   const int oh0 = band * o.rows_per_tile, oh1 = min(Ho, oh0 + o.rows_per_tile);
   const int ih_lo = max(0, oh0 * o.sh - o.ph);
   const int ih_hi = min(H, (oh1 - 1) * o.sh - o.ph + o.kh);
@@ -544,7 +549,7 @@ __device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, cons
   const float inv = 1.0f / (float)(o.kh * o.kw);
   const int n_out = (oh1 - oh0) * Wo;
   for (int i = tid; i < n_out; i += kThreads) {
-    const int oh = oh0 + i / Wo, ow = i - (i / Wo) * Wo;
+    const int q = fdiv(i, o.fd_wo), oh = oh0 + q, ow = i - q * Wo;
     float acc = is_max ? -INFINITY : 0.f;
     for (int u = 0; u < o.kh; ++u) {
       const int ih = oh * o.sh + u - o.ph;
@@ -565,8 +570,8 @@ __device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, cons
 template <bool COH>
 __device__ __forceinline__ void sum_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, bool mean) {
   const int hw = o.Ho * o.Wo, C = o.Cout;
-  const int plane = t / o.tiles_per_plane, chunk = t - plane * o.tiles_per_plane;
-  const int img = plane / C, c = plane - img * C;
+  const int plane = fdiv(t, o.fd_tpp), chunk = t - plane * o.tiles_per_plane;
+  const int img = fdiv(plane, o.fd_c), c = plane - img * C;
   const int p0 = chunk * kEltPerTile;
   float *__restrict__ out = sl[o.route_slot[0]] +
                             (size_t)(img * o.route_ctot[0] + o.route_coff[0] + c) * hw;
@@ -695,12 +700,21 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl
 
 // Dynamic LDS of a launch: the buffer pointers (kSlotWords words), the stage
 // table, then the tile's own scratch.  A workgroup fills the first two with
-// one round of loads before its first tile.
+// one round of loads before its first tile: the table pointer and size are
+// preloaded into scalar registers at dispatch, and every load (table words,
+// pointer words from the kernel arguments) is issued before the first wait.
 __device__ __forceinline__ float *stage_prologue(const int4 *__restrict__ table, int table_words,
                                                  const StageArgs &a, int32_t *meta) {
+  const int tid = threadIdx.x, nv = table_words >> 2;
+  const bool ht = tid < nv, hs = tid < kSlotWords;
+  int4 tv{};
+  int sv = 0;
+  if (ht) tv = table[tid];
+  if (hs) sv = ((const int32_t *)a.slot)[tid];
   int4 *dst = (int4 *)(meta + kSlotWords);
-  for (int i = threadIdx.x; i < (table_words >> 2); i += kThreads) dst[i] = table[i];
-  if (threadIdx.x < 2 * a.n_slots) meta[threadIdx.x] = ((const int32_t *)a.slot)[threadIdx.x];
+  if (ht) dst[tid] = tv;
+  if (hs) meta[tid] = sv;
+  for (int i = tid + kThreads; i < nv; i += kThreads) dst[i] = table[i];   // tables over 8 KB
   __syncthreads();
   return (float *)(meta + kSlotWords + table_words);
 }

@@ -205,19 +205,21 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
   const bool relu_in = o.pre_relu != 0;
   const bool full_c = o.Cin == o.CinP;
   const int cmax = o.Cin - kq;                    // channel 4 * cs + kq exists iff 4 * cs < cmax
-  // byte offset of each 16-column block's groups, -1 for blocks past the
-  // packed ones (columns past Cout)
+  // per-lane byte offset of each 16-column block's groups (kOOB for blocks
+  // past the packed ones, i.e. columns past Cout)
   const int nblk = o.Npad >> 4;
-  int nbo[FN];
+  int nbv[FN];
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
     const int nb = (tn * WN + wn) * FN + fn;
-    nbo[fn] = nb < nblk ? nb * NG * 1024 : -1;
+    nbv[fn] = nb < nblk ? nb * NG * 1024 + lane * 16 : kOOB;
   }
 
   // walk of (tap row u, tap column v, channel step cs) over the k-steps, in
   // load order, starting at this wave's first group; toff[fm] is the byte
-  // offset of this lane's input for the current tap (kOOB outside the image)
+  // offset of this lane's input for the current tap (kOOB outside the image).
+  // kOOB plus any offset inside a buffer stays past its end, so every load
+  // offset below is one addition of a uniform term.
   int w_tap = fdiv(4 * g0, o.fd_spt);
   int w_cs = 4 * g0 - w_tap * spt;
   int w_u = fdiv(w_tap, o.fd_kw), w_v = w_tap - w_u * kw;
@@ -239,34 +241,48 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
       if (last && !gok) break;                     // nothing is loaded after this chunk
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        const bool kok = gok && 4 * g + s < KS;    // uniform
-        const bool cok = full_c || 4 * w_cs < cmax;
+        const int ka = gok && 4 * g + s < KS ? w_cs * HW16 : kOOB;   // uniform
 #pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-          A[gi * 4 + s][fm] = bld(xr, kok && cok && toff[fm] != kOOB ? toff[fm] + w_cs * HW16 : kOOB, 0);
+        for (int fm = 0; fm < FM; ++fm) {
+          int off = (int)((uint32_t)toff[fm] + (uint32_t)ka);   // up to 2^31: past any buffer
+          if (!full_c && 4 * w_cs >= cmax) off = kOOB;                 // channel past Cin
+          A[gi * 4 + s][fm] = bld(xr, off, 0);
+        }
         if (++w_cs == spt) {
           w_cs = 0;
           if (++w_v == kw) { w_v = 0; ++w_u; }
           set_tap();
         }
       }
+      const int kb = gok ? g * 1024 : kOOB;        // uniform
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn)
-        B[gi][fn] = bld4(wr, gok && nbo[fn] >= 0 ? nbo[fn] + g * 1024 + lane * 16 : kOOB, 0);
+      for (int fn = 0; fn < FN; ++fn) B[gi][fn] = bld4(wr, (int)((uint32_t)nbv[fn] + (uint32_t)kb), 0);
     }
   };
   auto compute = [&](const AChunk &A, const BChunk &B, int gb) {
+    if (relu_in) {
 #pragma unroll
-    for (int gi = 0; gi < CG; ++gi) {
-      if (gb + gi >= g1) break;                    // uniform
+      for (int gi = 0; gi < CG; ++gi) {
+        if (gb + gi >= g1) break;                  // uniform
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+        for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int fm = 0; fm < FM; ++fm) {
-          const float x = relu_in ? fmaxf(A[gi * 4 + s][fm], 0.f) : A[gi * 4 + s][fm];
+          for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(x, B[gi][fn][s], acc[fm][fn]);
-        }
+            for (int fn = 0; fn < FN; ++fn)
+              acc[fm][fn] = mfma16x16x4(fmaxf(A[gi * 4 + s][fm], 0.f), B[gi][fn][s], acc[fm][fn]);
+      }
+    } else {
+#pragma unroll
+      for (int gi = 0; gi < CG; ++gi) {
+        if (gb + gi >= g1) break;                  // uniform
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+            for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(A[gi * 4 + s][fm], B[gi][fn][s], acc[fm][fn]);
+      }
     }
   };
   AChunk A0, A1;

@@ -185,6 +185,35 @@ def write_traffic(args, fetch_dir, write_dir):
     print(json.dumps(out))
 
 
+def trace_summary(args, trace_dir):
+    """Stage-kernel launch durations of the timed loop from a rocprofv3
+    --kernel-trace run of this benchmark (run with --no-stage-times, so the
+    timed loop is the last steps x stages stage-kernel dispatches; bench.json
+    in the directory holds that run's JSON line)."""
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if "ios_stage_kernel" in r["Kernel_Name"]:
+                rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), int(r.get("Grid_Size_X") or r.get("Grid_Size")) // 512))
+    rows.sort()
+    meta = json.load(open(os.path.join(trace_dir, "bench.json")))
+    n = meta["steps"] * meta["stages"]
+    timed = rows[-n:]
+    dur = [e - b for b, e, _ in timed]
+    by_grid = {}
+    for (b, e, wg) in timed:
+        by_grid.setdefault(wg, []).append(e - b)
+    gaps = [timed[i + 1][0] - timed[i][1] for i in range(len(timed) - 1)]
+    out = {"launches": len(timed), "mean_ns": statistics.mean(dur), "median_ns": statistics.median(dur),
+           "by_workgroups": {str(k): {"launches": len(v), "median_ns": statistics.median(v)}
+                             for k, v in sorted(by_grid.items())},
+           "median_gap_ns": statistics.median(gaps) if gaps else None,
+           "step_us_of_that_run": meta["value"]}
+    print(json.dumps(out, indent=1))
+
+
 # NASNet at batch 32 is left out: its ~56k candidate stages at that batch take
 # longer to profile than a benchmark run should.
 SUITE = [("tiny", 1), ("inception", 1), ("inception", 16), ("randwire", 1), ("nasnet", 1),
@@ -272,6 +301,9 @@ def main():
     ap.add_argument("--suite", default="",
                     help="instead of the headline line, measure every configuration and batch "
                          "(IOS vs sequential vs greedy) and write a JSON report to this path")
+    ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
+                    help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
+                         "benchmark and exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
                          "into profiles/traffic_<workload>.json and exit")
@@ -281,6 +313,9 @@ def main():
               "build has no multi-GPU path (batch sharding is a design note only).", file=sys.stderr)
         sys.exit(2)
 
+    if args.trace_summary:
+        trace_summary(args, args.trace_summary)
+        return
     if args.traffic_from:
         write_traffic(args, *args.traffic_from)
         return

@@ -277,6 +277,137 @@ def run_suite(args):
         json.dump(report, f, indent=1)
 
 
+def _setup(I, W, torch, config, batch, seed):
+    import numpy as np
+    spec, ten = W.make(config, batch, seed)
+    g = I.Graph(spec, ten)
+    dev = "cuda:0"
+    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(dev) for t in spec["inputs"]]
+    shp = W.infer_shapes(spec)
+    outs = [torch.empty((batch,) + shp[o], device=dev) for o in spec["outputs"]]
+    return spec, g, ins, outs
+
+
+def _cost_table(I, g):
+    """The graph's last search's stage latencies: {(block, mask): {strategy: ns}}."""
+    import tempfile
+    with tempfile.NamedTemporaryFile("r", suffix=".jsonl") as f:
+        I.ios_schedule_dump_costs(g.handle, f.name)
+        rows = [json.loads(x) for x in open(f.name)]
+    tab = {}
+    for r in rows:
+        tab[(r["block"], r["mask"])] = {I.IOS_CONCURRENT: r["concurrent_ns"], I.IOS_MERGE: r["merge_ns"]}
+    return tab
+
+
+def run_next(args):
+    """Follow-up experiments on the same calls (written to args.next as JSON):
+    (1) strategy ablation -- IOS-Both, IOS-Parallel (no merge), IOS-Merge (no
+        concurrency), sequential and greedy, on every configuration at batch
+        1; the variants replay IOS-Both's measured stage latencies so that all
+        DP runs see the same costs (Sec. 6.1);
+    (2) batch specialisation -- schedules optimised at one batch size run at
+        the others (Inception block at 1 / 16, SqueezeNet stack at 1 / 32 /
+        128; Sec. 7.2);
+    (3) pruning -- r in {1, 2, 3}, s in {3, 8}: search time, stages measured,
+        latency of the schedule found (Sec. 4.3, Sec. 7.1)."""
+    import torch
+
+    import paper_2011_01302_amd as I
+    import workloads as W
+    stream = torch.cuda.current_stream().cuda_stream
+    out = {"ablation": [], "batch": [], "pruning": []}
+
+    def fast(o, config):
+        if config in ("randwire", "nasnet"):       # tens of thousands of candidate stages
+            o.warmup, o.reps, o.repeats = 1, 3, 1
+        return o
+
+    def timed(g, q, ins, outs, gflop):
+        steps = max(20, min(args.steps, int(2e5 / max(1.0, gflop * 1e3))))
+        us = time_steps(I, g, q, ins, outs, stream, 10, steps, torch)
+        assert I.ios_device_status(g.handle, stream) == 0
+        return round(us, 2)
+
+    # (1) strategy ablation
+    for config in W.CONFIG_NAMES:
+        spec, g, ins, outs = _setup(I, W, torch, config, 1, args.seed)
+        gflop = sum(w[0] + w[1] for w in unit_work(spec, 1).values()) / 1e9
+        row = {"config": config}
+        o = fast(I.ios_sched_opts_default(), config)
+        t0 = time.perf_counter()
+        q, pred = I.ios_schedule(g.handle, o)
+        row["search_s"] = round(time.perf_counter() - t0, 2)
+        tab = _cost_table(I, g)
+        row["ios_both"] = {"us": timed(g, q, ins, outs, gflop), "stages": len(I.ios_schedule_get(q)),
+                           "predicted_us": pred / 1e3}
+        I.ios_schedule_destroy(q)
+        for name, strat in (("ios_parallel", 1), ("ios_merge", 2)):
+            o = I.ios_sched_opts_default()
+            o.strategies = strat
+            q, pred = I.ios_schedule(g.handle, o, cost=lambda b, m, ids, t: tab[(b, m)][t])
+            row[name] = {"us": timed(g, q, ins, outs, gflop), "stages": len(I.ios_schedule_get(q)),
+                         "predicted_us": pred / 1e3}
+            I.ios_schedule_destroy(q)
+        for name, mode in (("sequential", I.IOS_SCHED_SEQUENTIAL), ("greedy", I.IOS_SCHED_GREEDY)):
+            o = I.ios_sched_opts_default()
+            o.mode = mode
+            q, pred = I.ios_schedule(g.handle, o)
+            row[name] = {"us": timed(g, q, ins, outs, gflop), "stages": len(I.ios_schedule_get(q))}
+            I.ios_schedule_destroy(q)
+        print(f"[next] ablation {config}: " + json.dumps({k: v["us"] for k, v in row.items() if isinstance(v, dict)}),
+              file=sys.stderr, flush=True)
+        out["ablation"].append(row)
+        g.close()
+
+    # (2) batch specialisation
+    for config, batches in (("inception", (1, 16)), ("squeeze", (1, 32, 128))):
+        scheds = {}
+        for b in batches:
+            spec, g, ins, outs = _setup(I, W, torch, config, b, args.seed)
+            q, _ = I.ios_schedule(g.handle, I.ios_sched_opts_default())
+            scheds[b] = [(ids, t) for ids, t in I.ios_schedule_get(q)]
+            I.ios_schedule_destroy(q)
+            g.close()
+            del ins, outs
+        for run_b in batches:
+            spec, g, ins, outs = _setup(I, W, torch, config, run_b, args.seed)
+            gflop = sum(w[0] + w[1] for w in unit_work(spec, run_b).values()) / 1e9
+            row = {"config": config, "run_batch": run_b}
+            for opt_b in batches:
+                q = I.ios_schedule_from_stages(g.handle, [ids for ids, _ in scheds[opt_b]],
+                                               [t for _, t in scheds[opt_b]])
+                row[f"optimised_for_bs{opt_b}"] = timed(g, q, ins, outs, gflop)
+                I.ios_schedule_destroy(q)
+            print(f"[next] batch {config} run at bs{run_b}: " + json.dumps(row), file=sys.stderr, flush=True)
+            out["batch"].append(row)
+            g.close()
+            del ins, outs
+            torch.cuda.empty_cache()
+
+    # (3) pruning
+    for config in ("inception", "randwire", "nasnet"):
+        spec, g, ins, outs = _setup(I, W, torch, config, 1, args.seed)
+        gflop = sum(w[0] + w[1] for w in unit_work(spec, 1).values()) / 1e9
+        for r in (1, 2, 3):
+            for s_ in (3, 8):
+                o = fast(I.ios_sched_opts_default(), config)
+                o.r, o.s = r, s_
+                t0 = time.perf_counter()
+                q, pred = I.ios_schedule(g.handle, o)
+                search = time.perf_counter() - t0
+                st, tr, ms = I.ios_schedule_stats(q)
+                row = {"config": config, "r": r, "s": s_, "search_s": round(search, 2), "states": st,
+                       "transitions": tr, "stages_measured": ms, "predicted_us": pred / 1e3,
+                       "us": timed(g, q, ins, outs, gflop), "stages": len(I.ios_schedule_get(q))}
+                I.ios_schedule_destroy(q)
+                print(f"[next] pruning " + json.dumps(row), file=sys.stderr, flush=True)
+                out["pruning"].append(row)
+        g.close()
+    with open(args.next, "w") as f:
+        json.dump(out, f, indent=1)
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -301,6 +432,9 @@ def main():
     ap.add_argument("--suite", default="",
                     help="instead of the headline line, measure every configuration and batch "
                          "(IOS vs sequential vs greedy) and write a JSON report to this path")
+    ap.add_argument("--next", default="",
+                    help="run the follow-up experiments (strategy ablation, batch specialisation, "
+                         "pruning sweep) and write a JSON report to this path")
     ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
                     help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
                          "benchmark and exit")
@@ -326,6 +460,9 @@ def main():
         __graft_entry__._load_build_module().build()
     if args.suite:
         run_suite(args)
+        return
+    if args.next:
+        run_next(args)
         return
     import numpy as np
     import torch

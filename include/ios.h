@@ -81,7 +81,7 @@ typedef struct ios_graph ios_graph;
 typedef struct ios_schedule_t ios_schedule_t;
 
 /* Create an empty graph for batch size `batch` (>= 1).  The paper tunes a
- * schedule per batch size (Sec. 6.2), so the batch is fixed per graph.
+ * schedule per batch size (Sec. 7.2), so the batch is fixed per graph.
  * *out receives a handle owned by the caller; free it with ios_graph_destroy.
  * Errors: IOS_E_ARG (batch < 1, out NULL), IOS_E_OOM. */
 int ios_graph_create(int32_t batch, ios_graph **out);

@@ -139,7 +139,7 @@ def test_merged_conv_equals_separate(kinds):
 
 
 def test_merged_asymmetric_3x1_1x3():
-    # the 3x1 / 1x3 pair padded to 3x3 (Sec. 6.2, last Inception block)
+    # the 3x1 / 1x3 pair padded to 3x3 (Sec. 7.2, last Inception block)
     x = rnd((1, 4, 8, 8), 40)
     convs = [{"w": rnd((2, 4, 3, 1), 41), "b": None, "pad": (1, 0), "post_relu": 1},
              {"w": rnd((3, 4, 1, 3), 42), "b": None, "pad": (0, 1), "post_relu": 1}]

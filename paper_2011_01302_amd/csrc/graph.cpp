@@ -2,6 +2,7 @@
 // copies of weights (Sec. 3 "Computation Graph"; Sec. 4.2 block-wise
 // optimisation).
 #include <algorithm>
+#include <chrono>
 #include <cstdlib>
 #include <cstring>
 #include <functional>
@@ -370,6 +371,11 @@ static int choose_sep_nbt(const Op &op) {
 // Conv tile shape for an M x N output before measurement.  IOS_CONV_TILE=<0..5>
 // in the environment (read when a graph is finalized or a merged stage is
 // built) forces one shape for every conv, for tuning and for tests.
+// Tuning: warm-up time before the first measurement, and the fraction of the
+// fastest time within which a conv tile shape with fewer workgroups is taken.
+constexpr int kTuneWarmMs = 50;
+constexpr double kTuneSlack = 0.03;
+
 int choose_conv_tile(int64_t M, int N) {
   if (const char *e = std::getenv("IOS_CONV_TILE")) {
     int v = std::atoi(e);
@@ -456,24 +462,44 @@ void ensure_device(ios_graph *g) {
   }
   hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
   g->device_ready = true;
+  const bool tune_conv = !std::getenv("IOS_CONV_TILE"), tune_sep = !std::getenv("IOS_SEP_NBT");
+  if ((tune_conv || tune_sep) && !g->units.empty()) {
+    // keep the GPU busy for a while first, so that the measurements below
+    // are taken at the clocks the stages will run at
+    const auto t0 = std::chrono::steady_clock::now();
+    while (std::chrono::steady_clock::now() - t0 < std::chrono::milliseconds(kTuneWarmMs))
+      profile_stage(g, {g->units[0]}, IOS_CONCURRENT, 0, 100, 1);
+  }
   // Tile shape of every conv, chosen by measuring the conv alone with each
-  // shape (unless IOS_CONV_TILE forces one).
-  if (!std::getenv("IOS_CONV_TILE")) {
+  // shape (unless IOS_CONV_TILE forces one).  Among the shapes within
+  // kTuneSlack of the fastest the one with the fewest workgroups wins: a
+  // stage runs the conv beside others, and fewer workgroups leave more room
+  // for them.
+  if (tune_conv) {
     for (int oi : g->units) {
       Op &op = g->ops[oi];
       if (op.d.kind != IOS_CONV) continue;
-      int best = op.tcfg;
-      int64_t best_ns = INT64_MAX;
+      const int64_t M = (int64_t)g->batch * op.ho * op.wo;
+      std::vector<std::pair<int64_t, int>> meas;   // (ns, cfg)
       for (int cfg = 0; cfg < TC_COUNT; ++cfg) {
         op.tcfg = cfg;
-        int64_t ns = profile_stage(g, {oi}, IOS_CONCURRENT, 2, 10, 3);
-        if (ns < best_ns) { best_ns = ns; best = cfg; }
+        meas.push_back({profile_stage(g, {oi}, IOS_CONCURRENT, 3, 20, 5), cfg});
       }
+      int64_t fastest = INT64_MAX;
+      for (auto &m : meas) fastest = std::min(fastest, m.first);
+      auto tiles = [&](int cfg) {
+        return ((M + tile_bm(cfg) - 1) / tile_bm(cfg)) * ((op.d.cout + tile_bn(cfg) - 1) / tile_bn(cfg));
+      };
+      int best = -1;
+      for (auto &m : meas)
+        if (m.first <= fastest + (int64_t)(fastest * kTuneSlack) &&
+            (best < 0 || tiles(m.second) < tiles(best)))
+          best = m.second;
       op.tcfg = best;
     }
   }
   // Output blocks per SEPCONV tile, likewise measured (unless IOS_SEP_NBT).
-  if (!std::getenv("IOS_SEP_NBT")) {
+  if (tune_sep) {
     for (int oi : g->units) {
       Op &op = g->ops[oi];
       if (op.d.kind != IOS_SEPCONV) continue;

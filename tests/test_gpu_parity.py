@@ -35,8 +35,17 @@ def reference(config, batch=1, seed=0):
     return E.outputs(spec, ten)
 
 
-def run(g, q, spec, ten, stream=0):
-    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(DEV) for t in spec["inputs"]]
+def device_input(a, offset=0):
+    """`a` on the device, starting `offset` floats into its allocation (so
+    that offset 1..3 gives a base address off a 16-byte boundary)."""
+    flat = torch.from_numpy(np.ascontiguousarray(a)).reshape(-1)
+    buf = torch.empty(flat.numel() + offset, dtype=torch.float32, device=DEV)
+    buf[offset:].copy_(flat.to(DEV))
+    return buf[offset:].view(a.shape)
+
+
+def run(g, q, spec, ten, stream=0, offset=0):
+    ins = [device_input(ten[t["name"]], offset) for t in spec["inputs"]]
     shp = W.infer_shapes(spec)
     outs = [torch.full((g.batch,) + shp[o], float("nan"), device=DEV) for o in spec["outputs"]]
     I.ios_run(g.handle, q, [t.data_ptr() for t in ins], [o.data_ptr() for o in outs], stream)
@@ -314,8 +323,13 @@ def ragged_spec(batch):
             "ops": ops, "outputs": ["ad", "mn", "cat", "cat2", "s3", "s4"]}
 
 
-@pytest.mark.parametrize("batch", [1, 2])
-def test_parity_ragged_shapes(batch):
+# tile None: shapes chosen by measurement, else forced; offset: inputs start
+# 1 or 3 floats past a 16-byte boundary
+@pytest.mark.parametrize("batch,tile,offset", [(1, None, 0), (2, None, 0), (1, "1", 1), (1, "0", 3),
+                                               (2, "4", 1)])
+def test_parity_ragged_shapes(batch, tile, offset, monkeypatch):
+    if tile is not None:
+        monkeypatch.setenv("IOS_CONV_TILE", tile)
     spec = ragged_spec(batch)
     ten = W.make_tensors(spec, 3)
     ref = E.outputs(spec, ten)
@@ -325,7 +339,21 @@ def test_parity_ragged_shapes(batch):
                                                     [g.tid[n] for n in ("c5", "s1", "s2", "s3", "s4", "mp",
                                                                         "ap", "ad", "mn")]],
                                          [I.IOS_MERGE, I.IOS_CONCURRENT])):
-        check(run(g, q, spec, ten), ref, "ragged")
+        check(run(g, q, spec, ten, offset=offset), ref, "ragged")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
+@pytest.mark.parametrize("tile", ["0", "1", "4"])
+def test_parity_conv_tiles_batched_small(tile, monkeypatch):
+    """Forced conv tile shapes over several small images (the 16-pixel
+    blocks of an 8x8 plane never span two images)."""
+    monkeypatch.setenv("IOS_CONV_TILE", tile)
+    spec, ten = case("tiny", 3)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), block_stages(g)):
+        check(run(g, q, spec, ten), ref, f"tiny/bs3/tile{tile}")
         I.ios_schedule_destroy(q)
     g.close()
 

@@ -150,7 +150,7 @@ __device__ __forceinline__ floatx4 bld4(__amdgpu_buffer_rsrc_t r, int voff, int 
 // are in flight while chunk c runs on the MFMA unit, and every load is issued
 // on a straight path so that each wait only covers the chunk it needs (a
 // wave with a single chunk skips the groups past its range instead).
-template <int FM, int FN, int WM, int WN, int WK, bool COH>
+template <int FM, int FN, int WM, int WN, int WK, bool COH, bool RELU, bool FULLC>
 __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN * WN, LDM = BM + 1;
   constexpr int CG = FM * FN >= 2 ? 2 : 4;     // groups per register chunk
@@ -196,14 +196,12 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  const int spt = o.CinP >> 2, KS = kh * kw * spt, NG = o.NG;
+  const int spt = o.CinP >> 2, NG = o.NG;
   const int g0 = NG * wk / WK, g1 = NG * (wk + 1) / WK;
   const int nc = (g1 - g0 + CG - 1) / CG;
   const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
   const int HW16 = HW * 16;                        // bytes between k-steps (4 channels)
-  const bool relu_in = o.pre_relu != 0;
-  const bool full_c = o.Cin == o.CinP;
   const int cmax = o.Cin - kq;                    // channel 4 * cs + kq exists iff 4 * cs < cmax
   // per-lane byte offset of each 16-column block's groups (kOOB for blocks
   // past the packed ones, i.e. columns past Cout)
@@ -217,12 +215,16 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
 
   // walk of (tap row u, tap column v, channel step cs) over the k-steps, in
   // load order, starting at this wave's first group; toff[fm] is the byte
-  // offset of this lane's input for the current tap (kOOB outside the image).
-  // kOOB plus any offset inside a buffer stays past its end, so every load
-  // offset below is one addition of a uniform term.
+  // offset of this lane's input, channel kq, for the current tap (kOOB
+  // outside the image and past the last tap) and w_ka the uniform offset of
+  // channel step cs.  A load takes toff in its per-lane offset, which the
+  // buffer range check covers, and w_ka in its scalar offset, which it does
+  // not: a lane either reads inside the buffer (a valid tap and channel) or
+  // has a per-lane offset past its end, so no unchecked address leaves it.
   int w_tap = fdiv(4 * g0, o.fd_spt);
   int w_cs = 4 * g0 - w_tap * spt;
   int w_u = fdiv(w_tap, o.fd_kw), w_v = w_tap - w_u * kw;
+  int w_ka = w_cs * HW16;
   int toff[FM];
   auto set_tap = [&]() {
 #pragma unroll
@@ -233,6 +235,8 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
 
   typedef float AChunk[4 * CG][FM];
   typedef floatx4 BChunk[CG][FN];
+  // A of groups past the wave's range is loaded but never used (compute
+  // stops at g1), and k-steps past the last tap read 0 (their B is 0 too).
   auto load = [&](AChunk &A, BChunk &B, int gb, bool last) {
 #pragma unroll
     for (int gi = 0; gi < CG; ++gi) {
@@ -241,15 +245,16 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
       if (last && !gok) break;                     // nothing is loaded after this chunk
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        const int ka = gok && 4 * g + s < KS ? w_cs * HW16 : kOOB;   // uniform
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm) {
-          int off = (int)((uint32_t)toff[fm] + (uint32_t)ka);   // up to 2^31: past any buffer
-          if (!full_c && 4 * w_cs >= cmax) off = kOOB;                 // channel past Cin
-          A[gi * 4 + s][fm] = bld(xr, off, 0);
+          int off = toff[fm];
+          if constexpr (!FULLC) off = 4 * w_cs < cmax ? off : kOOB;   // channel past Cin
+          A[gi * 4 + s][fm] = bld(xr, off, w_ka);
         }
+        w_ka += HW16;
         if (++w_cs == spt) {
           w_cs = 0;
+          w_ka = 0;
           if (++w_v == kw) { w_v = 0; ++w_u; }
           set_tap();
         }
@@ -260,29 +265,17 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
     }
   };
   auto compute = [&](const AChunk &A, const BChunk &B, int gb) {
-    if (relu_in) {
 #pragma unroll
-      for (int gi = 0; gi < CG; ++gi) {
-        if (gb + gi >= g1) break;                  // uniform
+    for (int gi = 0; gi < CG; ++gi) {
+      if (gb + gi >= g1) break;                    // uniform
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
-          for (int fm = 0; fm < FM; ++fm)
+        for (int fm = 0; fm < FM; ++fm) {
+          const float a = RELU ? fmaxf(A[gi * 4 + s][fm], 0.f) : A[gi * 4 + s][fm];
 #pragma unroll
-            for (int fn = 0; fn < FN; ++fn)
-              acc[fm][fn] = mfma16x16x4(fmaxf(A[gi * 4 + s][fm], 0.f), B[gi][fn][s], acc[fm][fn]);
-      }
-    } else {
-#pragma unroll
-      for (int gi = 0; gi < CG; ++gi) {
-        if (gb + gi >= g1) break;                  // uniform
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-            for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(A[gi * 4 + s][fm], B[gi][fn][s], acc[fm][fn]);
-      }
+          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16x16x4(a, B[gi][fn][s], acc[fm][fn]);
+        }
     }
   };
   AChunk A0, A1;
@@ -617,22 +610,36 @@ __device__ __forceinline__ void sum_tile(const Slots &sl, const DevOp &op, const
 //   KV_LIGHT  16x16 and 16x32 conv tiles, pooling, add / mean
 //   KV_SEP    KV_LIGHT + SEPCONV tiles
 //   KV_FULL   every tile kind and conv tile shape
+// A conv tile with the input ReLU and the channel check resolved at compile
+// time (no branch between its loads and MFMAs).
+template <int FM, int FN, int WM, int WN, int WK, bool COH>
+__device__ __forceinline__ void conv_any(const Slots &sl, const DevOp &op, const DevOp &o, int ti, float *lds) {
+  const bool full = o.Cin == o.CinP;
+  if (o.pre_relu) {
+    if (full) conv_tile<FM, FN, WM, WN, WK, COH, true, true>(sl, op, o, ti, lds);
+    else conv_tile<FM, FN, WM, WN, WK, COH, true, false>(sl, op, o, ti, lds);
+  } else {
+    if (full) conv_tile<FM, FN, WM, WN, WK, COH, false, true>(sl, op, o, ti, lds);
+    else conv_tile<FM, FN, WM, WN, WK, COH, false, false>(sl, op, o, ti, lds);
+  }
+}
+
 template <bool COH, int KV>
 __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const DevOp &o, int ti, float *lds) {
   switch (o.kind) {
     case DK_CONV:
       if constexpr (KV != KV_FULL) {
-        if (o.tcfg == TC_16x16_K8) conv_tile<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds);
-        else conv_tile<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds);
+        if (o.tcfg == TC_16x16_K8) conv_any<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds);
+        else conv_any<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds);
         break;
       } else {
         switch (o.tcfg) {
-          case TC_16x16_K8: conv_tile<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
-          case TC_16x32_K8: conv_tile<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
-          case TC_32x32_K8: conv_tile<2, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
-          case TC_32x64_K4: conv_tile<2, 2, 1, 2, 4, COH>(sl, op, o, ti, lds); break;
-          case TC_64x64_K2: conv_tile<2, 2, 2, 2, 2, COH>(sl, op, o, ti, lds); break;
-          default: conv_tile<2, 2, 4, 2, 1, COH>(sl, op, o, ti, lds); break;
+          case TC_16x16_K8: conv_any<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_16x32_K8: conv_any<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_32x32_K8: conv_any<2, 2, 1, 1, 8, COH>(sl, op, o, ti, lds); break;
+          case TC_32x64_K4: conv_any<2, 2, 1, 2, 4, COH>(sl, op, o, ti, lds); break;
+          case TC_64x64_K2: conv_any<2, 2, 2, 2, 2, COH>(sl, op, o, ti, lds); break;
+          default: conv_any<2, 2, 4, 2, 1, COH>(sl, op, o, ti, lds); break;
         }
         break;
       }

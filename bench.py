@@ -438,6 +438,10 @@ def main():
     ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
                     help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
                          "benchmark and exit")
+    ap.add_argument("--plan-from", default="", metavar="BENCH_JSON",
+                    help="replay the schedule and conv tile shapes of an earlier run (the last JSON "
+                         "line of this file) instead of searching: for profiler runs, whose added "
+                         "per-launch cost would change the search's choices")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
                          "into profiles/traffic_<workload>.json and exit")
@@ -479,13 +483,26 @@ def main():
     outs = [torch.empty((args.batch,) + shp[o], device=dev) for o in spec["outputs"]]
     stream = torch.cuda.current_stream().cuda_stream
 
-    # Algorithm 1 with on-device stage profiling
-    opts = I.ios_sched_opts_default()
-    opts.r, opts.s = args.r, args.s
-    t0 = time.perf_counter()
-    q, pred_ns = I.ios_schedule(g.handle, opts)
-    search_s = time.perf_counter() - t0
-    states, transitions, measured = I.ios_schedule_stats(q)
+    conv_units = [op["name"] for op in spec["ops"] if op["kind"] == "conv"]
+    if args.plan_from:
+        # the earlier run's conv tile shapes and stages, no search
+        plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{")][-1]
+        for name, shape in plan["tiles"].items():
+            I.ios_set_conv_tile(g.handle, g.tid[name], shape)
+        q = I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in st["units"]] for st in plan["schedule"]],
+                                       [I.IOS_MERGE if st["strategy"] == "merge" else I.IOS_CONCURRENT
+                                        for st in plan["schedule"]])
+        search_s, pred_ns = 0.0, plan["search"]["predicted_ns"]
+        states, transitions, measured = 0, 0, 0
+    else:
+        # Algorithm 1 with on-device stage profiling
+        opts = I.ios_sched_opts_default()
+        opts.r, opts.s = args.r, args.s
+        t0 = time.perf_counter()
+        q, pred_ns = I.ios_schedule(g.handle, opts)
+        search_s = time.perf_counter() - t0
+        states, transitions, measured = I.ios_schedule_stats(q)
+    tiles = {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in conv_units}
     if args.dump_costs:
         I.ios_schedule_dump_costs(g.handle, args.dump_costs)
     stages = I.ios_schedule_get(q)
@@ -545,6 +562,7 @@ def main():
                      "mean_launch_ns": round(kern_ns / n_launch, 1),
                      "mfma_flop_per_launch": tot_mfma / n_launch, "kernel_sha": sha},
         "schedule": stage_rows,
+        "tiles": tiles,
         "search": {"seconds": round(search_s, 3), "states": states, "transitions": transitions,
                    "stages_measured": measured, "predicted_ns": pred_ns},
         "throughput_img_per_s": round(args.batch / us * 1e6, 1),

@@ -160,6 +160,21 @@ int ios_stage_mergeable(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_
 int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t strategy,
                       int32_t warmup, int32_t reps, int32_t repeats, int64_t *latency_ns);
 
+/* Tile shape of a conv unit (unit_ids as in ios_block_units): after the
+ * graph is finalized, the first call that touches the device measures every
+ * conv alone with each shape and keeps one; these calls read that choice or
+ * replace it, e.g. to replay the shapes of an earlier run.  Shapes are
+ * 0 .. IOS_CONV_TILE_SHAPES - 1 (16x16, 16x32, 32x32, 32x64, 64x64 and
+ * 128x64 output pixels x channels).  A new shape applies to stages compiled
+ * afterwards (ios_profile_stage, ios_schedule, ios_schedule_from_stages),
+ * not to schedules that already exist.  Both calls set up the device first
+ * (hence the measurement) if no earlier call has.
+ * Errors: IOS_E_ARG (not a conv unit, shape out of range, null pointer),
+ * IOS_E_STATE (not finalized), IOS_E_HIP. */
+enum { IOS_CONV_TILE_SHAPES = 6 };
+int ios_get_conv_tile(ios_graph *g, int32_t unit_id, int32_t *shape);
+int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
+
 /* Cost provider for the dynamic program: latency of stage `stage_mask`
  * (block-local bits, see ios_block_units; unit_ids lists the same units,
  * ascending) of block `block` under `strategy`.  Write a latency in ns, or

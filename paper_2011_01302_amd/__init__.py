@@ -42,11 +42,13 @@ ERRORS = {-1: "IOS_E_ARG", -2: "IOS_E_SHAPE", -3: "IOS_E_STATE", -4: "IOS_E_NOT_
 IOS_CONV, IOS_SEPCONV, IOS_POOL_MAX, IOS_POOL_AVG, IOS_ADD, IOS_MEAN, IOS_CONCAT, IOS_IDENTITY = range(8)
 IOS_CONCURRENT, IOS_MERGE = 0, 1
 IOS_SCHED_DP, IOS_SCHED_SEQUENTIAL, IOS_SCHED_GREEDY = 0, 1, 2
+IOS_CONV_TILE_SHAPES = 6
 INT64_MAX = (1 << 63) - 1
 
 EXPORTED = ["ios_graph_create", "ios_graph_destroy", "ios_add_input", "ios_add_op",
             "ios_mark_output", "ios_graph_finalize", "ios_graph_blocks", "ios_block_units",
-            "ios_stage_mergeable", "ios_profile_stage", "ios_sched_opts_default", "ios_schedule",
+            "ios_stage_mergeable", "ios_profile_stage", "ios_get_conv_tile", "ios_set_conv_tile",
+            "ios_sched_opts_default", "ios_schedule",
             "ios_schedule_from_stages", "ios_schedule_get", "ios_schedule_stats",
             "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_timed",
             "ios_device_status", "ios_last_error"]
@@ -90,6 +92,8 @@ _sig = {
     "ios_block_units": (ctypes.c_int, [_P, _i32, _pi32, _pi32]),
     "ios_stage_mergeable": (ctypes.c_int, [_P, _pi32, _i32, _pi32]),
     "ios_profile_stage": (ctypes.c_int, [_P, _pi32, _i32, _i32, _i32, _i32, _i32, _pi64]),
+    "ios_get_conv_tile": (ctypes.c_int, [_P, _i32, _pi32]),
+    "ios_set_conv_tile": (ctypes.c_int, [_P, _i32, _i32]),
     "ios_sched_opts_default": (None, [ctypes.POINTER(ios_sched_opts)]),
     "ios_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ios_sched_opts), COST_FN, _P,
                                     ctypes.POINTER(_P), _pi64]),
@@ -194,6 +198,16 @@ def ios_profile_stage(g: int, unit_ids: Sequence[int], strategy: int = IOS_CONCU
     _check(_lib.ios_profile_stage(g, _i32arr(unit_ids), len(unit_ids), strategy, warmup, reps,
                                   repeats, ctypes.byref(ns)))
     return ns.value
+
+
+def ios_get_conv_tile(g: int, unit_id: int) -> int:
+    v = _i32()
+    _check(_lib.ios_get_conv_tile(g, unit_id, ctypes.byref(v)))
+    return v.value
+
+
+def ios_set_conv_tile(g: int, unit_id: int, shape: int) -> None:
+    _check(_lib.ios_set_conv_tile(g, unit_id, shape))
 
 
 def ios_sched_opts_default() -> ios_sched_opts:

@@ -161,6 +161,28 @@ int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t 
   });
 }
 
+int ios_get_conv_tile(ios_graph *g, int32_t unit_id, int32_t *shape) {
+  return guarded([&] {
+    need_final(g);
+    need(shape != nullptr, "null argument");
+    const int op = unit_op_of_tensor(g, unit_id);
+    need(g->ops[op].d.kind == IOS_CONV, "not a conv unit");
+    ensure_device(g);
+    *shape = g->ops[op].tcfg;
+  });
+}
+
+int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape) {
+  return guarded([&] {
+    need_final(g);
+    const int op = unit_op_of_tensor(g, unit_id);
+    need(g->ops[op].d.kind == IOS_CONV, "not a conv unit");
+    need(shape >= 0 && shape < TC_COUNT, "tile shape out of range");
+    ensure_device(g);
+    g->ops[op].tcfg = shape;
+  });
+}
+
 void ios_sched_opts_default(ios_sched_opts *o) {
   if (!o) return;
   o->mode = IOS_SCHED_DP;

@@ -51,6 +51,7 @@ enum TileCfg : int32_t {
   TC_128x64 = 5,     // FM2 FN2 WM4 WN2 WK1
   TC_COUNT = 6,
 };
+static_assert(TC_COUNT == IOS_CONV_TILE_SHAPES, "tile shapes of the public API");
 
 struct TileShape { int fm, fn, wm, wn, wk; };
 inline TileShape tile_shape(int cfg) {

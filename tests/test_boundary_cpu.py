@@ -227,6 +227,7 @@ def test_graph_error_paths():
     expect("IOS_E_SHAPE", I.ios_add_op, g, desc(I.IOS_ADD), [x, y])
     expect("IOS_E_STATE", I.ios_graph_blocks, g)
     expect("IOS_E_STATE", I.ios_schedule, g, None, lambda *a: 1)
+    expect("IOS_E_STATE", I.ios_get_conv_tile, g, x)
     expect("IOS_E_UNSUPPORTED", I.ios_mark_output, g, x)
     c = I.ios_add_op(g, desc(I.IOS_CONV, 3, 3, p=1), [x], w)
     cat = I.ios_add_op(g, desc(I.IOS_CONCAT), [c])
@@ -238,6 +239,10 @@ def test_graph_error_paths():
     expect("IOS_E_STATE", I.ios_add_input, g, 1, 1, 1)
     expect("IOS_E_ARG", I.ios_profile_stage, g, [x])                          # not a unit
     expect("IOS_E_ARG", I.ios_block_units, g, 5)
+    # conv tile shapes: argument errors come before any device work
+    expect("IOS_E_ARG", I.ios_get_conv_tile, g, x)                            # not a unit
+    expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, I.IOS_CONV_TILE_SHAPES)
+    expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, -1)
     I.ios_graph_destroy(g)
     expect("IOS_E_ARG", I.ios_graph_create, 0)
 

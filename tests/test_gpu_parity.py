@@ -240,6 +240,28 @@ def test_profile_stage_and_errors():
     g.close()
 
 
+def test_conv_tile_shapes_read_and_replayed():
+    """The tuned shape of every conv can be read back and replaced; stages
+    compiled afterwards use the new shapes (results still match the oracle)."""
+    spec, ten = case("inception")
+    g = I.Graph(spec, ten)
+    convs = [u["name"] for u in W.unit_ops(spec) if u["kind"] == "conv"]
+    tuned = {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in convs}
+    assert all(0 <= v < I.IOS_CONV_TILE_SHAPES for v in tuned.values())
+    with pytest.raises(I.IosError) as e:
+        I.ios_get_conv_tile(g.handle, g.tid["pool"])
+    assert e.value.name == "IOS_E_ARG"
+    for k, n in enumerate(convs):
+        I.ios_set_conv_tile(g.handle, g.tid[n], k % I.IOS_CONV_TILE_SHAPES)
+    assert [I.ios_get_conv_tile(g.handle, g.tid[n]) for n in convs] == \
+        [k % I.IOS_CONV_TILE_SHAPES for k in range(len(convs))]
+    for mode in (I.IOS_SCHED_SEQUENTIAL, I.IOS_SCHED_GREEDY):
+        q = sched(g, mode)
+        check(run(g, q, spec, ten), reference("inception"), f"inception/replayed tiles/mode{mode}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_run_timed_and_determinism():
     spec, ten = case("inception")
     g = I.Graph(spec, ten)

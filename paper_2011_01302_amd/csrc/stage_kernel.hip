@@ -535,6 +535,8 @@ __device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const
 
 // ------------------------------------------------------------------ elementwise
 
+constexpr int kPoolBatch = 4;   // staging loads per thread in flight
+
 // One band of output rows of one (image, channel) plane: the input rows it
 // needs are staged in LDS with coalesced loads (each input value is read from
 // memory once), then every output is reduced from LDS.
@@ -551,7 +553,21 @@ __device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, cons
   const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
   const int src = ((img * o.in_ctot[0] + o.in_coff[0] + c) * H + ih_lo) * W;
   const int n_in = (ih_hi - ih_lo) * W;
-  for (int i = tid; i < n_in; i += kThreads) lds[i] = bld(xr, (src + i) * 4, 0);
+  // batches of kPoolBatch loads per thread, all issued before any is
+  // written to LDS: one memory round trip per batch
+  for (int base = 0; base < n_in; base += kPoolBatch * kThreads) {
+    float v[kPoolBatch];
+#pragma unroll
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const int i = base + k * kThreads + tid;
+      v[k] = bld(xr, i < n_in ? (src + i) * 4 : kOOB, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const int i = base + k * kThreads + tid;
+      if (i < n_in) lds[i] = v[k];
+    }
+  }
   __syncthreads();
   float *__restrict__ out = sl[o.route_slot[0]] +
                             (size_t)(img * o.route_ctot[0] + o.route_coff[0] + c) * Ho * Wo;
@@ -587,14 +603,23 @@ __device__ __forceinline__ void sum_tile(const Slots &sl, const DevOp &op, const
   float s[kEltPerTile / kThreads];
 #pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) s[e] = 0.f;
-  for (int i = 0; i < o.n_in; ++i) {
-    const __amdgpu_buffer_rsrc_t r = rsrc(sl[U(op.in_slot[i])], U(op.in_bytes[i]));
-    const int base = (img * U(op.in_ctot[i]) + U(op.in_coff[i]) + c) * hw;
+  // inputs two at a time: both inputs' loads are issued before either is added
+  for (int i = 0; i < o.n_in; i += 2) {
+    const int j = min(i + 1, o.n_in - 1);
+    const __amdgpu_buffer_rsrc_t r0 = rsrc(sl[U(op.in_slot[i])], U(op.in_bytes[i]));
+    const __amdgpu_buffer_rsrc_t r1 = rsrc(sl[U(op.in_slot[j])], U(op.in_bytes[j]));
+    const int base0 = (img * U(op.in_ctot[i]) + U(op.in_coff[i]) + c) * hw;
+    const int base1 = (img * U(op.in_ctot[j]) + U(op.in_coff[j]) + c) * hw;
+    const bool two = j != i;                       // uniform
+    float a[kEltPerTile / kThreads], b[kEltPerTile / kThreads];
 #pragma unroll
     for (int e = 0; e < kEltPerTile / kThreads; ++e) {
       const int pix = p0 + e * kThreads + threadIdx.x;
-      s[e] += bld(r, pix < hw ? (base + pix) * 4 : kOOB, 0);
+      a[e] = bld(r0, pix < hw ? (base0 + pix) * 4 : kOOB, 0);
+      b[e] = bld(r1, two && pix < hw ? (base1 + pix) * 4 : kOOB, 0);
     }
+#pragma unroll
+    for (int e = 0; e < kEltPerTile / kThreads; ++e) s[e] += a[e] + b[e];
   }
 #pragma unroll
   for (int e = 0; e < kEltPerTile / kThreads; ++e) {

@@ -247,6 +247,7 @@ def run_suite(args):
             o.mode = mode
             if config in ("randwire", "nasnet"):      # tens of thousands of candidate stages
                 o.warmup, o.reps, o.repeats = 1, 3, 1
+                o.verify_reps = 20                     # the picked stages measured in full
             print(f"[suite] {config} bs{batch} {name}: scheduling", file=sys.stderr, flush=True)
             t0 = time.perf_counter()
             q, pred = I.ios_schedule(g.handle, o)
@@ -321,6 +322,7 @@ def run_next(args):
     def fast(o, config):
         if config in ("randwire", "nasnet"):       # tens of thousands of candidate stages
             o.warmup, o.reps, o.repeats = 1, 3, 1
+            o.verify_reps = 20                      # the picked stages measured in full
         return o
 
     def timed(g, q, ins, outs, gflop):

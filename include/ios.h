@@ -196,10 +196,19 @@ typedef struct {
   int32_t strategies;  /* bit 0 concurrent, bit 1 merge: 3 = IOS-Both,
                           1 = IOS-Parallel, 2 = IOS-Merge (Sec. 6.1)         */
   int32_t warmup, reps, repeats;   /* profiler settings when fn is NULL     */
+  int32_t verify_reps; /* DP with fn NULL, > 0: after a block's search the
+                          stages of its schedule are measured again (3 warm-up
+                          launches, 3 repeats of verify_reps launches), their
+                          table entries replaced, and the search repeated on
+                          the updated table until every stage it picks has been
+                          measured that way (at most 16 rounds).  Guards a
+                          search run with few launches per candidate against
+                          stages whose short measurement came out low; the
+                          result is optimal for the final table.  0 = off    */
 } ios_sched_opts;
 
 /* Fill opts with the paper's defaults: DP, r = 3, s = 8 (Sec. 5), both
- * strategies, warmup 3, reps 20, repeats 3. */
+ * strategies, warmup 3, reps 20, repeats 3, no verification rounds. */
 void ios_sched_opts_default(ios_sched_opts *opts);
 
 /* Find a schedule (Algorithm 1, block by block).  With fn == NULL each

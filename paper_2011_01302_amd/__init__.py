@@ -69,7 +69,7 @@ class ios_op_desc(ctypes.Structure):
 
 class ios_sched_opts(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("mode", "r", "s", "strategies", "warmup", "reps", "repeats")]
+                ("mode", "r", "s", "strategies", "warmup", "reps", "repeats", "verify_reps")]
 
 
 COST_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64,

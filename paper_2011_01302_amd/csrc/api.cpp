@@ -192,6 +192,7 @@ void ios_sched_opts_default(ios_sched_opts *o) {
   o->warmup = 3;
   o->reps = 20;
   o->repeats = 3;
+  o->verify_reps = 0;
 }
 
 int ios_schedule(ios_graph *g, const ios_sched_opts *opts, ios_cost_fn fn, void *ctx,

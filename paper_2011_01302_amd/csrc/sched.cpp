@@ -16,6 +16,7 @@
 #include <cstdio>
 #include <functional>
 #include <unordered_map>
+#include <unordered_set>
 
 #include "ios_internal.h"
 
@@ -92,11 +93,13 @@ struct Provider {
   ios_sched_opts o;
   int64_t measured = 0;
 
-  int64_t latency(int block, uint64_t mask, int strategy) {
+  int64_t latency(int block, uint64_t mask, int strategy, bool verify = false) {
     const Block &B = g->blocks[block];
     auto ops = ops_of_mask(B, mask);
     int64_t ns = kInf;
-    if (fn) {
+    if (verify) {
+      ns = profile_stage(g, ops, strategy, 3, o.verify_reps, 3);
+    } else if (fn) {
       std::vector<int32_t> ids;
       for (int oi : ops) ids.push_back(g->ops[oi].out);
       int rc = fn(ctx, block, mask, ids.data(), (int32_t)ids.size(), strategy, &ns);
@@ -116,15 +119,16 @@ struct Provider {
     return ns;
   }
 
-  // GenerateStage (Algorithm 1): the better strategy and its latency.
-  std::pair<int64_t, int> generate_stage(int block, uint64_t mask) {
+  // GenerateStage (Algorithm 1): the better strategy and its latency
+  // (verify: measured with the verification protocol).
+  std::pair<int64_t, int> generate_stage(int block, uint64_t mask, bool verify = false) {
     const Block &B = g->blocks[block];
     // with concurrent execution off (IOS-Merge) a one-unit stage still runs alone
     bool single = (mask & (mask - 1)) == 0;
-    int64_t lc = ((o.strategies & 1) || single) ? latency(block, mask, IOS_CONCURRENT) : kInf;
+    int64_t lc = ((o.strategies & 1) || single) ? latency(block, mask, IOS_CONCURRENT, verify) : kInf;
     int64_t lm = kInf;
     if ((o.strategies & 2) && stage_mergeable(g, ops_of_mask(B, mask)))
-      lm = latency(block, mask, IOS_MERGE);
+      lm = latency(block, mask, IOS_MERGE, verify);
     if (lc < lm) return {lc, IOS_CONCURRENT};
     return {lm, IOS_MERGE};
   }
@@ -201,16 +205,39 @@ ios_schedule_t *run_schedule(ios_graph *g, const ios_sched_opts &o, ios_cost_fn 
       dp.memo[0] = Memo{0, 0, IOS_CONCURRENT};
       int64_t c = dp.scheduler(B.full());
       if (c == kInf) fail(IOS_E_BAD_STAGE, "no schedule satisfies the pruning strategy");
-      total = sat_add(total, c);
-      std::vector<std::pair<uint64_t, int>> rev;
-      for (uint64_t S = B.full(); S;) {
-        const Memo &m = dp.memo.at(S);
-        rev.push_back({m.choice, m.strategy});
-        S &= ~m.choice;
+      const int64_t states0 = (int64_t)dp.memo.size(), transitions0 = dp.transitions;   // the search itself
+      auto chosen = [&]() {
+        std::vector<std::pair<uint64_t, int>> rev;
+        for (uint64_t S = B.full(); S;) {
+          const Memo &m = dp.memo.at(S);
+          rev.push_back({m.choice, m.strategy});
+          S &= ~m.choice;
+        }
+        return rev;
+      };
+      std::vector<std::pair<uint64_t, int>> rev = chosen();
+      if (o.verify_reps > 0 && !fn) {
+        // verification rounds: measure the picked stages again, replace their
+        // entries, search again on the updated table
+        std::unordered_set<uint64_t> verified;
+        for (int round = 0; round < 16; ++round) {
+          bool fresh = false;
+          for (const auto &st : rev)
+            if (verified.insert(st.first).second) {
+              dp.stages[st.first] = P.generate_stage(b, st.first, true);
+              fresh = true;
+            }
+          if (!fresh) break;
+          dp.memo.clear();
+          dp.memo[0] = Memo{0, 0, IOS_CONCURRENT};
+          c = dp.scheduler(B.full());
+          rev = chosen();
+        }
       }
+      total = sat_add(total, c);
       for (auto it = rev.rbegin(); it != rev.rend(); ++it) append_stage(q.get(), g, b, it->first, it->second);
-      q->states += (int64_t)dp.memo.size();
-      q->transitions += dp.transitions;
+      q->states += states0;
+      q->transitions += transitions0;
     } else if (o.mode == IOS_SCHED_SEQUENTIAL) {
       for (int i = 0; i < (int)B.ops.size(); ++i) {
         int64_t c = P.latency(b, 1ull << i, IOS_CONCURRENT);

@@ -197,15 +197,18 @@ def test_device_dp_schedule_replays_in_oracle(config, tmp_path):
     g.close()
 
 
-@pytest.mark.parametrize("config", ["randwire", "nasnet"])
-def test_device_dp_large_blocks_replay_in_oracle(config, tmp_path):
+@pytest.mark.parametrize("config,verify", [("randwire", 0), ("nasnet", 0), ("randwire", 10), ("nasnet", 10)])
+def test_device_dp_large_blocks_replay_in_oracle(config, verify, tmp_path):
     """RandWire (33 units, ~31k candidate stages) and NASNet (17 units, ~56k):
-    the search runs on the device with light profiling; the schedule must be
-    the oracle's on the dumped table and the outputs must match."""
+    the search runs on the device with light profiling (and, with verify, the
+    picked stages measured again until the search keeps its choice); the
+    schedule must be the oracle's on the final dumped table and the outputs
+    must match."""
     spec, ten = case(config)
     g = I.Graph(spec, ten)
     o = I.ios_sched_opts_default()
     o.warmup, o.reps, o.repeats = 1, 2, 1
+    o.verify_reps = verify
     q, cost = I.ios_schedule(g.handle, o)
     check(run(g, q, spec, ten), reference(config), f"{config}/dp")
     path = tmp_path / "costs.jsonl"

@@ -185,6 +185,55 @@ def write_traffic(args, fetch_dir, write_dir):
     print(json.dumps(out))
 
 
+def write_occupancy(args, ios_dir, seq_dir):
+    """Mean resident waves per CU while the stage kernels run, for the IOS
+    schedule and for the sequential one-unit-per-launch schedule of the same
+    kernels (Sec. 6.3 compares active warps the same way).  From two
+    rocprofv3 --pmc MeanOccupancyPerCU GRBM_GUI_ACTIVE runs: the derived
+    counter is SQ_LEVEL_WAVES accumulated over the dispatch / the GPU-active
+    cycles of the dispatch / CUs, so launch and drain count as empty time.
+    The timed loop is the last steps x stages stage-kernel dispatches; each
+    is weighted by its GPU-active cycles."""
+    out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": kernel_sha(),
+           "counter": "MeanOccupancyPerCU (waves per CU over the dispatch's GPU-active cycles; "
+                      "a CU holds at most 32 wave64, this kernel at most 16)"}
+    for name, d in (("ios", ios_dir), ("sequential", seq_dir)):
+        occ = _pmc_rows(d, "MeanOccupancyPerCU")
+        act = {i: v for i, _, v in _pmc_rows(d, "GRBM_GUI_ACTIVE")}
+        info = _pmc_info(d)
+        meta = json.load(open(os.path.join(d, "bench.json")))
+        ns = meta["stages"]
+        timed = [(i, v) for i, k, v in occ if "ios_stage_kernel" in k][-meta["steps"] * ns:]
+        w = sum(act[i] for i, _ in timed)
+        stages = []
+        for k in range(ns):
+            rows = timed[k::ns]
+            wk = sum(act[i] for i, _ in rows)
+            stages.append({"units": meta["schedule"][k]["units"], "strategy": meta["schedule"][k]["strategy"],
+                           "workgroups": info[rows[0][0]][0],
+                           "mean_waves_per_cu": round(sum(v * act[i] for i, v in rows) / wk, 3),
+                           "dispatch_us": round(statistics.median(info[i][1] for i, _ in rows) / 1e3, 2)})
+        out[name] = {"stages": ns, "mean_waves_per_cu": round(sum(v * act[i] for i, v in timed) / w, 3),
+                     "per_stage": stages}
+    out["ios_over_sequential"] = round(out["ios"]["mean_waves_per_cu"] / out["sequential"]["mean_waves_per_cu"], 3)
+    path = os.path.join(ROOT, "profiles", f"occupancy_{args.config}_bs{args.batch}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
+
+
+def _pmc_info(d):
+    """Dispatch id -> (workgroups, dispatch ns under counter collection)."""
+    import csv
+    import glob
+    info = {}
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            wg = int(r["Grid_Size"]) // max(1, int(r["Workgroup_Size"]))
+            info[int(r["Dispatch_Id"])] = (wg, int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    return info
+
+
 def trace_summary(args, trace_dir):
     """Stage-kernel launch durations of the timed loop from a rocprofv3
     --kernel-trace run of this benchmark (run with --no-stage-times, so the
@@ -444,6 +493,12 @@ def main():
                     help="replay the schedule and conv tile shapes of an earlier run (the last JSON "
                          "line of this file) instead of searching: for profiler runs, whose added "
                          "per-launch cost would change the search's choices")
+    ap.add_argument("--mode", choices=("dp", "sequential", "greedy"), default="dp",
+                    help="schedule of the timed step: the DP search (default) or a baseline "
+                         "(with --plan-from: that run's tile shapes, this mode's schedule)")
+    ap.add_argument("--occupancy-from", nargs=2, metavar=("IOS_DIR", "SEQ_DIR"),
+                    help="turn two rocprofv3 --pmc MeanOccupancyPerCU GRBM_GUI_ACTIVE runs (IOS "
+                         "schedule, --mode sequential) into profiles/occupancy_<workload>.json and exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
                          "into profiles/traffic_<workload>.json and exit")
@@ -458,6 +513,9 @@ def main():
         return
     if args.traffic_from:
         write_traffic(args, *args.traffic_from)
+        return
+    if args.occupancy_from:
+        write_occupancy(args, *args.occupancy_from)
         return
 
     lib = os.path.join(ROOT, "paper_2011_01302_amd", "libios.so")
@@ -487,10 +545,19 @@ def main():
 
     conv_units = [op["name"] for op in spec["ops"] if op["kind"] == "conv"]
     if args.plan_from:
-        # the earlier run's conv tile shapes and stages, no search
         plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{")][-1]
         for name, shape in plan["tiles"].items():
             I.ios_set_conv_tile(g.handle, g.tid[name], shape)
+    if args.mode != "dp":
+        # a baseline schedule of the same kernels
+        o = I.ios_sched_opts_default()
+        o.mode = I.IOS_SCHED_SEQUENTIAL if args.mode == "sequential" else I.IOS_SCHED_GREEDY
+        t0 = time.perf_counter()
+        q, pred_ns = I.ios_schedule(g.handle, o)
+        search_s = time.perf_counter() - t0
+        states, transitions, measured = I.ios_schedule_stats(q)
+    elif args.plan_from:
+        # the earlier run's conv tile shapes and stages, no search
         q = I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in st["units"]] for st in plan["schedule"]],
                                        [I.IOS_MERGE if st["strategy"] == "merge" else I.IOS_CONCURRENT
                                         for st in plan["schedule"]])
@@ -522,7 +589,9 @@ def main():
             dst.copy_(src)
             torch.cuda.synchronize()
         print(json.dumps({"value": round(us, 3), "unit": "us", "stages": len(stages),
-                          "steps": args.steps, "copy_mb": args.copy_mb}), flush=True)
+                          "steps": args.steps, "copy_mb": args.copy_mb, "mode": args.mode,
+                          "schedule": [{"units": g.names(ids), "strategy": "merge" if strat else "concurrent"}
+                                       for ids, strat in stages]}), flush=True)
         return
 
     # per-stage roofline on the stage kernel

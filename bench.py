@@ -459,6 +459,74 @@ def run_next(args):
         json.dump(out, f, indent=1)
 
 
+def run_network(args):
+    """Whole networks scheduled block by block (the block-wise speed-up
+    appendix): for every network, the DP runs on each block with on-device
+    profiling; the whole network is then timed end to end under the IOS,
+    sequential and greedy schedules, and per block from HIP events around each
+    stage launch (sum of the block's stage medians).  Written to args.network
+    as JSON."""
+    import torch
+
+    import paper_2011_01302_amd as I
+    import workloads as W
+    stream = torch.cuda.current_stream().cuda_stream
+    report = []
+    for net in W.NETWORK_NAMES:
+        print(f"[network] {net} bs{args.batch}: graph", file=sys.stderr, flush=True)
+        spec, g, ins, outs = _setup(I, W, torch, net, args.batch, args.seed)
+        work = unit_work(spec, args.batch)
+        gflop = sum(w[0] + w[1] for w in work.values()) / 1e9
+        block_of = {}
+        for b in range(I.ios_graph_blocks(g.handle)):
+            for u in I.ios_block_units(g.handle, b):
+                block_of[u] = b
+        names = spec.get("block_names") or [str(b) for b in range(len(set(block_of.values())))]
+        row = {"network": net, "batch": args.batch, "units": len(block_of), "blocks": len(names),
+               "gflop": round(gflop, 3)}
+        per_block = {n: {} for n in names}
+        for name, mode in (("ios", I.IOS_SCHED_DP), ("sequential", I.IOS_SCHED_SEQUENTIAL),
+                           ("greedy", I.IOS_SCHED_GREEDY)):
+            o = I.ios_sched_opts_default()
+            o.mode = mode
+            o.r, o.s = args.r, args.s
+            print(f"[network] {net}: {name} schedule", file=sys.stderr, flush=True)
+            t0 = time.perf_counter()
+            q, pred = I.ios_schedule(g.handle, o)
+            search = time.perf_counter() - t0
+            sched = I.ios_schedule_get(q)
+            us = time_steps(I, g, q, ins, outs, stream, 10, max(20, min(args.steps, 100)), torch)
+            assert I.ios_device_status(g.handle, stream) == 0
+            entry = {"us": round(us, 2), "stages": len(sched), "predicted_us": round(pred / 1e3, 2),
+                     "search_s": round(search, 2)}
+            if mode == I.IOS_SCHED_DP:
+                st, tr, ms = I.ios_schedule_stats(q)
+                entry.update({"states": st, "transitions": tr, "stages_measured": ms,
+                              "schedule": [(g.names(ids), "merge" if t else "concurrent") for ids, t in sched]})
+            if mode != I.IOS_SCHED_GREEDY:
+                st_ns, _ = stage_times(I, g, q, ins, outs, stream, 20)
+                for (ids, _t), ns in zip(sched, st_ns):
+                    pb = per_block[names[block_of[ids[0]]]]
+                    pb[name + "_us"] = round(pb.get(name + "_us", 0.0) + ns / 1e3, 2)
+                    pb[name + "_stages"] = pb.get(name + "_stages", 0) + 1
+            row[name] = entry
+            I.ios_schedule_destroy(q)
+            print(f"[network] {net} {name}: {us:.2f} us, {len(sched)} stages, search {search:.1f} s",
+                  file=sys.stderr, flush=True)
+        for n, pb in per_block.items():
+            pb["speedup"] = round(pb["sequential_us"] / pb["ios_us"], 3)
+        row["per_block"] = per_block
+        row["speedup_vs_sequential"] = round(row["sequential"]["us"] / row["ios"]["us"], 3)
+        row["speedup_vs_greedy"] = round(row["greedy"]["us"] / row["ios"]["us"], 3)
+        row["tflops"] = round(gflop / row["ios"]["us"] * 1e3, 2)
+        report.append(row)
+        g.close()
+        del ins, outs
+        torch.cuda.empty_cache()
+    with open(args.network, "w") as f:
+        json.dump(report, f, indent=1)
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -486,6 +554,9 @@ def main():
     ap.add_argument("--next", default="",
                     help="run the follow-up experiments (strategy ablation, batch specialisation, "
                          "pruning sweep) and write a JSON report to this path")
+    ap.add_argument("--network", default="",
+                    help="schedule whole networks block by block (IOS vs sequential vs greedy, "
+                         "end to end and per block) and write a JSON report to this path")
     ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
                     help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
                          "benchmark and exit")
@@ -527,6 +598,9 @@ def main():
         return
     if args.next:
         run_next(args)
+        return
+    if args.network:
+        run_network(args)
         return
     import numpy as np
     import torch

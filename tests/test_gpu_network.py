@@ -1,0 +1,110 @@
+"""GPU parity on a whole network: Inception-V3 (3x299x299 -> 1000 logits,
+13 blocks, 109 schedule units, random weights) through the C ABI against the
+fp64 oracle (max|gpu - oracle| / max|oracle| <= 1e-4 on the logits), under
+the baseline schedules and under the DP run block by block on the device,
+whose schedule must equal the oracle DP replayed on the dumped cost table."""
+import functools
+import json
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+
+torch = pytest.importorskip("torch")
+I = pytest.importorskip("paper_2011_01302_amd")
+from oracle import evaluator as E          # noqa: E402
+from oracle import schedule as O           # noqa: E402
+
+DEV = "cuda:0"
+NET = "inception_v3"
+
+
+@functools.lru_cache(maxsize=None)
+def case():
+    return W.make(NET, 1, 0)
+
+
+@functools.lru_cache(maxsize=None)
+def reference():
+    spec, ten = case()
+    print("[gpu-case] oracle evaluation of the whole network", flush=True)
+    return E.outputs(spec, ten)
+
+
+def run(g, q, spec, ten):
+    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(DEV) for t in spec["inputs"]]
+    shp = W.infer_shapes(spec)
+    outs = [torch.full((g.batch,) + shp[o], float("nan"), device=DEV) for o in spec["outputs"]]
+    I.ios_run(g.handle, q, [t.data_ptr() for t in ins], [o.data_ptr() for o in outs], 0)
+    torch.cuda.synchronize()
+    assert I.ios_device_status(g.handle, 0) == 0
+    return [o.cpu().numpy() for o in outs]
+
+
+def check(outs, refs, what):
+    for got, ref in zip(outs, refs):
+        assert got.shape == ref.shape
+        assert np.isfinite(got).all(), what
+        e = float(np.abs(got.astype(np.float64) - ref).max() / np.abs(ref).max())
+        assert e <= TOL, f"{what}: relative error {e:.3e}"
+
+
+@pytest.fixture(autouse=True)
+def _print_case(request):
+    print(f"\n[gpu-case] {request.node.name}", flush=True)
+    yield
+
+
+def test_network_parity_baseline_schedules():
+    """Sequential (one unit per launch), greedy (every ready unit per launch)
+    and one stage per block (branches chained inside the launch, chains of up
+    to five convs)."""
+    spec, ten = case()
+    ref = reference()
+    g = I.Graph(spec, ten)
+    assert len(g.blocks()) == 13
+    for mode in (I.IOS_SCHED_SEQUENTIAL, I.IOS_SCHED_GREEDY):
+        o = I.ios_sched_opts_default()
+        o.mode = mode
+        q, _ = I.ios_schedule(g.handle, o, lambda b, m, ids, t: 1000)
+        check(run(g, q, spec, ten), ref, f"mode {mode}")
+        I.ios_schedule_destroy(q)
+    blocks = g.blocks()
+    q = I.ios_schedule_from_stages(g.handle, blocks, [I.IOS_CONCURRENT] * len(blocks))
+    check(run(g, q, spec, ten), ref, "one stage per block")
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
+def test_network_device_dp_replays_in_oracle(tmp_path):
+    """Algorithm 1 on each of the 13 blocks with on-device stage profiling
+    (light protocol); the outputs must match and the schedule must be the
+    oracle DP's on the dumped cost table, block by block."""
+    spec, ten = case()
+    g = I.Graph(spec, ten)
+    o = I.ios_sched_opts_default()
+    o.warmup, o.reps, o.repeats = 1, 3, 1
+    q, cost = I.ios_schedule(g.handle, o)
+    check(run(g, q, spec, ten), reference(), "dp")
+    path = tmp_path / "costs.jsonl"
+    I.ios_schedule_dump_costs(g.handle, str(path))
+    table = {}
+    for line in open(path):
+        r = json.loads(line)
+        table[(r["block"], r["mask"], 0)] = r["concurrent_ns"]
+        if r["merge_ns"] is not None:
+            table[(r["block"], r["mask"], 1)] = r["merge_ns"]
+    total, stages = 0, []
+    for b, blk in enumerate(O.blocks_of(spec)):
+        res = O.ios_dp(blk, lambda m, t: table[(b, m, t)], 3, 8)
+        total += res.cost
+        stages += [(sorted(blk.units[i]["name"] for i in O.bits(m)), t) for m, t in res.schedule]
+    lib = [(sorted(g.names(ids)), t) for ids, t in I.ios_schedule_get(q)]
+    assert lib == stages
+    assert total == cost
+    I.ios_schedule_destroy(q)
+    g.close()

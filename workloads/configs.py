@@ -10,6 +10,11 @@ each network is replaced by a block of the same shapes built here:
   nasnet     NASNet-A style normal cell, two 168x42x42 inputs -> 840x42x42
   squeeze    8 SqueezeNet fire modules, 96x55x55 input, two max-pools
 
+and, for the block-wise whole-network runs (not one of the blocks above):
+
+  inception_v3   the whole Inception-V3 network, 3x299x299 -> 1000 logits,
+                 13 blocks (stem, eleven modules, head)
+
 A workload is a plain description (``spec``) plus a dict of float32 numpy
 arrays (``tensors``).  The description lists the operators in insertion
 order, which is a topological order; both the oracle and the library read it.
@@ -199,8 +204,124 @@ def spec_squeeze(batch: int = 1, seed: int = 0) -> dict:
             "ops": ops, "outputs": [cur]}
 
 
+# ---------------------------------------------------------------- whole networks
+#
+# Inception-V3 (Szegedy et al., "Rethinking the Inception Architecture",
+# 299x299 input, no auxiliary head, no batch-norm: each conv carries a bias
+# and a ReLU) built from its published layer table: a stem of five convs and
+# two max-pools, three 35x35 modules, a grid reduction to 17x17, four 17x17
+# modules with factorised 7x7 convs, a reduction to 8x8, two 8x8 modules with
+# split 1x3 / 3x1 outputs, global average pooling and the 1000-way classifier
+# (a 1x1 conv on the 1x1 map, no ReLU).  The eleven modules are the blocks the
+# paper schedules one at a time (Table 2, block-wise speed-up appendix); the
+# stem and the head are blocks of their own.
+
+
+def _inception_a(ops, p, inp, pool_features, block):
+    ops += [_conv(f"{p}_1x1", inp, 64, 1, 0, block=block),
+            _conv(f"{p}_5x5a", inp, 48, 1, 0, block=block),
+            _conv(f"{p}_5x5b", f"{p}_5x5a", 64, 5, 2, block=block),
+            _conv(f"{p}_3x3a", inp, 64, 1, 0, block=block),
+            _conv(f"{p}_3x3b", f"{p}_3x3a", 96, 3, 1, block=block),
+            _conv(f"{p}_3x3c", f"{p}_3x3b", 96, 3, 1, block=block),
+            _pool(f"{p}_pool", inp, "avgpool", 3, 1, 1, block=block),
+            _conv(f"{p}_pp", f"{p}_pool", pool_features, 1, 0, block=block),
+            _view(p, "concat", [f"{p}_1x1", f"{p}_5x5b", f"{p}_3x3c", f"{p}_pp"])]
+
+
+def _inception_b(ops, p, inp, block):
+    # 35x35 -> 17x17 grid reduction
+    ops += [_conv(f"{p}_3x3", inp, 384, 3, 0, stride=2, block=block),
+            _conv(f"{p}_dbla", inp, 64, 1, 0, block=block),
+            _conv(f"{p}_dblb", f"{p}_dbla", 96, 3, 1, block=block),
+            _conv(f"{p}_dblc", f"{p}_dblb", 96, 3, 0, stride=2, block=block),
+            _pool(f"{p}_pool", inp, "maxpool", 3, 2, 0, block=block),
+            _view(p, "concat", [f"{p}_3x3", f"{p}_dblc", f"{p}_pool"])]
+
+
+def _inception_c(ops, p, inp, c7, block):
+    # 17x17 module, 7x7 convs factorised into 1x7 and 7x1
+    r, c = ((1, 7), (0, 3)), ((7, 1), (3, 0))
+    ops += [_conv(f"{p}_1x1", inp, 192, 1, 0, block=block),
+            _conv(f"{p}_7a", inp, c7, 1, 0, block=block),
+            _conv(f"{p}_7b", f"{p}_7a", c7, *r, block=block),
+            _conv(f"{p}_7c", f"{p}_7b", 192, *c, block=block),
+            _conv(f"{p}_d7a", inp, c7, 1, 0, block=block),
+            _conv(f"{p}_d7b", f"{p}_d7a", c7, *c, block=block),
+            _conv(f"{p}_d7c", f"{p}_d7b", c7, *r, block=block),
+            _conv(f"{p}_d7d", f"{p}_d7c", c7, *c, block=block),
+            _conv(f"{p}_d7e", f"{p}_d7d", 192, *r, block=block),
+            _pool(f"{p}_pool", inp, "avgpool", 3, 1, 1, block=block),
+            _conv(f"{p}_pp", f"{p}_pool", 192, 1, 0, block=block),
+            _view(p, "concat", [f"{p}_1x1", f"{p}_7c", f"{p}_d7e", f"{p}_pp"])]
+
+
+def _inception_d(ops, p, inp, block):
+    # 17x17 -> 8x8 grid reduction
+    ops += [_conv(f"{p}_3a", inp, 192, 1, 0, block=block),
+            _conv(f"{p}_3b", f"{p}_3a", 320, 3, 0, stride=2, block=block),
+            _conv(f"{p}_7a", inp, 192, 1, 0, block=block),
+            _conv(f"{p}_7b", f"{p}_7a", 192, (1, 7), (0, 3), block=block),
+            _conv(f"{p}_7c", f"{p}_7b", 192, (7, 1), (3, 0), block=block),
+            _conv(f"{p}_7d", f"{p}_7c", 192, 3, 0, stride=2, block=block),
+            _pool(f"{p}_pool", inp, "maxpool", 3, 2, 0, block=block),
+            _view(p, "concat", [f"{p}_3b", f"{p}_7d", f"{p}_pool"])]
+
+
+def _inception_e(ops, p, inp, block):
+    # 8x8 module whose 3x3 branches end in parallel 1x3 and 3x1 convs
+    r, c = ((1, 3), (0, 1)), ((3, 1), (1, 0))
+    ops += [_conv(f"{p}_1x1", inp, 320, 1, 0, block=block),
+            _conv(f"{p}_3a", inp, 384, 1, 0, block=block),
+            _conv(f"{p}_3b1", f"{p}_3a", 384, *r, block=block),
+            _conv(f"{p}_3b2", f"{p}_3a", 384, *c, block=block),
+            _view(f"{p}_3", "concat", [f"{p}_3b1", f"{p}_3b2"]),
+            _conv(f"{p}_d3a", inp, 448, 1, 0, block=block),
+            _conv(f"{p}_d3b", f"{p}_d3a", 384, 3, 1, block=block),
+            _conv(f"{p}_d3c1", f"{p}_d3b", 384, *r, block=block),
+            _conv(f"{p}_d3c2", f"{p}_d3b", 384, *c, block=block),
+            _view(f"{p}_d3", "concat", [f"{p}_d3c1", f"{p}_d3c2"]),
+            _pool(f"{p}_pool", inp, "avgpool", 3, 1, 1, block=block),
+            _conv(f"{p}_pp", f"{p}_pool", 192, 1, 0, block=block),
+            _view(p, "concat", [f"{p}_1x1", f"{p}_3", f"{p}_d3", f"{p}_pp"])]
+
+
+INCEPTION_V3_BLOCKS = ["stem", "5b", "5c", "5d", "6a", "6b", "6c", "6d", "6e", "7a", "7b", "7c", "head"]
+
+
+def spec_inception_v3(batch: int = 1, seed: int = 0) -> dict:
+    ops = [_conv("stem_1a", "x", 32, 3, 0, stride=2, block=0),
+           _conv("stem_2a", "stem_1a", 32, 3, 0, block=0),
+           _conv("stem_2b", "stem_2a", 64, 3, 1, block=0),
+           _pool("stem_p1", "stem_2b", "maxpool", 3, 2, 0, block=0),
+           _conv("stem_3b", "stem_p1", 80, 1, 0, block=0),
+           _conv("stem_4a", "stem_3b", 192, 3, 0, block=0),
+           _pool("stem_p2", "stem_4a", "maxpool", 3, 2, 0, block=0)]
+    cur = "stem_p2"
+    for b, (p, pf) in enumerate([("5b", 32), ("5c", 64), ("5d", 64)], start=1):
+        _inception_a(ops, p, cur, pf, b)
+        cur = p
+    _inception_b(ops, "6a", cur, 4)
+    cur = "6a"
+    for b, (p, c7) in enumerate([("6b", 128), ("6c", 160), ("6d", 160), ("6e", 192)], start=5):
+        _inception_c(ops, p, cur, c7, b)
+        cur = p
+    _inception_d(ops, "7a", cur, 9)
+    cur = "7a"
+    for b, p in enumerate(["7b", "7c"], start=10):
+        _inception_e(ops, p, cur, b)
+        cur = p
+    ops += [_pool("head_pool", cur, "avgpool", 8, 1, 0, block=12),
+            _conv("head_fc", "head_pool", 1000, 1, 0, post_relu=0, block=12)]
+    return {"name": "inception_v3", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 3, "h": 299, "w": 299}],
+            "ops": ops, "outputs": ["head_fc"], "block_names": INCEPTION_V3_BLOCKS}
+
+
+NETWORK_NAMES = ["inception_v3"]
+
 SPECS = {"tiny": spec_tiny, "inception": spec_inception, "randwire": spec_randwire,
-         "nasnet": spec_nasnet, "squeeze": spec_squeeze}
+         "nasnet": spec_nasnet, "squeeze": spec_squeeze, "inception_v3": spec_inception_v3}
 
 
 # ---------------------------------------------------------------- shapes

@@ -272,6 +272,21 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.tiles_per_plane = cdiv(d.Ho, rows);
       d.tiles_m = d.N * d.Cout * d.tiles_per_plane;
       d.tiles_n = 1;
+      d.planes_per_tile = 1;
+      const int in_rows_all = std::min(d.H, (d.Ho - 1) * d.sh - d.ph + d.kh);
+      if (rows == d.Ho && in_rows_all > 0) {
+        // small planes: several whole planes per tile, so that the threads
+        // of a tile have outputs to compute
+        const int in_rows = in_rows_all;
+        const int planes = d.N * d.Cout;
+        const int p = std::min({kThreads / (d.Ho * d.Wo), kPoolLdsFloats / (in_rows * d.W),
+                                planes / kPoolMinTiles});
+        if (p > 1) {
+          d.planes_per_tile = p;
+          d.pool_in_rows = in_rows;
+          d.tiles_m = cdiv(planes, p);
+        }
+      }
     } else {
       d.tiles_per_plane = cdiv((int64_t)d.Ho * d.Wo, kEltPerTile);
       d.tiles_m = d.N * d.Cout * d.tiles_per_plane;
@@ -288,6 +303,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.fd_bpr = fd(d.sep_bpr);
     d.fd_tpp = fd(d.tiles_per_plane);
     d.fd_c = fd(d.Cout);
+    d.fd_pin = fd(d.pool_in_rows * d.W);
   }
   // tile order: producers before consumers (depth), longer tiles first; the
   // ops are stored in that order so that each owns a contiguous tile range

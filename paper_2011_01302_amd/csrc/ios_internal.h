@@ -96,6 +96,10 @@ __host__ __device__ inline int sep_lds_bytes(int CinP, int K, int nbt) {
 // whose input rows (with halo) fit in kPoolLdsFloats of LDS.
 constexpr int kEltPerTile = 4 * kThreads;
 constexpr int kPoolLdsFloats = 8192;
+// Pools whose whole plane fits one tile take several planes per tile when a
+// plane has fewer outputs than a workgroup has threads, as long as the launch
+// keeps at least this many pool tiles.
+constexpr int kPoolMinTiles = 256;
 
 // Division by a run-time constant d >= 1 as a multiply-high and a shift:
 // n / d == (umulhi(n, mul) + n) >> shr for 0 <= n < 2^31 (Granlund and
@@ -130,6 +134,8 @@ struct alignas(16) DevOp {
   float inv_n;                 // MEAN: 1 / n_in
   int32_t rows_per_tile;       // POOL: output rows per tile
   int32_t tiles_per_plane;     // POOL / ADD / MEAN: tiles per (image, channel) plane
+  int32_t planes_per_tile;     // POOL: whole planes per tile when a plane is small (else 1)
+  int32_t pool_in_rows;        // POOL with planes_per_tile > 1: input rows staged per plane
   int32_t sep_k;               // SEP: depthwise window K (3, 5 or 7)
   int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
   int32_t sep_bpr;             // SEP: 16-pixel blocks per output row
@@ -141,6 +147,7 @@ struct alignas(16) DevOp {
   FDiv fd_spt, fd_kw;          // CONV: k-steps per tap, kw
   FDiv fd_pimg, fd_bpr;        // SEP: 16-pixel blocks per image, per row
   FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
+  FDiv fd_pin;                 // POOL with planes_per_tile > 1: floats staged per plane
   const float *wpk;            // CONV: see pack_conv_weights; SEP: pointwise [CinP][Npad]
   const float *bias;           // [Npad]
   const float *dw;             // SEP: depthwise [CinP][sep_kkp(K)], kh x kw taps at the top left of K x K

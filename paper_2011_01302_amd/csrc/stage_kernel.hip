@@ -537,12 +537,66 @@ __device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const
 
 constexpr int kPoolBatch = 4;   // staging loads per thread in flight
 
+// planes_per_tile whole (image, channel) planes of a pool whose planes are
+// small: the planes' input rows are staged in LDS one plane after another
+// (coalesced, each input value read once), then every output of the tile is
+// reduced from LDS.  Planes run over images: plane = image * C + channel.
+template <bool COH>
+__device__ __forceinline__ void pool_planes_tile(const Slots &sl, const DevOp &o, int t, bool is_max,
+                                                 float *lds) {
+  const int tid = threadIdx.x;
+  const int C = o.Cout, H = o.H, W = o.W, Wo = o.Wo, howo = o.Ho * Wo;
+  const int p0 = t * o.planes_per_tile, np = min(o.planes_per_tile, o.N * C - p0);
+  const int rows = o.pool_in_rows, n_pl = rows * W, n_in = np * n_pl;
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  for (int base = 0; base < n_in; base += kPoolBatch * kThreads) {
+    float v[kPoolBatch];
+#pragma unroll
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const int i = base + k * kThreads + tid;
+      const int p = fdiv(i, o.fd_pin), j = i - p * n_pl;
+      const int img = fdiv(p0 + p, o.fd_c), c = p0 + p - img * C;
+      v[k] = bld(xr, i < n_in ? ((img * o.in_ctot[0] + o.in_coff[0] + c) * H * W + j) * 4 : kOOB, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const int i = base + k * kThreads + tid;
+      if (i < n_in) lds[i] = v[k];
+    }
+  }
+  __syncthreads();
+  const float inv = 1.0f / (float)(o.kh * o.kw);
+  for (int i = tid; i < np * howo; i += kThreads) {
+    const int p = fdiv(i, o.fd_howo), r = i - p * howo;
+    const int oh = fdiv(r, o.fd_wo), ow = r - oh * Wo;
+    const float *pl = lds + p * n_pl;
+    float acc = is_max ? -INFINITY : 0.f;
+    for (int u = 0; u < o.kh; ++u) {
+      const int ih = oh * o.sh + u - o.ph;
+      if (ih < 0 || ih >= rows) continue;          // outside the image
+      for (int q = 0; q < o.kw; ++q) {
+        const int iw = ow * o.sw + q - o.pw;
+        if (iw < 0 || iw >= W) continue;
+        const float v = pl[ih * W + iw];
+        acc = is_max ? fmaxf(acc, v) : acc + v;
+      }
+    }
+    if (!is_max) acc *= inv;
+    const int img = fdiv(p0 + p, o.fd_c), c = p0 + p - img * C;
+    st<COH>(sl[o.route_slot[0]] + (size_t)(img * o.route_ctot[0] + o.route_coff[0] + c) * howo + r, acc);
+  }
+}
+
 // One band of output rows of one (image, channel) plane: the input rows it
 // needs are staged in LDS with coalesced loads (each input value is read from
 // memory once), then every output is reduced from LDS.
 template <bool COH>
 __device__ __forceinline__ void pool_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, bool is_max,
                                           float *lds) {
+  if (o.planes_per_tile > 1) {
+    pool_planes_tile<COH>(sl, o, t, is_max, lds);
+    return;
+  }
   const int tid = threadIdx.x;
   const int C = o.Cout, H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo;
   const int plane = fdiv(t, o.fd_tpp), band = t - plane * o.tiles_per_plane;
@@ -815,6 +869,8 @@ int op_lds_bytes(const DevOp &op) {
     return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
   }
   if (op.kind == DK_SEP) return sep_lds_bytes(op.CinP, op.sep_k, op.sep_nbt);
+  if ((op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG) && op.planes_per_tile > 1)
+    return op.planes_per_tile * op.pool_in_rows * op.W * (int)sizeof(float);
   if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
     return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
   return 0;

@@ -369,6 +369,38 @@ def test_parity_ragged_shapes(batch, tile, offset, monkeypatch):
     g.close()
 
 
+def pool_planes_spec(batch):
+    """Pools over many small planes (several whole planes per tile from 512
+    planes up): inputs read from concat slices, outputs written into one,
+    a global average pool, planes of a tile crossing an image boundary and
+    a last tile with fewer planes."""
+    conv = lambda n, co: {"name": n, "kind": "conv", "in": ["x"], "cout": co, "kh": 1, "kw": 1, "sh": 1,
+                          "sw": 1, "ph": 0, "pw": 0, "pre_relu": 0, "post_relu": 0}
+    pool = lambda n, kind, i, kh, kw, s, p: {"name": n, "kind": kind, "in": [i], "kh": kh, "kw": kw,
+                                            "sh": s, "sw": s, "ph": p, "pw": p}
+    ops = [conv("c1", 400), conv("c2", 400),
+           {"name": "cat", "kind": "concat", "in": ["c1", "c2"]},
+           pool("mp", "maxpool", "c2", 3, 3, 2, 1),
+           pool("ap", "avgpool", "c1", 3, 3, 1, 1),
+           pool("gp", "avgpool", "c2", 7, 7, 1, 0),
+           pool("m2", "maxpool", "c1", 3, 3, 2, 1),
+           {"name": "outc", "kind": "concat", "in": ["mp", "m2"]}]
+    return {"name": "pool_planes", "batch": batch, "inputs": [{"name": "x", "c": 5, "h": 7, "w": 7}],
+            "ops": ops, "outputs": ["cat", "ap", "gp", "outc"]}
+
+
+@pytest.mark.parametrize("batch", [1, 2, 3])
+def test_parity_pool_planes(batch):
+    spec = pool_planes_spec(batch)
+    ten = W.make_tensors(spec, 5)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), ref, f"pool planes bs{batch}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
 @pytest.mark.parametrize("tile", ["0", "1", "4"])
 def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     """Forced conv tile shapes over several small images (the 16-pixel

@@ -95,6 +95,20 @@ def stage_bytes(spec, batch, names):
 
 # ------------------------------------------------------------------ timing
 
+def conv_tiles(I, g):
+    """The graph's current conv tile shapes, {unit id: shape}."""
+    return {g.tid[op["name"]]: I.ios_get_conv_tile(g.handle, g.tid[op["name"]])
+            for op in g.spec["ops"] if op["kind"] == "conv"}
+
+
+def tune_for(I, g, q, iso):
+    """Start from the shapes each conv chose alone (iso), then pick shapes per
+    stage of q; returns the stages' summed measured latency (ns)."""
+    for u, t in iso.items():
+        I.ios_set_conv_tile(g.handle, u, t)
+    return I.ios_schedule_tune_tiles(g.handle, q)
+
+
 def time_steps(I, g, q, ins, outs, stream, warmup, steps, torch):
     ip = [t.data_ptr() for t in ins]
     op = [t.data_ptr() for t in outs]
@@ -288,6 +302,7 @@ def run_suite(args):
         outs = [torch.empty((batch,) + shp[o], device=dev) for o in spec["outputs"]]
         stream = torch.cuda.current_stream().cuda_stream
         row = {"config": config, "batch": batch}
+        iso = conv_tiles(I, g)
         work = unit_work(spec, batch)
         row["gflop"] = round(sum(w[0] + w[1] for w in work.values()) / 1e9, 4)
         for name, mode in (("ios", I.IOS_SCHED_DP), ("sequential", I.IOS_SCHED_SEQUENTIAL),
@@ -299,8 +314,11 @@ def run_suite(args):
                 o.verify_reps = 20                     # the picked stages measured in full
             print(f"[suite] {config} bs{batch} {name}: scheduling", file=sys.stderr, flush=True)
             t0 = time.perf_counter()
+            for u, t in iso.items():
+                I.ios_set_conv_tile(g.handle, u, t)
             q, pred = I.ios_schedule(g.handle, o)
             search = time.perf_counter() - t0
+            tune_for(I, g, q, iso)
             steps = max(20, min(args.steps, int(2e5 / max(1.0, row["gflop"] * 1e3))))
             us = time_steps(I, g, q, ins, outs, stream, 10, steps, torch)
             assert I.ios_device_status(g.handle, stream) == 0
@@ -374,10 +392,16 @@ def run_next(args):
             o.verify_reps = 20                      # the picked stages measured in full
         return o
 
+    isos = {}
+
     def timed(g, q, ins, outs, gflop):
+        iso = isos.setdefault(g.handle, conv_tiles(I, g))
+        tune_for(I, g, q, iso)
         steps = max(20, min(args.steps, int(2e5 / max(1.0, gflop * 1e3))))
         us = time_steps(I, g, q, ins, outs, stream, 10, steps, torch)
         assert I.ios_device_status(g.handle, stream) == 0
+        for u, t in iso.items():                    # searches start from the isolated choice
+            I.ios_set_conv_tile(g.handle, u, t)
         return round(us, 2)
 
     # (1) strategy ablation
@@ -485,20 +509,24 @@ def run_network(args):
         row = {"network": net, "batch": args.batch, "units": len(block_of), "blocks": len(names),
                "gflop": round(gflop, 3)}
         per_block = {n: {} for n in names}
+        iso = conv_tiles(I, g)
         for name, mode in (("ios", I.IOS_SCHED_DP), ("sequential", I.IOS_SCHED_SEQUENTIAL),
                            ("greedy", I.IOS_SCHED_GREEDY)):
             o = I.ios_sched_opts_default()
             o.mode = mode
             o.r, o.s = args.r, args.s
             print(f"[network] {net}: {name} schedule", file=sys.stderr, flush=True)
+            for u, t in iso.items():
+                I.ios_set_conv_tile(g.handle, u, t)
             t0 = time.perf_counter()
             q, pred = I.ios_schedule(g.handle, o)
             search = time.perf_counter() - t0
+            tuned = tune_for(I, g, q, iso)
             sched = I.ios_schedule_get(q)
             us = time_steps(I, g, q, ins, outs, stream, 10, max(20, min(args.steps, 100)), torch)
             assert I.ios_device_status(g.handle, stream) == 0
             entry = {"us": round(us, 2), "stages": len(sched), "predicted_us": round(pred / 1e3, 2),
-                     "search_s": round(search, 2)}
+                     "tuned_us": round(tuned / 1e3, 2), "search_s": round(search, 2)}
             if mode == I.IOS_SCHED_DP:
                 st, tr, ms = I.ios_schedule_stats(q)
                 entry.update({"states": st, "transitions": tr, "stages_measured": ms,
@@ -618,6 +646,8 @@ def main():
     stream = torch.cuda.current_stream().cuda_stream
 
     conv_units = [op["name"] for op in spec["ops"] if op["kind"] == "conv"]
+    iso = conv_tiles(I, g)
+    tuned_ns = None
     if args.plan_from:
         plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{")][-1]
         for name, shape in plan["tiles"].items():
@@ -645,11 +675,14 @@ def main():
         q, pred_ns = I.ios_schedule(g.handle, opts)
         search_s = time.perf_counter() - t0
         states, transitions, measured = I.ios_schedule_stats(q)
+        # conv tile shapes per stage, in the stage's company
+        tuned_ns = I.ios_schedule_tune_tiles(g.handle, q)
     tiles = {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in conv_units}
     if args.dump_costs:
         I.ios_schedule_dump_costs(g.handle, args.dump_costs)
     stages = I.ios_schedule_get(q)
-    print(f"[bench] search {search_s:.2f}s, {len(stages)} stages, predicted {pred_ns} ns",
+    print(f"[bench] search {search_s:.2f}s, {len(stages)} stages, predicted {pred_ns} ns, "
+          f"tuned {tuned_ns} ns",
           file=sys.stderr, flush=True)
 
     us = time_steps(I, g, q, ins, outs, stream, args.warmup, args.steps, torch)
@@ -709,7 +742,7 @@ def main():
         "schedule": stage_rows,
         "tiles": tiles,
         "search": {"seconds": round(search_s, 3), "states": states, "transitions": transitions,
-                   "stages_measured": measured, "predicted_ns": pred_ns},
+                   "stages_measured": measured, "predicted_ns": pred_ns, "tuned_ns": tuned_ns},
         "throughput_img_per_s": round(args.batch / us * 1e6, 1),
     }
     if not args.no_baselines:
@@ -717,7 +750,10 @@ def main():
         for name, mode in (("sequential", I.IOS_SCHED_SEQUENTIAL), ("greedy", I.IOS_SCHED_GREEDY)):
             o = I.ios_sched_opts_default()
             o.mode = mode
+            for u, t in iso.items():
+                I.ios_set_conv_tile(g.handle, u, t)
             qb, _ = I.ios_schedule(g.handle, o)
+            tune_for(I, g, qb, iso)
             ub = time_steps(I, g, qb, ins, outs, stream, args.warmup, args.steps, torch)
             base[name] = {"us": round(ub, 3), "launches": len(I.ios_schedule_get(qb)),
                           "speedup_of_ios": round(ub / us, 3)}

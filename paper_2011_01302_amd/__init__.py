@@ -50,7 +50,7 @@ EXPORTED = ["ios_graph_create", "ios_graph_destroy", "ios_add_input", "ios_add_o
             "ios_stage_mergeable", "ios_profile_stage", "ios_get_conv_tile", "ios_set_conv_tile",
             "ios_sched_opts_default", "ios_schedule",
             "ios_schedule_from_stages", "ios_schedule_get", "ios_schedule_stats",
-            "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_timed",
+            "ios_schedule_tune_tiles", "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_timed",
             "ios_device_status", "ios_last_error"]
 
 
@@ -101,6 +101,7 @@ _sig = {
     "ios_schedule_get": (ctypes.c_int, [_P, _pi32, ctypes.POINTER(_pi32), ctypes.POINTER(_pi32),
                                         ctypes.POINTER(_pi32)]),
     "ios_schedule_stats": (ctypes.c_int, [_P, _pi64, _pi64, _pi64]),
+    "ios_schedule_tune_tiles": (ctypes.c_int, [_P, _P, ctypes.POINTER(ios_sched_opts), _pi64]),
     "ios_schedule_destroy": (None, [_P]),
     "ios_schedule_dump_costs": (ctypes.c_int, [_P, ctypes.c_char_p]),
     "ios_run": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), ctypes.POINTER(_P), _P]),
@@ -265,6 +266,15 @@ def ios_schedule_stats(q: int) -> Tuple[int, int, int]:
     a, b, c = _i64(), _i64(), _i64()
     _check(_lib.ios_schedule_stats(q, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
     return a.value, b.value, c.value
+
+
+def ios_schedule_tune_tiles(g: int, q: int, opts: Optional[ios_sched_opts] = None) -> int:
+    """Per-stage conv tile shapes for schedule q (kept on the graph); returns
+    the sum of the stages' measured latencies in ns."""
+    opts = opts or ios_sched_opts_default()
+    c = _i64()
+    _check(_lib.ios_schedule_tune_tiles(g, q, ctypes.byref(opts), ctypes.byref(c)))
+    return c.value
 
 
 def ios_schedule_destroy(q: int) -> None:

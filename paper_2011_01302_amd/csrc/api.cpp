@@ -1,5 +1,6 @@
 // extern "C" entry points of libios (declared and documented in ios.h).
 // Every call catches the library's internal errors and returns a code.
+#include <cstdlib>
 #include <algorithm>
 #include <cstring>
 #include <new>
@@ -218,6 +219,80 @@ int ios_schedule_from_stages(ios_graph *g, int32_t n_stages, const int32_t *stag
     need_final(g);
     need(out != nullptr, "null argument");
     *out = schedule_from_stages(g, n_stages, stage_offsets, unit_ids, strategies);
+  });
+}
+
+// Conv tile shapes chosen per stage: each stage of q is measured with its
+// convs' shapes varied one conv at a time (all of them together in a merge
+// stage, whose merged conv takes one shape), keeping a change only when the
+// stage gets faster by more than kStageTileSlack.  A shape measured alone
+// fills the GPU by itself; inside a stage other operators share the CUs, so
+// larger tiles can pay off there.
+static constexpr double kStageTileSlack = 0.02;
+
+int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opts *opts,
+                            int64_t *cost_ns) {
+  return guarded([&] {
+    need_final(g);
+    need(q != nullptr && q->g == g, "schedule does not belong to this graph");
+    need(cost_ns != nullptr, "null argument");
+    ios_sched_opts o;
+    ios_sched_opts_default(&o);
+    if (opts) o = *opts;
+    need(o.warmup >= 0 && o.reps >= 1 && o.repeats >= 1, "bad profiling counts");
+    ensure_device(g);
+    const bool forced = std::getenv("IOS_CONV_TILE") != nullptr;
+    int64_t total = 0;
+    for (size_t k = 0; k < q->strategies.size(); ++k) {
+      std::vector<int> ops, convs;
+      for (int i = q->offsets[k]; i < q->offsets[k + 1]; ++i) {
+        const int op = unit_op_of_tensor(g, q->unit_ids[i]);
+        ops.push_back(op);
+        if (g->ops[op].d.kind == IOS_CONV) convs.push_back(op);
+      }
+      const int strat = q->strategies[k];
+      auto measure = [&] { return profile_stage(g, ops, strat, o.warmup, o.reps, o.repeats); };
+      int64_t best = measure();
+      if (!forced && !convs.empty()) {
+        // each entry: the convs that take one shape together
+        std::vector<std::vector<int>> knobs;
+        if (strat == IOS_MERGE) {
+          int largest = convs[0];
+          for (int c : convs)
+            if (g->ops[c].d.cout > g->ops[largest].d.cout) largest = c;
+          for (int c : convs) g->ops[c].tcfg = g->ops[largest].tcfg;
+          best = measure();
+          knobs.push_back(convs);
+        } else {
+          for (int c : convs) knobs.push_back({c});
+        }
+        for (int pass = 0; pass < 2; ++pass) {
+          bool improved = false;
+          for (const auto &kn : knobs) {
+            const int cur = g->ops[kn[0]].tcfg;
+            int keep = cur;
+            for (int t = 0; t < TC_COUNT; ++t) {
+              if (t == cur) continue;
+              for (int c : kn) g->ops[c].tcfg = t;
+              const int64_t ns = measure();
+              if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
+                best = ns;
+                keep = t;
+                improved = true;
+              }
+            }
+            for (int c : kn) g->ops[c].tcfg = keep;
+          }
+          if (!improved) break;
+        }
+      }
+      total += best;
+    }
+    // stages compiled for q before this call used the old shapes
+    for (auto &cs : q->compiled)
+      if (cs) free_stage(cs.get());
+    q->compiled.clear();
+    *cost_ns = total;
   });
 }
 

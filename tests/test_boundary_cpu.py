@@ -228,6 +228,7 @@ def test_graph_error_paths():
     expect("IOS_E_STATE", I.ios_graph_blocks, g)
     expect("IOS_E_STATE", I.ios_schedule, g, None, lambda *a: 1)
     expect("IOS_E_STATE", I.ios_get_conv_tile, g, x)
+    expect("IOS_E_STATE", I.ios_schedule_tune_tiles, g, None)
     expect("IOS_E_UNSUPPORTED", I.ios_mark_output, g, x)
     c = I.ios_add_op(g, desc(I.IOS_CONV, 3, 3, p=1), [x], w)
     cat = I.ios_add_op(g, desc(I.IOS_CONCAT), [c])
@@ -243,6 +244,19 @@ def test_graph_error_paths():
     expect("IOS_E_ARG", I.ios_get_conv_tile, g, x)                            # not a unit
     expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, I.IOS_CONV_TILE_SHAPES)
     expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, -1)
+    # per-stage tile choice: argument errors come before any device work
+    q = I.ios_schedule_from_stages(g, [[c]], [I.IOS_CONCURRENT])
+    o = I.ios_sched_opts_default()
+    o.reps = 0
+    expect("IOS_E_ARG", I.ios_schedule_tune_tiles, g, q, o)
+    expect("IOS_E_ARG", I.ios_schedule_tune_tiles, g, None)
+    g2 = I.ios_graph_create(1)
+    y2 = I.ios_add_input(g2, 1, 2, 2)
+    I.ios_mark_output(g2, I.ios_add_op(g2, desc(I.IOS_ADD), [y2]))
+    I.ios_graph_finalize(g2)
+    expect("IOS_E_ARG", I.ios_schedule_tune_tiles, g2, q)                    # another graph's schedule
+    I.ios_graph_destroy(g2)
+    I.ios_schedule_destroy(q)
     I.ios_graph_destroy(g)
     expect("IOS_E_ARG", I.ios_graph_create, 0)
 

@@ -106,5 +106,8 @@ def test_network_device_dp_replays_in_oracle(tmp_path):
     lib = [(sorted(g.names(ids)), t) for ids, t in I.ios_schedule_get(q)]
     assert lib == stages
     assert total == cost
+    # conv tile shapes chosen per stage, then the same schedule again
+    assert I.ios_schedule_tune_tiles(g.handle, q, o) > 0
+    check(run(g, q, spec, ten), reference(), "dp, per-stage tiles")
     I.ios_schedule_destroy(q)
     g.close()

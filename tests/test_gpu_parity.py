@@ -265,6 +265,32 @@ def test_conv_tile_shapes_read_and_replayed():
     g.close()
 
 
+def test_schedule_tune_tiles_per_stage(monkeypatch):
+    """Per-stage conv tile shapes: the call measures every stage, leaves the
+    chosen shapes on the graph and the schedule runs with them (results still
+    match); with IOS_CONV_TILE set the shapes stay as they are."""
+    spec, ten = case("inception")
+    g = I.Graph(spec, ten)
+    convs = [u["name"] for u in W.unit_ops(spec) if u["kind"] == "conv"]
+    o = I.ios_sched_opts_default()
+    o.warmup, o.reps, o.repeats = 2, 5, 3
+    q, _ = I.ios_schedule(g.handle, o)
+    check(run(g, q, spec, ten), reference("inception"), "inception/dp")
+    total = I.ios_schedule_tune_tiles(g.handle, q, o)
+    assert total > 0
+    tiles = {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in convs}
+    assert all(0 <= v < I.IOS_CONV_TILE_SHAPES for v in tiles.values())
+    for st_ids, strat in I.ios_schedule_get(q):
+        if strat == I.IOS_MERGE:                       # a merged conv takes one shape
+            assert len({tiles[n] for n in g.names(st_ids)}) == 1
+    check(run(g, q, spec, ten), reference("inception"), "inception/dp/tuned tiles")
+    monkeypatch.setenv("IOS_CONV_TILE", "2")
+    assert I.ios_schedule_tune_tiles(g.handle, q, o) > 0
+    assert {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in convs} == tiles
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_run_timed_and_determinism():
     spec, ten = case("inception")
     g = I.Graph(spec, ten)

@@ -1,8 +1,9 @@
-"""GPU parity on a whole network: Inception-V3 (3x299x299 -> 1000 logits,
-13 blocks, 109 schedule units, random weights) through the C ABI against the
-fp64 oracle (max|gpu - oracle| / max|oracle| <= 1e-4 on the logits), under
-the baseline schedules and under the DP run block by block on the device,
-whose schedule must equal the oracle DP replayed on the dumped cost table."""
+"""GPU parity on whole networks: Inception-V3 (3x299x299 -> 1000 logits,
+13 blocks, 109 schedule units) and SqueezeNet v1.0 (3x227x227 -> 1000, 12
+blocks, 28 units), random weights, through the C ABI against the fp64 oracle
+(max|gpu - oracle| / max|oracle| <= 1e-4 on the logits), under the baseline
+schedules and under the DP run block by block on the device, whose schedule
+must equal the oracle DP replayed on the dumped cost table."""
 import functools
 import json
 
@@ -20,18 +21,17 @@ from oracle import evaluator as E          # noqa: E402
 from oracle import schedule as O           # noqa: E402
 
 DEV = "cuda:0"
-NET = "inception_v3"
 
 
 @functools.lru_cache(maxsize=None)
-def case():
-    return W.make(NET, 1, 0)
+def case(net):
+    return W.make(net, 1, 0)
 
 
 @functools.lru_cache(maxsize=None)
-def reference():
-    spec, ten = case()
-    print("[gpu-case] oracle evaluation of the whole network", flush=True)
+def reference(net):
+    spec, ten = case(net)
+    print(f"[gpu-case] oracle evaluation of {net}", flush=True)
     return E.outputs(spec, ten)
 
 
@@ -59,14 +59,15 @@ def _print_case(request):
     yield
 
 
-def test_network_parity_baseline_schedules():
+@pytest.mark.parametrize("net", W.NETWORK_NAMES)
+def test_network_parity_baseline_schedules(net):
     """Sequential (one unit per launch), greedy (every ready unit per launch)
     and one stage per block (branches chained inside the launch, chains of up
     to five convs)."""
-    spec, ten = case()
-    ref = reference()
+    spec, ten = case(net)
+    ref = reference(net)
     g = I.Graph(spec, ten)
-    assert len(g.blocks()) == 13
+    assert len(g.blocks()) == len(spec["block_names"])
     for mode in (I.IOS_SCHED_SEQUENTIAL, I.IOS_SCHED_GREEDY):
         o = I.ios_sched_opts_default()
         o.mode = mode
@@ -80,16 +81,17 @@ def test_network_parity_baseline_schedules():
     g.close()
 
 
-def test_network_device_dp_replays_in_oracle(tmp_path):
-    """Algorithm 1 on each of the 13 blocks with on-device stage profiling
+@pytest.mark.parametrize("net", W.NETWORK_NAMES)
+def test_network_device_dp_replays_in_oracle(net, tmp_path):
+    """Algorithm 1 on each block with on-device stage profiling
     (light protocol); the outputs must match and the schedule must be the
     oracle DP's on the dumped cost table, block by block."""
-    spec, ten = case()
+    spec, ten = case(net)
     g = I.Graph(spec, ten)
     o = I.ios_sched_opts_default()
     o.warmup, o.reps, o.repeats = 1, 3, 1
     q, cost = I.ios_schedule(g.handle, o)
-    check(run(g, q, spec, ten), reference(), "dp")
+    check(run(g, q, spec, ten), reference(net), "dp")
     path = tmp_path / "costs.jsonl"
     I.ios_schedule_dump_costs(g.handle, str(path))
     table = {}
@@ -108,6 +110,6 @@ def test_network_device_dp_replays_in_oracle(tmp_path):
     assert total == cost
     # conv tile shapes chosen per stage, then the same schedule again
     assert I.ios_schedule_tune_tiles(g.handle, q, o) > 0
-    check(run(g, q, spec, ten), reference(), "dp, per-stage tiles")
+    check(run(g, q, spec, ten), reference(net), "dp, per-stage tiles")
     I.ios_schedule_destroy(q)
     g.close()

@@ -1,5 +1,5 @@
-"""Whole-network workload (Inception-V3, scheduled block by block): the
-description against the network's published layer table, and the oracle's
+"""Whole-network workloads (Inception-V3, SqueezeNet; scheduled block by block): the
+descriptions against the networks' published layer tables, and the oracle's
 block split and state spaces against closed forms.  No GPU."""
 import math
 
@@ -111,3 +111,26 @@ def test_inception_v3_dp_not_worse_than_baselines():
                       else 10 ** 9) for v in range(blk.n))
         assert res.cost <= seq
         assert res.cost <= 5 * blk.n + 3 * blk.n
+
+
+def test_squeezenet_layer_table():
+    """SqueezeNet v1.0's published layer table at 227x227: conv1 111x111x96,
+    max-pool 55x55x96, fire2..4 at 55x55 (128, 128, 256), max-pool 27x27,
+    fire5..8 at 27x27 (256, 384, 384, 512), max-pool 13x13, fire9 512,
+    conv10 13x13x1000, global pool 1x1x1000; every fire module a 3-unit block
+    whose two expand convs read the squeeze output and can merge."""
+    s = W.SPECS["squeezenet"]()
+    shp = W.infer_shapes(s)
+    assert shp["conv1"] == (96, 111, 111) and shp["pool1"] == (96, 55, 55)
+    assert [shp[f"f{m}"] for m in (2, 3, 4)] == [(128, 55, 55), (128, 55, 55), (256, 55, 55)]
+    assert shp["pool4"] == (256, 27, 27)
+    assert [shp[f"f{m}"][0] for m in (5, 6, 7, 8)] == [256, 384, 384, 512]
+    assert shp["pool8"] == (512, 13, 13) and shp["f9"] == (512, 13, 13)
+    assert shp["conv10"] == (1000, 13, 13) and shp["gpool"] == (1000, 1, 1)
+    blocks = O.blocks_of(s)
+    assert [b.n for b in blocks] == [2, 3, 3, 3, 1, 3, 3, 3, 3, 1, 3, 2]
+    assert len(s["block_names"]) == len(blocks)
+    for b in blocks:
+        if b.n == 3:
+            assert O.mergeable(b, 0b110)
+            assert O.ios_dp(b, lambda m, t: 1, 3, 8).states == 5    # a squeeze unit feeding two

@@ -14,6 +14,8 @@ and, for the block-wise whole-network runs (not one of the blocks above):
 
   inception_v3   the whole Inception-V3 network, 3x299x299 -> 1000 logits,
                  13 blocks (stem, eleven modules, head)
+  squeezenet     the whole SqueezeNet v1.0 network, 3x227x227 -> 1000,
+                 12 blocks (conv1 + pool, eight fire modules, two pools, head)
 
 A workload is a plain description (``spec``) plus a dict of float32 numpy
 arrays (``tensors``).  The description lists the operators in insertion
@@ -318,10 +320,40 @@ def spec_inception_v3(batch: int = 1, seed: int = 0) -> dict:
             "ops": ops, "outputs": ["head_fc"], "block_names": INCEPTION_V3_BLOCKS}
 
 
-NETWORK_NAMES = ["inception_v3"]
+def spec_squeezenet(batch: int = 1, seed: int = 0) -> dict:
+    """SqueezeNet v1.0 (Iandola et al.) from its published layer table, 227x227
+    input: conv1 7x7/2 (96), max-pool 3x3/2, fire2..fire9 with max-pools
+    3x3/2 after fire4 and fire8 (the fire modules of the stack above), conv10
+    1x1 (1000) with ReLU, global 13x13 average pooling.  Blocks: conv1 and
+    its pool, each fire module, each later pool, conv10 and the global pool."""
+    ops = [_conv("conv1", "x", 96, 7, 0, stride=2, block=0),
+           _pool("pool1", "conv1", "maxpool", 3, 2, 0, block=0)]
+    cur, block = "pool1", 1
+    for m, (s, e) in enumerate(FIRE, start=2):
+        ops.append(_conv(f"f{m}sq", cur, s, 1, 0, block=block))
+        ops.append(_conv(f"f{m}e1", f"f{m}sq", e, 1, 0, block=block))
+        ops.append(_conv(f"f{m}e3", f"f{m}sq", e, 3, 1, block=block))
+        ops.append(_view(f"f{m}", "concat", [f"f{m}e1", f"f{m}e3"]))
+        cur = f"f{m}"
+        block += 1
+        if m in (4, 8):
+            ops.append(_pool(f"pool{m}", cur, "maxpool", 3, 2, 0, block=block))
+            cur = f"pool{m}"
+            block += 1
+    ops += [_conv("conv10", cur, 1000, 1, 0, block=block),
+            _pool("gpool", "conv10", "avgpool", 13, 1, 0, block=block)]
+    names = ["conv1", "fire2", "fire3", "fire4", "pool4", "fire5", "fire6", "fire7", "fire8", "pool8",
+             "fire9", "head"]
+    return {"name": "squeezenet", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 3, "h": 227, "w": 227}],
+            "ops": ops, "outputs": ["gpool"], "block_names": names}
+
+
+NETWORK_NAMES = ["inception_v3", "squeezenet"]
 
 SPECS = {"tiny": spec_tiny, "inception": spec_inception, "randwire": spec_randwire,
-         "nasnet": spec_nasnet, "squeeze": spec_squeeze, "inception_v3": spec_inception_v3}
+         "nasnet": spec_nasnet, "squeeze": spec_squeeze, "inception_v3": spec_inception_v3,
+         "squeezenet": spec_squeezenet}
 
 
 # ---------------------------------------------------------------- shapes

@@ -831,6 +831,21 @@ __device__ __forceinline__ float *stage_prologue(const int4 *__restrict__ table,
 // guarantee the residency too, but costs about 20 us per launch here.)
 // The table pointer and size come first so that they can be preloaded into
 // scalar registers at dispatch.
+// Workgroups are handed to the 8 XCDs in turn (workgroup b to XCD b % 8),
+// and each XCD has its own L2.  A launch without in-stage dependencies runs
+// tile xcd_tile(b) in workgroup b: runs of kXcdChunk consecutive tiles (the
+// N-tiles of one M-tile, neighbouring M-tiles whose input rows and cache
+// lines overlap) land on one XCD, while the chunks still start in tile
+// order.  A permutation of [0, n); the last n % (8 kXcdChunk) tiles keep
+// their index.
+constexpr int kXcdChunk = 4;
+__device__ __forceinline__ int xcd_tile(int b, int n) {
+  const int full = n / (8 * kXcdChunk) * (8 * kXcdChunk);
+  if (b >= full) return b;
+  const int xcd = b & 7, local = b >> 3;
+  return ((local / kXcdChunk) * 8 + xcd) * kXcdChunk + local % kXcdChunk;
+}
+
 template <int KV, bool PERSIST>
 __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restrict__ table, int table_words,
                                                              StageArgs a) {
@@ -840,7 +855,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   const Slots sl{(float *const *)meta};
   const int32_t *tab = meta + kSlotWords;
   if constexpr (!PERSIST) {
-    process_tile<KV>(a, sl, tab, blockIdx.x, true, lds);
+    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x), true, lds);
     return;
   }
   const int n_tiles = U(tab[1]), n_ops = U(tab[0]);

@@ -188,11 +188,19 @@ def write_traffic(args, fetch_dir, write_dir):
         timed = stage[-n:]
         copy_bytes = meta["copy_mb"] << 20
         scale = copy_bytes / (copy * 1024.0)
+        ns = meta["stages"]
         res[counter] = {"kib_per_launch_raw": sum(timed) / len(timed), "copy_kib_raw": copy,
-                        "scale": scale, "bytes_per_launch": sum(timed) / len(timed) * 1024.0 * scale}
+                        "scale": scale, "bytes_per_launch": sum(timed) / len(timed) * 1024.0 * scale,
+                        "per_stage_bytes": [statistics.mean(timed[k::ns]) * 1024.0 * scale for k in range(ns)]}
     out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": kernel_sha(),
            "fetch": res["FETCH_SIZE"], "write": res["WRITE_SIZE"],
            "traffic_bytes_per_launch": res["FETCH_SIZE"]["bytes_per_launch"] + res["WRITE_SIZE"]["bytes_per_launch"]}
+    sched = json.load(open(os.path.join(fetch_dir, "bench.json"))).get("schedule")
+    if sched:
+        out["per_stage"] = [{"units": st["units"], "strategy": st["strategy"],
+                             "fetch_bytes": round(f), "write_bytes": round(w)}
+                            for st, f, w in zip(sched, res["FETCH_SIZE"]["per_stage_bytes"],
+                                                res["WRITE_SIZE"]["per_stage_bytes"])]
     path = os.path.join(ROOT, "profiles", f"traffic_{args.config}_bs{args.batch}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
@@ -269,7 +277,11 @@ def trace_summary(args, trace_dir):
     for (b, e, wg) in timed:
         by_grid.setdefault(wg, []).append(e - b)
     gaps = [timed[i + 1][0] - timed[i][1] for i in range(len(timed) - 1)]
+    ns = meta["stages"]
+    per_stage = [{"units": (meta.get("schedule") or [{}] * ns)[k].get("units"),
+                  "workgroups": timed[k][2], "median_ns": statistics.median(dur[k::ns])} for k in range(ns)]
     out = {"launches": len(timed), "mean_ns": statistics.mean(dur), "median_ns": statistics.median(dur),
+           "per_stage": per_stage,
            "by_workgroups": {str(k): {"launches": len(v), "median_ns": statistics.median(v)}
                              for k, v in sorted(by_grid.items())},
            "median_gap_ns": statistics.median(gaps) if gaps else None,

@@ -244,17 +244,20 @@ int ios_schedule_get(const ios_schedule_t *q, int32_t *n_stages, const int32_t *
 int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transitions,
                        int64_t *stages_measured);
 
-/* Choose conv tile shapes per stage of q.  The stage profiler of Sec. 4.1
- * measures a whole stage; this call uses the same measurement (o's warmup /
- * reps / repeats, or the defaults when o is NULL) to pick, for every stage,
- * the tile shapes of its convs in that stage's company: one conv at a time,
- * each shape tried, a change kept when the stage gets more than 2% faster
- * (two passes); a merge stage's convs take one shape together.  The shapes
- * stay set on the graph (ios_get_conv_tile reads them), so call it on the
- * schedule that will run; q's stages are recompiled on its next run.  A unit
- * belongs to one stage of a schedule, so the stages do not compete.  With
- * IOS_CONV_TILE set in the environment the shapes stay fixed and the stages
- * are only measured.  *cost_ns = sum of the stages' final measured latencies.
+/* Choose conv tile shapes and tile order per stage of q.  The stage profiler
+ * of Sec. 4.1 measures a whole stage; this call uses the same measurement
+ * (o's warmup / reps / repeats, or the defaults when o is NULL) to pick, for
+ * every stage, (1) how its tiles are spread over the 8 XCDs (runs of 1, 4 or
+ * 16 consecutive tiles per XCD, else the library's L2-fill model) and (2) the
+ * tile shapes of its convs in that stage's company: one conv at a time, each
+ * shape tried, a change kept when the stage gets more than 2% faster (two
+ * passes); a merge stage's convs take one shape together.  The choices stay
+ * set on the graph's units (ios_get_conv_tile reads the shapes), so call it
+ * on the schedule that will run; q's stages are recompiled on its next run.
+ * A unit belongs to one stage of a schedule, so the stages do not compete.
+ * With IOS_CONV_TILE set in the environment the shapes stay fixed (the tile
+ * order is still chosen).  *cost_ns = sum of the stages' final measured
+ * latencies.
  * Errors: IOS_E_ARG (null pointer, bad counts, schedule of another graph),
  * IOS_E_STATE (not finalized), IOS_E_HIP. */
 int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opts *o,

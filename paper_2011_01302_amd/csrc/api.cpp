@@ -222,10 +222,12 @@ int ios_schedule_from_stages(ios_graph *g, int32_t n_stages, const int32_t *stag
   });
 }
 
-// Conv tile shapes chosen per stage: each stage of q is measured with its
-// convs' shapes varied one conv at a time (all of them together in a merge
-// stage, whose merged conv takes one shape), keeping a change only when the
-// stage gets faster by more than kStageTileSlack.  A shape measured alone
+// Conv tile shapes and the XCD tile order chosen per stage: each stage of q
+// is measured with its tile order's run length set explicitly (else the
+// stage kernel's L2-fill model picks it) and with its convs' shapes varied
+// one conv at a time (all of them together in a merge stage, whose merged
+// conv takes one shape), keeping a change only when the stage gets faster by
+// more than kStageTileSlack.  A shape measured alone
 // fills the GPU by itself; inside a stage other operators share the CUs, so
 // larger tiles can pay off there.
 static constexpr double kStageTileSlack = 0.02;
@@ -252,7 +254,24 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
       }
       const int strat = q->strategies[k];
       auto measure = [&] { return profile_stage(g, ops, strat, o.warmup, o.reps, o.repeats); };
+      for (int op : ops) g->ops[op].xcd_lg = -1;
       int64_t best = measure();
+      // the XCD run length of the stage's tile order (see the stage kernel):
+      // the modelled choice, or an explicit one measured faster
+      auto tune_xcd_order = [&] {
+        int keep = -1;
+        for (int lg : {0, 2, 4}) {
+          for (int op : ops) g->ops[op].xcd_lg = lg;
+          const int64_t ns = measure();
+          if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
+            best = ns;
+            keep = lg;
+          }
+        }
+        for (int op : ops) g->ops[op].xcd_lg = keep;
+        return keep >= 0;
+      };
+      if (forced || convs.empty()) tune_xcd_order();
       if (!forced && !convs.empty()) {
         // each entry: the convs that take one shape together
         std::vector<std::vector<int>> knobs;
@@ -267,7 +286,7 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
           for (int c : convs) knobs.push_back({c});
         }
         for (int pass = 0; pass < 2; ++pass) {
-          bool improved = false;
+          bool improved = pass == 0 && tune_xcd_order();
           for (const auto &kn : knobs) {
             const int cur = g->ops[kn[0]].tcfg;
             int keep = cur;

@@ -13,6 +13,8 @@
 //     op's buffer, which stands in for the split operator (Sec. 3).
 // GenerateStage measures a stage by launching it repeatedly between HIP
 // events (Sec. 4.1).
+#include <tuple>
+#include <set>
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
@@ -78,6 +80,47 @@ void fill_common(const ios_graph *g, const Op &op, DevOp &d) {
   d.sh = op.d.stride_h; d.sw = op.d.stride_w;
   d.ph = op.d.pad_h; d.pw = op.d.pad_w;
   d.pre_relu = op.d.pre_relu; d.post_relu = op.d.post_relu;
+}
+
+// The kernel's tile order across XCDs (workgroup b on XCD b % 8 runs tile
+// xcd_tile(b, n, lg), per round of `grid` tiles).
+static int xcd_tile_host(int b, int n, int lg) {
+  const int full = (n >> (3 + lg)) << (3 + lg);
+  if (b >= full) return b;
+  const int xcd = b & 7, local = b >> 3;
+  return ((((local >> lg) << 3) + xcd) << lg) + (local & ((1 << lg) - 1));
+}
+
+// Run length 2^lg of the XCD tile order for a stage: the one whose modelled
+// L2 fills are smallest, the shorter run on a tie.  Each XCD is taken to
+// fetch, once, the input rows of every conv M-tile its workgroups touch
+// (tile rows x input channels x kernel rows) and the weights of every conv
+// N-tile (tile columns x padded reduction length).  Long runs keep the
+// N-tiles of an M-tile (shared input rows) on one XCD; the plain order keeps
+// an N-tile's weights on one XCD when an op has a multiple of 8 N-tiles.
+static int choose_xcd_runs(const std::vector<DevOp> &ops, const std::vector<int32_t> &start, int grid) {
+  const int n = start.back();
+  double best = -1.0;
+  int best_lg = 0;
+  for (int lg : {0, 2, 4}) {
+    std::set<std::tuple<int, int, int>> a_seen, b_seen;
+    double bytes = 0.0;
+    for (int b = 0; b < grid; ++b)
+      for (int base = 0; base + b < n; base += grid) {
+        const int t = base + xcd_tile_host(b, std::min(grid, n - base), lg);
+        const int i = (int)(std::upper_bound(start.begin(), start.end(), t) - start.begin()) - 1;
+        const DevOp &d = ops[i];
+        if (d.kind != DK_CONV) continue;
+        const int ti = t - start[i], tm = ti / d.tiles_n, tn = ti % d.tiles_n;
+        if (a_seen.insert({i, b & 7, tm}).second) bytes += 4.0 * tile_bm(d.tcfg) * d.CinP * d.kh;
+        if (b_seen.insert({i, b & 7, tn}).second) bytes += 4.0 * tile_bn(d.tcfg) * 16.0 * d.NG;
+      }
+    if (best < 0.0 || bytes < best) {
+      best = bytes;
+      best_lg = lg;
+    }
+  }
+  return best_lg;
 }
 
 // Per-tile work estimate (MACs or elementwise ops), for ordering tiles.
@@ -364,6 +407,12 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   cs->table[0] = n;
   cs->table[1] = start.back();
   cs->table[2] = devop_off;
+  // XCD run length: the one ios_schedule_tune_tiles set on all of the
+  // stage's units, else the L2-fill model's choice
+  int lg = g->ops[ops[0]].xcd_lg;
+  for (int i : ops)
+    if (g->ops[i].xcd_lg != lg) lg = -1;
+  cs->table[3] = lg >= 0 ? lg : choose_xcd_runs(sorted, start, cs->grid);
   for (int i = 0; i <= n; ++i) cs->table[4 + i] = start[i];
   std::memcpy(&cs->table[devop_off], cs->ops.data(), sizeof(DevOp) * n);
   size_t d0 = 0, d2 = 0;

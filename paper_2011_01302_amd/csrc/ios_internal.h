@@ -219,6 +219,7 @@ struct Op {
   // device copies (units only)
   int CinP = 0, Npad = 0, NG = 0, tcfg = TC_16x32_K8;
   int sep_nbt = 1;               // SEPCONV: output blocks of 16 channels per tile
+  int xcd_lg = -1;               // XCD run length 2^xcd_lg of the stage holding it; -1: modelled
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
 };
 

@@ -832,19 +832,17 @@ __device__ __forceinline__ float *stage_prologue(const int4 *__restrict__ table,
 // The table pointer and size come first so that they can be preloaded into
 // scalar registers at dispatch.
 // Workgroups are handed to the 8 XCDs in turn (workgroup b to XCD b % 8),
-// and each XCD has its own L2.  Workgroup b of a launch of n tiles runs
-// tile xcd_tile(b, n) (a persistent launch does so per round of gridDim.x
-// tiles): runs of kXcdChunk consecutive tiles (the
-// N-tiles of one M-tile, neighbouring M-tiles whose input rows and cache
-// lines overlap) land on one XCD, while the chunks still start in tile
-// order.  A permutation of [0, n); the last n % (8 kXcdChunk) tiles keep
-// their index.
-constexpr int kXcdChunk = 16;
-__device__ __forceinline__ int xcd_tile(int b, int n) {
-  const int full = n / (8 * kXcdChunk) * (8 * kXcdChunk);
+// and each XCD has its own L2.  Workgroup b of a launch of n tiles runs tile
+// xcd_tile(b, n, lg) (a persistent launch does so per round of gridDim.x
+// tiles): runs of 2^lg consecutive tiles land on one XCD, while the runs
+// still start in tile order.  The host picks lg per stage (word 3 of the
+// table header).  A permutation of [0, n); the last n % (8 2^lg) tiles keep
+// their index, and lg = 0 is the plain order.
+__device__ __forceinline__ int xcd_tile(int b, int n, int lg) {
+  const int full = (n >> (3 + lg)) << (3 + lg);
   if (b >= full) return b;
   const int xcd = b & 7, local = b >> 3;
-  return ((local / kXcdChunk) * 8 + xcd) * kXcdChunk + local % kXcdChunk;
+  return ((((local >> lg) << 3) + xcd) << lg) + (local & ((1 << lg) - 1));
 }
 
 template <int KV, bool PERSIST>
@@ -856,15 +854,15 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   const Slots sl{(float *const *)meta};
   const int32_t *tab = meta + kSlotWords;
   if constexpr (!PERSIST) {
-    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x), true, lds);
+    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x, U(tab[3])), true, lds);
     return;
   }
   // round r takes tiles [r G, r G + G), permuted inside the round as above:
   // a workgroup still meets its tiles in increasing order, so the lowest
   // unfinished tile always has its producers done and its workgroup free
-  const int n_tiles = U(tab[1]), n_ops = U(tab[0]), G = gridDim.x, b = blockIdx.x;
+  const int n_tiles = U(tab[1]), n_ops = U(tab[0]), lg = U(tab[3]), G = gridDim.x, b = blockIdx.x;
   for (int base = 0; base + b < n_tiles; base += G) {
-    process_tile<KV>(a, sl, tab, base + xcd_tile(b, min(G, n_tiles - base)), false, lds);
+    process_tile<KV>(a, sl, tab, base + xcd_tile(b, min(G, n_tiles - base), lg), false, lds);
     __syncthreads();   // the next tile reuses LDS
   }
   if (threadIdx.x == 0) {

@@ -136,6 +136,19 @@ def stage_times(I, g, q, ins, outs, stream, reps):
     return [statistics.median(r[k] for r in rows) for k in range(n)], rows
 
 
+def host_cpu():
+    """CPU model and logical CPU count of the host the oracle ran on."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count()}
+
+
 def cpu_oracle(spec, ten, budget_s):
     from oracle import evaluator as E
     E.build()
@@ -713,6 +726,9 @@ def main():
                                        for ids, strat in stages]}), flush=True)
         return
 
+    # the timing protocol's repeats: 5 x 100 back-to-back steps (median, min, stdev)
+    rep_us = [time_steps(I, g, q, ins, outs, stream, 0, 100, torch) for _ in range(5)]
+
     # per-stage roofline on the stage kernel
     work = unit_work(spec, args.batch)
     st_ns, _ = stage_times(I, g, q, ins, outs, stream, max(20, min(args.steps, 100)))
@@ -756,6 +772,8 @@ def main():
         "search": {"seconds": round(search_s, 3), "states": states, "transitions": transitions,
                    "stages_measured": measured, "predicted_ns": pred_ns, "tuned_ns": tuned_ns},
         "throughput_img_per_s": round(args.batch / us * 1e6, 1),
+        "repeats": {"n": 5, "steps": 100, "median_us": round(statistics.median(rep_us), 3),
+                    "min_us": round(min(rep_us), 3), "stdev_us": round(statistics.stdev(rep_us), 3)},
     }
     if not args.no_baselines:
         base = {}
@@ -776,7 +794,8 @@ def main():
         cpu_us, n = cpu_oracle(spec, ten, args.cpu_seconds)
         result["cpu_baseline"] = {"value": round(cpu_us, 1), "unit": "us", "cores": 1, "kind": "oracle",
                                   "sample": f"{n} full evaluations of the {args.config} block at batch "
-                                            f"{args.batch} (fp64 direct loops, single thread)"}
+                                            f"{args.batch} (fp64 direct loops, single thread)",
+                                  "host": host_cpu()}
         print(f"[bench] cpu oracle {cpu_us:.0f} us/eval", file=sys.stderr, flush=True)
     I.ios_schedule_destroy(q)
     g.close()

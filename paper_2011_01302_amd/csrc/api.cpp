@@ -2,6 +2,7 @@
 // Every call catches the library's internal errors and returns a code.
 #include <cstdlib>
 #include <algorithm>
+#include <array>
 #include <cstring>
 #include <new>
 
@@ -244,68 +245,82 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
     need(o.warmup >= 0 && o.reps >= 1 && o.repeats >= 1, "bad profiling counts");
     ensure_device(g);
     const bool forced = std::getenv("IOS_CONV_TILE") != nullptr;
+    // on an error the units get their shapes and orders back
+    std::vector<std::array<int, 3>> saved;
+    for (int32_t u : q->unit_ids) {
+      const int op = unit_op_of_tensor(g, u);
+      saved.push_back({op, g->ops[op].tcfg, g->ops[op].xcd_lg});
+    }
     int64_t total = 0;
-    for (size_t k = 0; k < q->strategies.size(); ++k) {
-      std::vector<int> ops, convs;
-      for (int i = q->offsets[k]; i < q->offsets[k + 1]; ++i) {
-        const int op = unit_op_of_tensor(g, q->unit_ids[i]);
-        ops.push_back(op);
-        if (g->ops[op].d.kind == IOS_CONV) convs.push_back(op);
-      }
-      const int strat = q->strategies[k];
-      auto measure = [&] { return profile_stage(g, ops, strat, o.warmup, o.reps, o.repeats); };
-      for (int op : ops) g->ops[op].xcd_lg = -1;
-      int64_t best = measure();
-      // the XCD run length of the stage's tile order (see the stage kernel):
-      // the modelled choice, or an explicit one measured faster
-      auto tune_xcd_order = [&] {
-        int keep = -1;
-        for (int lg : {0, 2, 4}) {
-          for (int op : ops) g->ops[op].xcd_lg = lg;
-          const int64_t ns = measure();
-          if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
-            best = ns;
-            keep = lg;
-          }
+    try {
+      for (size_t k = 0; k < q->strategies.size(); ++k) {
+        std::vector<int> ops, convs;
+        for (int i = q->offsets[k]; i < q->offsets[k + 1]; ++i) {
+          const int op = unit_op_of_tensor(g, q->unit_ids[i]);
+          ops.push_back(op);
+          if (g->ops[op].d.kind == IOS_CONV) convs.push_back(op);
         }
-        for (int op : ops) g->ops[op].xcd_lg = keep;
-        return keep >= 0;
-      };
-      if (forced || convs.empty()) tune_xcd_order();
-      if (!forced && !convs.empty()) {
-        // each entry: the convs that take one shape together
-        std::vector<std::vector<int>> knobs;
-        if (strat == IOS_MERGE) {
-          int largest = convs[0];
-          for (int c : convs)
-            if (g->ops[c].d.cout > g->ops[largest].d.cout) largest = c;
-          for (int c : convs) g->ops[c].tcfg = g->ops[largest].tcfg;
-          best = measure();
-          knobs.push_back(convs);
-        } else {
-          for (int c : convs) knobs.push_back({c});
-        }
-        for (int pass = 0; pass < 2; ++pass) {
-          bool improved = pass == 0 && tune_xcd_order();
-          for (const auto &kn : knobs) {
-            const int cur = g->ops[kn[0]].tcfg;
-            int keep = cur;
-            for (int t = 0; t < TC_COUNT; ++t) {
-              if (t == cur) continue;
-              for (int c : kn) g->ops[c].tcfg = t;
-              const int64_t ns = measure();
-              if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
-                best = ns;
-                keep = t;
-                improved = true;
-              }
+        const int strat = q->strategies[k];
+        auto measure = [&] { return profile_stage(g, ops, strat, o.warmup, o.reps, o.repeats); };
+        for (int op : ops) g->ops[op].xcd_lg = -1;
+        int64_t best = measure();
+        // the XCD run length of the stage's tile order (see the stage kernel):
+        // the modelled choice, or an explicit one measured faster
+        auto tune_xcd_order = [&] {
+          int keep = -1;
+          for (int lg : {0, 2, 4}) {
+            for (int op : ops) g->ops[op].xcd_lg = lg;
+            const int64_t ns = measure();
+            if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
+              best = ns;
+              keep = lg;
             }
-            for (int c : kn) g->ops[c].tcfg = keep;
           }
-          if (!improved) break;
+          for (int op : ops) g->ops[op].xcd_lg = keep;
+          return keep >= 0;
+        };
+        if (forced || convs.empty()) tune_xcd_order();
+        if (!forced && !convs.empty()) {
+          // each entry: the convs that take one shape together
+          std::vector<std::vector<int>> knobs;
+          if (strat == IOS_MERGE) {
+            int largest = convs[0];
+            for (int c : convs)
+              if (g->ops[c].d.cout > g->ops[largest].d.cout) largest = c;
+            for (int c : convs) g->ops[c].tcfg = g->ops[largest].tcfg;
+            best = measure();
+            knobs.push_back(convs);
+          } else {
+            for (int c : convs) knobs.push_back({c});
+          }
+          for (int pass = 0; pass < 2; ++pass) {
+            bool improved = pass == 0 && tune_xcd_order();
+            for (const auto &kn : knobs) {
+              const int cur = g->ops[kn[0]].tcfg;
+              int keep = cur;
+              for (int t = 0; t < TC_COUNT; ++t) {
+                if (t == cur) continue;
+                for (int c : kn) g->ops[c].tcfg = t;
+                const int64_t ns = measure();
+                if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
+                  best = ns;
+                  keep = t;
+                  improved = true;
+                }
+              }
+              for (int c : kn) g->ops[c].tcfg = keep;
+            }
+            if (!improved) break;
+          }
         }
+        total += best;
       }
-      total += best;
+    } catch (...) {
+      for (const auto &v : saved) {
+        g->ops[v[0]].tcfg = v[1];
+        g->ops[v[0]].xcd_lg = v[2];
+      }
+      throw;
     }
     // stages compiled for q before this call used the old shapes
     for (auto &cs : q->compiled)

@@ -74,23 +74,23 @@ int ios_graph_create(int32_t batch, ios_graph **out) {
 
 void ios_graph_destroy(ios_graph *g) {
   if (!g) return;
-  if (g->device_ready) hipSetDevice(g->device);
+  if (g->device_ready) (void)hipSetDevice(g->device);
   for (auto &b : g->bufs)
-    if (b.dev) hipFree(b.dev);
+    if (b.dev) (void)hipFree(b.dev);
   for (auto &op : g->ops) {
-    if (op.d_wpk) hipFree(op.d_wpk);
-    if (op.d_bias) hipFree(op.d_bias);
-    if (op.d_dw) hipFree(op.d_dw);
+    if (op.d_wpk) (void)hipFree(op.d_wpk);
+    if (op.d_bias) (void)hipFree(op.d_bias);
+    if (op.d_dw) (void)hipFree(op.d_dw);
   }
   CompiledStage &s = g->scratch;
-  if (s.d_table) hipFree(s.d_table);
-  if (s.d_ctr) hipFree(s.d_ctr);
-  if (s.d_mw) hipFree(s.d_mw);
-  if (s.d_mb) hipFree(s.d_mb);
-  if (g->d_err) hipFree(g->d_err);
-  if (g->ev0) hipEventDestroy(g->ev0);
-  if (g->ev1) hipEventDestroy(g->ev1);
-  if (g->stream) hipStreamDestroy(g->stream);
+  if (s.d_table) (void)hipFree(s.d_table);
+  if (s.d_ctr) (void)hipFree(s.d_ctr);
+  if (s.d_mw) (void)hipFree(s.d_mw);
+  if (s.d_mb) (void)hipFree(s.d_mb);
+  if (g->d_err) (void)hipFree(g->d_err);
+  if (g->ev0) (void)hipEventDestroy(g->ev0);
+  if (g->ev1) (void)hipEventDestroy(g->ev1);
+  if (g->stream) (void)hipStreamDestroy(g->stream);
   delete g;
 }
 
@@ -353,10 +353,10 @@ int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transi
 
 void ios_schedule_destroy(ios_schedule_t *q) {
   if (!q) return;
-  if (q->g && q->g->device_ready) hipSetDevice(q->g->device);
+  if (q->g && q->g->device_ready) (void)hipSetDevice(q->g->device);
   for (auto &cs : q->compiled)
     if (cs) free_stage(cs.get());
-  for (auto e : q->events) hipEventDestroy(e);
+  for (auto e : q->events) (void)hipEventDestroy(e);
   delete q;
 }
 

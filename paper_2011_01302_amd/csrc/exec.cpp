@@ -141,7 +141,7 @@ template <class T>
 void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool scratch) {
   size_t n = std::max<size_t>(v.size(), 1);
   if (!scratch || *cap < n) {
-    if (scratch && *dptr) hipFree(*dptr);
+    if (scratch && *dptr) (void)hipFree(*dptr);
     hip_check(hipMalloc(dptr, sizeof(T) * n), "hipMalloc(stage)");
     if (scratch) *cap = n;
   }
@@ -172,10 +172,10 @@ void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::v
 
 void free_stage(CompiledStage *cs) {
   if (!cs->owns) return;
-  if (cs->d_table) hipFree(cs->d_table);
-  if (cs->d_ctr) hipFree(cs->d_ctr);
-  if (cs->d_mw) hipFree(cs->d_mw);
-  if (cs->d_mb) hipFree(cs->d_mb);
+  if (cs->d_table) (void)hipFree(cs->d_table);
+  if (cs->d_ctr) (void)hipFree(cs->d_ctr);
+  if (cs->d_mw) (void)hipFree(cs->d_mw);
+  if (cs->d_mb) (void)hipFree(cs->d_mb);
   cs->d_table = nullptr; cs->d_ctr = nullptr;
   cs->d_mw = nullptr; cs->d_mb = nullptr;
 }

@@ -743,7 +743,7 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
 // `tab` is the stage table in LDS.
 template <int KV>
 __device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl, const int32_t *tab, int t,
-                                             bool remap, float *lds) {
+                                             float *lds) {
   const int tid = threadIdx.x, lane = tid & 63;
   // op_start is non-decreasing with op_start[0] = 0: the tile's op is the
   // last one starting at or before t.  Lane i holds op_start[i] and word
@@ -838,6 +838,7 @@ __device__ __forceinline__ float *stage_prologue(const int4 *__restrict__ table,
 // still start in tile order.  The host picks lg per stage (word 3 of the
 // table header).  A permutation of [0, n); the last n % (8 2^lg) tiles keep
 // their index, and lg = 0 is the plain order.
+static_assert(kXcds == 8, "xcd_tile divides by the XCD count with shifts by 3");
 __device__ __forceinline__ int xcd_tile(int b, int n, int lg) {
   const int full = (n >> (3 + lg)) << (3 + lg);
   if (b >= full) return b;
@@ -854,7 +855,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   const Slots sl{(float *const *)meta};
   const int32_t *tab = meta + kSlotWords;
   if constexpr (!PERSIST) {
-    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x, U(tab[3])), true, lds);
+    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x, U(tab[3])), lds);
     return;
   }
   // round r takes tiles [r G, r G + G), permuted inside the round as above:
@@ -862,7 +863,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   // unfinished tile always has its producers done and its workgroup free
   const int n_tiles = U(tab[1]), n_ops = U(tab[0]), lg = U(tab[3]), G = gridDim.x, b = blockIdx.x;
   for (int base = 0; base + b < n_tiles; base += G) {
-    process_tile<KV>(a, sl, tab, base + xcd_tile(b, min(G, n_tiles - base), lg), false, lds);
+    process_tile<KV>(a, sl, tab, base + xcd_tile(b, min(G, n_tiles - base), lg), lds);
     __syncthreads();   // the next tile reuses LDS
   }
   if (threadIdx.x == 0) {

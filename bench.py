@@ -220,6 +220,39 @@ def write_traffic(args, fetch_dir, write_dir):
     print(json.dumps(out))
 
 
+def write_mfma(args, d):
+    """fp32 MFMA work the hardware counted per stage launch of the timed loop
+    (rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_INSTS_VALU_MFMA_F32: add
+    and mul ops / 512, and MFMA instructions) against the stages' algorithmic
+    MFMA flops (2 x MAC of the convolutions as defined).  The excess is the
+    padding the kernel multiplies by zero: output channels to multiples of 16,
+    input channels to multiples of 4 and the reduction to multiples of 16,
+    pixel rows of the last M-tile, and the zero taps of merged kernels."""
+    import workloads as W
+    meta = json.load(open(os.path.join(d, "bench.json")))
+    ns, steps = meta["stages"], meta["steps"]
+    mops = [v for _, k, v in _pmc_rows(d, "SQ_INSTS_VALU_MFMA_MOPS_F32") if "ios_stage_kernel" in k][-steps * ns:]
+    inst = [v for _, k, v in _pmc_rows(d, "SQ_INSTS_VALU_MFMA_F32") if "ios_stage_kernel" in k][-steps * ns:]
+    spec, _ = W.make(args.config, args.batch, args.seed)
+    work = unit_work(spec, args.batch)
+    rows = []
+    for k in range(ns):
+        units = meta["schedule"][k]["units"]
+        alg = sum(work[n][0] for n in units)
+        counted = statistics.mean(mops[k::ns]) * 512
+        rows.append({"units": units, "strategy": meta["schedule"][k]["strategy"],
+                     "algorithmic_flop": alg, "counted_flop": counted,
+                     "mfma_instructions": statistics.mean(inst[k::ns]),
+                     "counted_over_algorithmic": round(counted / alg, 4) if alg else None})
+    out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": kernel_sha(), "per_stage": rows,
+           "counted_over_algorithmic": round(sum(r["counted_flop"] for r in rows) /
+                                             sum(r["algorithmic_flop"] for r in rows), 4)}
+    path = os.path.join(ROOT, "profiles", f"mfma_{args.config}_bs{args.batch}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def write_occupancy(args, ios_dir, seq_dir):
     """Mean resident waves per CU while the stage kernels run, for the IOS
     schedule and for the sequential one-unit-per-launch schedule of the same
@@ -623,6 +656,9 @@ def main():
     ap.add_argument("--occupancy-from", nargs=2, metavar=("IOS_DIR", "SEQ_DIR"),
                     help="turn two rocprofv3 --pmc MeanOccupancyPerCU GRBM_GUI_ACTIVE runs (IOS "
                          "schedule, --mode sequential) into profiles/occupancy_<workload>.json and exit")
+    ap.add_argument("--mfma-from", default="", metavar="PMC_DIR",
+                    help="turn a rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_INSTS_VALU_MFMA_F32 run "
+                         "into profiles/mfma_<workload>.json and exit")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this benchmark "
                          "into profiles/traffic_<workload>.json and exit")
@@ -640,6 +676,9 @@ def main():
         return
     if args.occupancy_from:
         write_occupancy(args, *args.occupancy_from)
+        return
+    if args.mfma_from:
+        write_mfma(args, args.mfma_from)
         return
 
     lib = os.path.join(ROOT, "paper_2011_01302_amd", "libios.so")

@@ -450,10 +450,10 @@ def run_next(args):
             o.verify_reps = 20                      # the picked stages measured in full
         return o
 
-    isos = {}
-
     def timed(g, q, ins, outs, gflop):
-        iso = isos.setdefault(g.handle, conv_tiles(I, g))
+        if not hasattr(g, "iso_tiles"):             # the isolated choice of this graph
+            g.iso_tiles = conv_tiles(I, g)
+        iso = g.iso_tiles
         tune_for(I, g, q, iso)
         steps = max(20, min(args.steps, int(2e5 / max(1.0, gflop * 1e3))))
         us = time_steps(I, g, q, ins, outs, stream, 10, steps, torch)

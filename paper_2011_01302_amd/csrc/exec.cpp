@@ -407,11 +407,17 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   cs->table[0] = n;
   cs->table[1] = start.back();
   cs->table[2] = devop_off;
-  // XCD run length: the one ios_schedule_tune_tiles set on all of the
-  // stage's units, else the L2-fill model's choice
+  // XCD run length: forced by IOS_XCD_RUNS=<0|2|4> (log2 of the run), else
+  // the one ios_schedule_tune_tiles set on all of the stage's units, else
+  // the L2-fill model's choice
   int lg = g->ops[ops[0]].xcd_lg;
   for (int i : ops)
     if (g->ops[i].xcd_lg != lg) lg = -1;
+  if (const char *e = std::getenv("IOS_XCD_RUNS")) {
+    const int v = std::atoi(e);
+    if (v != 0 && v != 2 && v != 4) fail(IOS_E_ARG, "IOS_XCD_RUNS must be 0, 2 or 4");
+    lg = v;
+  }
   cs->table[3] = lg >= 0 ? lg : choose_xcd_runs(sorted, start, cs->grid);
   for (int i = 0; i <= n; ++i) cs->table[4 + i] = start[i];
   std::memcpy(&cs->table[devop_off], cs->ops.data(), sizeof(DevOp) * n);

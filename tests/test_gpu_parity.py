@@ -265,6 +265,29 @@ def test_conv_tile_shapes_read_and_replayed():
     g.close()
 
 
+@pytest.mark.parametrize("lg", ["0", "2", "4"])
+def test_parity_every_xcd_tile_order(lg, monkeypatch):
+    """Each run length of the XCD tile order (forced for every stage; the
+    per-stage choice picks among these): ragged shapes with chained stages
+    (persistent launches) and the Inception block in one and several
+    stages."""
+    monkeypatch.setenv("IOS_XCD_RUNS", lg)
+    spec = ragged_spec(2)
+    ten = W.make_tensors(spec, 3)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), ref, f"ragged/xcd {lg}")
+        I.ios_schedule_destroy(q)
+    g.close()
+    spec, ten = case("inception")
+    g = I.Graph(spec, ten)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), reference("inception"), f"inception/xcd {lg}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_schedule_tune_tiles_per_stage(monkeypatch):
     """Per-stage conv tile shapes: the call measures every stage, leaves the
     chosen shapes on the graph and the schedule runs with them (results still

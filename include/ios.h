@@ -256,7 +256,8 @@ int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transi
  * on the schedule that will run; q's stages are recompiled on its next run.
  * A unit belongs to one stage of a schedule, so the stages do not compete.
  * With IOS_CONV_TILE set in the environment the shapes stay fixed (the tile
- * order is still chosen).  *cost_ns = sum of the stages' final measured
+ * order is still chosen); IOS_XCD_RUNS=0, 2 or 4 fixes the tile order's run
+ * length (2^value) for every stage compiled while it is set, for tests.  *cost_ns = sum of the stages' final measured
  * latencies.
  * Errors: IOS_E_ARG (null pointer, bad counts, schedule of another graph),
  * IOS_E_STATE (not finalized), IOS_E_HIP. */

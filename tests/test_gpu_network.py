@@ -24,14 +24,14 @@ DEV = "cuda:0"
 
 
 @functools.lru_cache(maxsize=None)
-def case(net):
-    return W.make(net, 1, 0)
+def case(net, batch=1):
+    return W.make(net, batch, 0)
 
 
 @functools.lru_cache(maxsize=None)
-def reference(net):
-    spec, ten = case(net)
-    print(f"[gpu-case] oracle evaluation of {net}", flush=True)
+def reference(net, batch=1):
+    spec, ten = case(net, batch)
+    print(f"[gpu-case] oracle evaluation of {net} at batch {batch}", flush=True)
     return E.outputs(spec, ten)
 
 
@@ -59,13 +59,13 @@ def _print_case(request):
     yield
 
 
-@pytest.mark.parametrize("net", W.NETWORK_NAMES)
-def test_network_parity_baseline_schedules(net):
+@pytest.mark.parametrize("net,batch", [(n, 1) for n in W.NETWORK_NAMES] + [("squeezenet", 3)])
+def test_network_parity_baseline_schedules(net, batch):
     """Sequential (one unit per launch), greedy (every ready unit per launch)
     and one stage per block (branches chained inside the launch, chains of up
     to five convs)."""
-    spec, ten = case(net)
-    ref = reference(net)
+    spec, ten = case(net, batch)
+    ref = reference(net, batch)
     g = I.Graph(spec, ten)
     assert len(g.blocks()) == len(spec["block_names"])
     for mode in (I.IOS_SCHED_SEQUENTIAL, I.IOS_SCHED_GREEDY):

@@ -311,6 +311,15 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       while (rows > 1 && ((rows - 1) * d.sh + d.kh) * d.W > kPoolLdsFloats) --rows;
       if (((rows - 1) * d.sh + d.kh) * d.W > kPoolLdsFloats)
         fail(IOS_E_UNSUPPORTED, "pooling input rows too wide for the LDS tile");
+      // strided pools over few planes (the stems' down-sampling pools): bands
+      // of rows until the pool has kPoolMinTiles tiles, each band at least one
+      // output per thread.  Stride-1 pools keep whole planes: beside convs in
+      // a stage, more and smaller pool tiles measured slower.
+      const int n_planes = d.N * d.Cout;
+      if (d.sh > 1 && n_planes * cdiv(d.Ho, rows) < kPoolMinTiles) {
+        const int bands = cdiv(kPoolMinTiles, n_planes);
+        rows = std::min(rows, std::max(cdiv(d.Ho, bands), cdiv(kThreads, d.Wo)));
+      }
       d.rows_per_tile = rows;
       d.tiles_per_plane = cdiv(d.Ho, rows);
       d.tiles_m = d.N * d.Cout * d.tiles_per_plane;

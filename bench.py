@@ -185,7 +185,7 @@ def _pmc_rows(d, counter):
     return rows
 
 
-def write_traffic(args, fetch_dir, write_dir):
+def write_traffic(args, fetch_dir, write_dir, out_dir=None):
     """HBM bytes per stage launch of the timed loop, from rocprofv3 --pmc
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what the
     same counter reads for the plain copy of --copy-mb MiB at the end of the
@@ -214,13 +214,13 @@ def write_traffic(args, fetch_dir, write_dir):
                              "fetch_bytes": round(f), "write_bytes": round(w)}
                             for st, f, w in zip(sched, res["FETCH_SIZE"]["per_stage_bytes"],
                                                 res["WRITE_SIZE"]["per_stage_bytes"])]
-    path = os.path.join(ROOT, "profiles", f"traffic_{args.config}_bs{args.batch}.json")
+    path = os.path.join(out_dir or os.path.join(ROOT, "profiles"), f"traffic_{args.config}_bs{args.batch}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out))
 
 
-def write_mfma(args, d):
+def write_mfma(args, d, out_dir=None):
     """fp32 MFMA work the hardware counted per stage launch of the timed loop
     (rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_INSTS_VALU_MFMA_F32: add
     and mul ops / 512, and MFMA instructions) against the stages' algorithmic
@@ -247,13 +247,13 @@ def write_mfma(args, d):
     out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": kernel_sha(), "per_stage": rows,
            "counted_over_algorithmic": round(sum(r["counted_flop"] for r in rows) /
                                              sum(r["algorithmic_flop"] for r in rows), 4)}
-    path = os.path.join(ROOT, "profiles", f"mfma_{args.config}_bs{args.batch}.json")
+    path = os.path.join(out_dir or os.path.join(ROOT, "profiles"), f"mfma_{args.config}_bs{args.batch}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out, indent=1))
 
 
-def write_occupancy(args, ios_dir, seq_dir):
+def write_occupancy(args, ios_dir, seq_dir, out_dir=None):
     """Mean resident waves per CU while the stage kernels run, for the IOS
     schedule and for the sequential one-unit-per-launch schedule of the same
     kernels (Sec. 6.3 compares active warps the same way).  From two
@@ -284,7 +284,7 @@ def write_occupancy(args, ios_dir, seq_dir):
         out[name] = {"stages": ns, "mean_waves_per_cu": round(sum(v * act[i] for i, v in timed) / w, 3),
                      "per_stage": stages}
     out["ios_over_sequential"] = round(out["ios"]["mean_waves_per_cu"] / out["sequential"]["mean_waves_per_cu"], 3)
-    path = os.path.join(ROOT, "profiles", f"occupancy_{args.config}_bs{args.batch}.json")
+    path = os.path.join(out_dir or os.path.join(ROOT, "profiles"), f"occupancy_{args.config}_bs{args.batch}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out, indent=1))

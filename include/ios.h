@@ -249,14 +249,15 @@ int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transi
  * (o's warmup / reps / repeats, or the defaults when o is NULL) to pick, for
  * every stage, (1) how its tiles are spread over the 8 XCDs (runs of 1, 4 or
  * 16 consecutive tiles per XCD, else the library's L2-fill model) and (2) the
- * tile shapes of its convs in that stage's company: one conv at a time, each
- * shape tried, a change kept when the stage gets more than 2% faster (two
- * passes); a merge stage's convs take one shape together.  The choices stay
+ * tile shapes of its convs and the 16-channel output blocks per tile of its
+ * SEPCONVs in that stage's company: one operator at a time, each value
+ * tried, a change kept when the stage gets more than 2% faster (two passes);
+ * a merge stage's convs take one shape together.  The choices stay
  * set on the graph's units (ios_get_conv_tile reads the shapes), so call it
  * on the schedule that will run; q's stages are recompiled on its next run.
  * A unit belongs to one stage of a schedule, so the stages do not compete.
- * With IOS_CONV_TILE set in the environment the shapes stay fixed (the tile
- * order is still chosen); IOS_XCD_RUNS=0, 2 or 4 fixes the tile order's run
+ * With IOS_CONV_TILE (IOS_SEP_NBT) set in the environment the conv shapes
+ * (SEPCONV blocks) stay fixed, the rest is still chosen; IOS_XCD_RUNS=0, 2 or 4 fixes the tile order's run
  * length (2^value) for every stage compiled while it is set, for tests.  *cost_ns = sum of the stages' final measured
  * latencies.
  * Errors: IOS_E_ARG (null pointer, bad counts, schedule of another graph),

@@ -223,12 +223,13 @@ int ios_schedule_from_stages(ios_graph *g, int32_t n_stages, const int32_t *stag
   });
 }
 
-// Conv tile shapes and the XCD tile order chosen per stage: each stage of q
-// is measured with its tile order's run length set explicitly (else the
-// stage kernel's L2-fill model picks it) and with its convs' shapes varied
-// one conv at a time (all of them together in a merge stage, whose merged
-// conv takes one shape), keeping a change only when the stage gets faster by
-// more than kStageTileSlack.  A shape measured alone
+// Conv tile shapes, SEPCONV output blocks per tile and the XCD tile order
+// chosen per stage: each stage of q is measured with its tile order's run
+// length set explicitly (else the stage kernel's L2-fill model picks it),
+// with its convs' shapes varied one conv at a time (all of them together in
+// a merge stage, whose merged conv takes one shape) and with each SEPCONV's
+// blocks per tile varied, keeping a change only when the stage gets faster
+// by more than kStageTileSlack.  A shape measured alone
 // fills the GPU by itself; inside a stage other operators share the CUs, so
 // larger tiles can pay off there.
 static constexpr double kStageTileSlack = 0.02;
@@ -245,11 +246,12 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
     need(o.warmup >= 0 && o.reps >= 1 && o.repeats >= 1, "bad profiling counts");
     ensure_device(g);
     const bool forced = std::getenv("IOS_CONV_TILE") != nullptr;
+    const bool sep_forced = std::getenv("IOS_SEP_NBT") != nullptr;
     // on an error the units get their shapes and orders back
-    std::vector<std::array<int, 3>> saved;
+    std::vector<std::array<int, 4>> saved;
     for (int32_t u : q->unit_ids) {
       const int op = unit_op_of_tensor(g, u);
-      saved.push_back({op, g->ops[op].tcfg, g->ops[op].xcd_lg});
+      saved.push_back({op, g->ops[op].tcfg, g->ops[op].xcd_lg, g->ops[op].sep_nbt});
     }
     int64_t total = 0;
     try {
@@ -279,39 +281,51 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
           for (int op : ops) g->ops[op].xcd_lg = keep;
           return keep >= 0;
         };
-        if (forced || convs.empty()) tune_xcd_order();
+        // knobs: the convs that take one tile shape together (all of a merge
+        // stage's), and each SEPCONV's output blocks per tile
+        struct Knob {
+          std::vector<int> ops;
+          bool sep;
+          int lo, hi;
+        };
+        std::vector<Knob> knobs;
         if (!forced && !convs.empty()) {
-          // each entry: the convs that take one shape together
-          std::vector<std::vector<int>> knobs;
           if (strat == IOS_MERGE) {
             int largest = convs[0];
             for (int c : convs)
               if (g->ops[c].d.cout > g->ops[largest].d.cout) largest = c;
             for (int c : convs) g->ops[c].tcfg = g->ops[largest].tcfg;
             best = measure();
-            knobs.push_back(convs);
+            knobs.push_back({convs, false, 0, TC_COUNT - 1});
           } else {
-            for (int c : convs) knobs.push_back({c});
+            for (int c : convs) knobs.push_back({{c}, false, 0, TC_COUNT - 1});
           }
-          for (int pass = 0; pass < 2; ++pass) {
-            bool improved = pass == 0 && tune_xcd_order();
-            for (const auto &kn : knobs) {
-              const int cur = g->ops[kn[0]].tcfg;
-              int keep = cur;
-              for (int t = 0; t < TC_COUNT; ++t) {
-                if (t == cur) continue;
-                for (int c : kn) g->ops[c].tcfg = t;
-                const int64_t ns = measure();
-                if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
-                  best = ns;
-                  keep = t;
-                  improved = true;
-                }
+        }
+        if (!sep_forced)
+          for (int op : ops)
+            if (g->ops[op].d.kind == IOS_SEPCONV) knobs.push_back({{op}, true, 1, max_sep_nbt(g->ops[op])});
+        auto get = [&](const Knob &kn) { return kn.sep ? g->ops[kn.ops[0]].sep_nbt : g->ops[kn.ops[0]].tcfg; };
+        auto set = [&](const Knob &kn, int v) {
+          for (int c : kn.ops) (kn.sep ? g->ops[c].sep_nbt : g->ops[c].tcfg) = v;
+        };
+        for (int pass = 0; pass < 2; ++pass) {
+          bool improved = pass == 0 && tune_xcd_order();
+          for (const auto &kn : knobs) {
+            const int cur = get(kn);
+            int keep = cur;
+            for (int v = kn.lo; v <= kn.hi; ++v) {
+              if (v == cur) continue;
+              set(kn, v);
+              const int64_t ns = measure();
+              if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
+                best = ns;
+                keep = v;
+                improved = true;
               }
-              for (int c : kn) g->ops[c].tcfg = keep;
             }
-            if (!improved) break;
+            set(kn, keep);
           }
+          if (!improved) break;
         }
         total += best;
       }
@@ -319,6 +333,7 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
       for (const auto &v : saved) {
         g->ops[v[0]].tcfg = v[1];
         g->ops[v[0]].xcd_lg = v[2];
+        g->ops[v[0]].sep_nbt = v[3];
       }
       throw;
     }

@@ -354,7 +354,7 @@ static T *upload(const std::vector<T> &v) {
 }
 
 // Largest number of 16-channel output blocks a SEPCONV tile can take (LDS).
-static int max_sep_nbt(const Op &op) {
+int max_sep_nbt(const Op &op) {
   const int K = sep_window(op.d.kh, op.d.kw);
   int n = std::min(kSepMaxNB, op.Npad / 16);
   while (n > 1 && sep_lds_bytes(op.CinP, K, n) > kSepMaxLds) --n;

@@ -312,6 +312,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
 void free_stage(CompiledStage *cs);
 void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
                      hipStream_t stream);
+int max_sep_nbt(const Op &op);
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,
                       int reps, int repeats);
 std::vector<float *> default_buffers(const ios_graph *g);

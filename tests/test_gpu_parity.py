@@ -314,6 +314,22 @@ def test_schedule_tune_tiles_per_stage(monkeypatch):
     g.close()
 
 
+def test_schedule_tune_sepconv_blocks():
+    """Per-stage choice on stages with SEPCONVs (blocks per tile), convs and
+    pools, including a stage whose groups are chains: results still match."""
+    spec = ragged_spec(2)
+    ten = W.make_tensors(spec, 3)
+    ref = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    o = I.ios_sched_opts_default()
+    o.warmup, o.reps, o.repeats = 1, 3, 1
+    for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        assert I.ios_schedule_tune_tiles(g.handle, q, o) > 0
+        check(run(g, q, spec, ten), ref, "ragged/tuned")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_run_timed_and_determinism():
     spec, ten = case("inception")
     g = I.Graph(spec, ten)

@@ -1,16 +1,19 @@
-"""Benchmark: batch-1 latency of an IOS-scheduled multi-branch CNN block on
-one MI355X, with per-stage achieved fp32 TFLOP/s against the MFMA peak.
+"""Benchmark: batch-1 latency of IOS-scheduled multi-branch CNN blocks on one
+MI355X, with achieved fp32 TFLOP/s of the stage kernel against the MFMA peak.
 
-One *step* is one ``ios_run`` of the whole block (every stage of the
+One *step* is one ``ios_run`` of the whole workload (every stage of the
 schedule found by Algorithm 1 with on-device profiling) on inputs already
-resident in HBM.  Default workload: the Inception-V3 mixed block
-(192x35x35 -> 256x35x35), batch 1, seed 0.
+resident in HBM.  Default workload: the SqueezeNet-style stack of eight fire
+modules (96x55x55 -> 512x13x13), batch 1, seed 0 -- the largest of the
+batch-1 configurations (1.14 GFLOP); the other four batch-1 configurations
+are measured the same way and reported beside it.
 
-Printed as one JSON line (rank 0, N = 1 only):
-  value        median-free mean latency of the timed steps, in microseconds
-  roofline     the stage kernel: algorithmic MFMA FLOPs per launch / its mean
-               launch duration (HIP events on the launch stream), vs the
-               fp32 MFMA peak
+Printed as one JSON line (N = 1 only):
+  value        median over 5 equal windows of the K timed steps (HIP events
+               on the launch stream), microseconds per step
+  roofline     the stage kernel: algorithmic MFMA flops per launch / the
+               mean launch duration over the timed region (step time /
+               launches per step), vs the fp32 MFMA peak
   baselines    the same kernels under the sequential (one unit per launch)
                and greedy schedules, timed the same way
   cpu_baseline the oracle (plain fp64 C loops, one thread) on the host
@@ -30,8 +33,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_TFLOPS = 157.3          # MI355X dense fp32 MFMA (256 CU x 2.4 GHz x 256 flop/clk)
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = ["paper_2011_01302_amd/csrc/stage_kernel.hip", "paper_2011_01302_amd/csrc/exec.cpp",
-                  "paper_2011_01302_amd/csrc/ios_internal.h"]
+KERNEL_SOURCES = ["paper_2011_01302_amd/csrc/" + f for f in (
+    "stage_kernel.h", "stage_kernel_full.hip", "stage_kernel_full_persist.hip", "stage_kernel_sep.hip",
+    "stage_kernel_sep_persist.hip", "stage_kernel_light.hip", "stage_kernel_light_persist.hip",
+    "stage_launch.cpp", "exec.cpp", "ios_internal.h")]
 
 
 def kernel_sha() -> str:
@@ -110,20 +115,41 @@ def tune_for(I, g, q, iso):
 
 
 def time_steps(I, g, q, ins, outs, stream, warmup, steps, torch):
+    return statistics.mean(timed_repeats(I, g, q, ins, outs, stream, warmup, steps, torch, 1))
+
+
+def timed_repeats(I, g, q, ins, outs, stream, warmup, steps, torch, repeats=5):
+    """`warmup` untimed runs, then `steps` back-to-back ios_runs split into
+    `repeats` equal windows between HIP events recorded on the launch stream
+    (torch's current stream, which ios_run is given); us per step of each
+    window."""
     ip = [t.data_ptr() for t in ins]
     op = [t.data_ptr() for t in outs]
     for _ in range(warmup):
         I.ios_run(g.handle, q, ip, op, stream)
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    per = steps // repeats
+    assert per * repeats == steps and per > 0, "steps must be a positive multiple of repeats"
     s = torch.cuda.current_stream()
-    e0.record(s)
-    for _ in range(steps):
-        I.ios_run(g.handle, q, ip, op, stream)
-    e1.record(s)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(repeats + 1)]
+    ev[0].record(s)
+    for r in range(repeats):
+        for _ in range(per):
+            I.ios_run(g.handle, q, ip, op, stream)
+        ev[r + 1].record(s)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) * 1e3 / steps          # us per step
+    return [ev[r].elapsed_time(ev[r + 1]) * 1e3 / per for r in range(repeats)]
+
+
+def unit_tiling(I, g):
+    """Every unit's tuning choices, {name: [tile, xcd_lg]} (for replays)."""
+    return {op["name"]: list(I.ios_get_unit_tiling(g.handle, g.tid[op["name"]]))
+            for op in g.spec["ops"] if op["kind"] not in ("concat", "identity")}
+
+
+def set_unit_tiling(I, g, tiling):
+    for name, (tile, lg) in tiling.items():
+        I.ios_set_unit_tiling(g.handle, g.tid[name], tile, lg)
 
 
 def stage_times(I, g, q, ins, outs, stream, reps):
@@ -171,6 +197,18 @@ def load_traffic(workload, sha):
     if d.get("kernel_sha") != sha:
         return None
     return d.get("traffic_bytes_per_launch")
+
+
+def load_trace(workload, sha):
+    """Kernel-trace summary of the same plan (profiles/trace_<workload>.json)
+    when it was taken from the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", f"trace_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("kernel_sha") != sha:
+        return None
+    return {k: d.get(k) for k in ("mean_ns", "mean_period_ns", "median_gap_ns", "frac_from_trace")}
 
 
 def _pmc_rows(d, counter):
@@ -302,13 +340,18 @@ def _pmc_info(d):
     return info
 
 
-def trace_summary(args, trace_dir):
+def trace_summary(args, trace_dir, out_dir=None):
     """Stage-kernel launch durations of the timed loop from a rocprofv3
     --kernel-trace run of this benchmark (run with --no-stage-times, so the
     timed loop is the last steps x stages stage-kernel dispatches; bench.json
-    in the directory holds that run's JSON line)."""
+    in the directory holds that run's JSON line).  Also the mean launch
+    period (first start to last end / launches, which includes the gaps the
+    event-based figure of the benchmark line includes) and the fraction of
+    the fp32 MFMA peak the kernel durations give.  Written to
+    profiles/trace_<workload>.json (or out_dir)."""
     import csv
     import glob
+    import workloads as W
     rows = []
     for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
@@ -324,14 +367,32 @@ def trace_summary(args, trace_dir):
         by_grid.setdefault(wg, []).append(e - b)
     gaps = [timed[i + 1][0] - timed[i][1] for i in range(len(timed) - 1)]
     ns = meta["stages"]
-    per_stage = [{"units": (meta.get("schedule") or [{}] * ns)[k].get("units"),
-                  "workgroups": timed[k][2], "median_ns": statistics.median(dur[k::ns])} for k in range(ns)]
-    out = {"launches": len(timed), "mean_ns": statistics.mean(dur), "median_ns": statistics.median(dur),
+    sched = meta.get("schedule") or [{}] * ns
+    spec, _ = W.make(args.config, args.batch, args.seed)
+    work = unit_work(spec, args.batch)
+    per_stage = []
+    for k in range(ns):
+        units = sched[k].get("units")
+        f_m = sum(work[u][0] for u in units) if units else None
+        med = statistics.median(dur[k::ns])
+        per_stage.append({"units": units, "workgroups": timed[k][2], "median_ns": med,
+                          "tflops": round(f_m / med / 1e3, 3) if f_m is not None else None})
+    mean = statistics.mean(dur)
+    period = (timed[-1][1] - timed[0][0]) / len(timed)
+    mfma_step = sum(w[0] for w in work.values())
+    out = {"workload": f"{args.config}_bs{args.batch}", "kernel_sha": meta.get("kernel_sha"),
+           "launches": len(timed), "mean_ns": mean, "median_ns": statistics.median(dur),
+           "mean_period_ns": round(period, 1),
+           "median_gap_ns": statistics.median(gaps) if gaps else None,
+           "frac_from_trace": round(mfma_step / ns / mean / 1e3 / PEAK_FP32_TFLOPS, 5),
+           "frac_from_period": round(mfma_step / ns / period / 1e3 / PEAK_FP32_TFLOPS, 5),
            "per_stage": per_stage,
            "by_workgroups": {str(k): {"launches": len(v), "median_ns": statistics.median(v)}
                              for k, v in sorted(by_grid.items())},
-           "median_gap_ns": statistics.median(gaps) if gaps else None,
            "step_us_of_that_run": meta["value"]}
+    path = os.path.join(out_dir or os.path.join(ROOT, "profiles"), f"trace_{args.config}_bs{args.batch}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
     print(json.dumps(out, indent=1))
 
 
@@ -615,12 +676,106 @@ def run_network(args):
 
 # ------------------------------------------------------------------ main
 
+BATCH1 = ["tiny", "inception", "randwire", "nasnet", "squeeze"]
+LARGE_SEARCH = ("randwire", "nasnet")      # tens of thousands of candidate stages
+
+
+def search_opts(I, config, r=3, s=8):
+    o = I.ios_sched_opts_default()
+    o.r, o.s = r, s
+    if config in LARGE_SEARCH:
+        o.warmup, o.reps, o.repeats = 1, 3, 1
+        o.verify_reps = 20                      # the picked stages measured in full
+    return o
+
+
+def stage_rows(I, g, spec, batch, stages):
+    """Per stage: its launch period when launched back to back alone (the
+    stage profiler's own measurement, with the schedule's tile choices),
+    algorithmic MFMA / VALU flops, compulsory bytes and their roofline."""
+    work = unit_work(spec, batch)
+    rows = []
+    for ids, strat in stages:
+        names = g.names(ids)
+        ns = I.ios_profile_stage(g.handle, ids, strat, 3, 20, 3)
+        f_m = sum(work[n][0] for n in names)
+        f_v = sum(work[n][1] for n in names)
+        by = stage_bytes(spec, batch, set(names)) + sum(work[n][2] for n in names)
+        t_roof = max(f_m / (PEAK_FP32_TFLOPS * 1e12), f_v / (PEAK_FP32_TFLOPS * 1e12),
+                     by / (PEAK_HBM_GBS * 1e9)) * 1e9
+        rows.append({"units": names, "strategy": "merge" if strat else "concurrent", "ns": ns,
+                     "mfma_flop": f_m, "valu_flop": f_v, "bytes": by,
+                     "tflops": round(f_m / ns / 1e3, 3) if ns else None,
+                     "frac_of_roofline": round(t_roof / ns, 5) if ns else None})
+    return rows
+
+
+def measure_config(I, W, torch, config, batch, seed, steps, warmup, args, plan=None, baselines=True):
+    """Search (or replay `plan`), tune, time; the same for the baselines."""
+    spec, g, ins, outs = _setup(I, W, torch, config, batch, seed)
+    stream = torch.cuda.current_stream().cuda_stream
+    work = unit_work(spec, batch)
+    mfma = sum(w[0] for w in work.values())
+    iso = conv_tiles(I, g)
+    res = {"config": config, "batch": batch, "gflop": round(sum(w[0] + w[1] for w in work.values()) / 1e9, 4)}
+    tuned_ns = None
+    if plan:
+        set_unit_tiling(I, g, plan["tiling"])
+        q = I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in st["units"]] for st in plan["schedule"]],
+                                       [I.IOS_MERGE if st["strategy"] == "merge" else I.IOS_CONCURRENT
+                                        for st in plan["schedule"]])
+        search_s, pred_ns, stats = 0.0, plan["search"]["predicted_ns"], (0, 0, 0)
+    else:
+        o = search_opts(I, config, args.r, args.s)
+        t0 = time.perf_counter()
+        q, pred_ns = I.ios_schedule(g.handle, o)
+        search_s = time.perf_counter() - t0
+        stats = I.ios_schedule_stats(q)
+        tuned_ns = I.ios_schedule_tune_tiles(g.handle, q)
+    stages = I.ios_schedule_get(q)
+    res["schedule"] = [{"units": g.names(ids), "strategy": "merge" if t else "concurrent"} for ids, t in stages]
+    res["tiling"] = unit_tiling(I, g)
+    res["search"] = {"seconds": round(search_s, 3), "states": stats[0], "transitions": stats[1],
+                     "stages_measured": stats[2], "predicted_ns": pred_ns, "tuned_ns": tuned_ns}
+    rep = timed_repeats(I, g, q, ins, outs, stream, warmup, steps, torch)
+    assert I.ios_device_status(g.handle, stream) == 0
+    us = statistics.median(rep)
+    res["us"] = round(us, 3)
+    res["launches"] = len(stages)
+    res["repeats"] = {"n": len(rep), "steps_each": steps // len(rep), "median_us": round(us, 3),
+                      "min_us": round(min(rep), 3), "max_us": round(max(rep), 3)}
+    res["mfma_flop_per_step"] = mfma
+    res["tflops"] = round(mfma / us / 1e6, 3)
+    res["frac_of_fp32_mfma_peak"] = round(mfma / us / 1e6 / PEAK_FP32_TFLOPS, 5)
+    print(f"[bench] {config} bs{batch}: IOS {us:.2f} us/step, {len(stages)} stages, search {search_s:.1f} s",
+          file=sys.stderr, flush=True)
+    if not args.no_stage_times:
+        res["stages"] = stage_rows(I, g, spec, batch, stages)
+    if baselines:
+        base = {}
+        for name, mode in (("sequential", I.IOS_SCHED_SEQUENTIAL), ("greedy", I.IOS_SCHED_GREEDY)):
+            o = I.ios_sched_opts_default()
+            o.mode = mode
+            for u, t in iso.items():
+                I.ios_set_conv_tile(g.handle, u, t)
+            qb, _ = I.ios_schedule(g.handle, o)
+            tune_for(I, g, qb, iso)
+            ub = statistics.median(timed_repeats(I, g, qb, ins, outs, stream, warmup, steps, torch))
+            base[name] = {"us": round(ub, 3), "launches": len(I.ios_schedule_get(qb)),
+                          "speedup_of_ios": round(ub / us, 3)}
+            I.ios_schedule_destroy(qb)
+            print(f"[bench] {config} bs{batch}: {name} {ub:.2f} us/step", file=sys.stderr, flush=True)
+        res["gpu_baselines"] = base
+    return spec, g, q, ins, outs, res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=500,
+                    help="timed steps of the headline, split into 5 equal windows (median reported)")
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="inception")
+    ap.add_argument("--config", default="squeeze")
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--r", type=int, default=3)
@@ -628,10 +783,13 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-baselines", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the other batch-1 configurations")
     ap.add_argument("--report", default="", help="also write the full report (JSON) here")
     ap.add_argument("--dump-costs", default="", help="write the search's stage-latency table here")
     ap.add_argument("--no-stage-times", action="store_true",
-                    help="skip the per-stage event pass (the timed loop is then the last launches)")
+                    help="profiler runs: time the headline only and print a short line (the timed "
+                         "loop is then the last launches of the run)")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="finish with one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--suite", default="",
@@ -646,10 +804,12 @@ def main():
     ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
                     help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
                          "benchmark and exit")
-    ap.add_argument("--plan-from", default="", metavar="BENCH_JSON",
-                    help="replay the schedule and conv tile shapes of an earlier run (the last JSON "
-                         "line of this file) instead of searching: for profiler runs, whose added "
-                         "per-launch cost would change the search's choices")
+    ap.add_argument("--plan-from", default="", metavar="PLAN_JSON",
+                    help="replay the schedule and tuning choices recorded in this file (the last "
+                         "JSON line holding a plan) instead of searching: for profiler runs, whose "
+                         "added per-launch cost would change the search's choices")
+    ap.add_argument("--save-plan", default="", metavar="PLAN_JSON",
+                    help="write the headline's schedule and tuning choices here (for --plan-from)")
     ap.add_argument("--mode", choices=("dp", "sequential", "greedy"), default="dp",
                     help="schedule of the timed step: the DP search (default) or a baseline "
                          "(with --plan-from: that run's tile shapes, this mode's schedule)")
@@ -694,150 +854,110 @@ def main():
     if args.network:
         run_network(args)
         return
-    import numpy as np
     import torch
 
     import paper_2011_01302_amd as I
     import workloads as W
 
     print(f"[bench] config={args.config} batch={args.batch} seed={args.seed}", file=sys.stderr, flush=True)
-    spec, ten = W.make(args.config, args.batch, args.seed)
-    dev = "cuda:0"
-    g = I.Graph(spec, ten)
-    ins = [torch.from_numpy(np.ascontiguousarray(ten[t["name"]])).to(dev) for t in spec["inputs"]]
-    shp = W.infer_shapes(spec)
-    outs = [torch.empty((args.batch,) + shp[o], device=dev) for o in spec["outputs"]]
-    stream = torch.cuda.current_stream().cuda_stream
-
-    conv_units = [op["name"] for op in spec["ops"] if op["kind"] == "conv"]
-    iso = conv_tiles(I, g)
-    tuned_ns = None
+    plan = None
     if args.plan_from:
-        plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{")][-1]
-        for name, shape in plan["tiles"].items():
-            I.ios_set_conv_tile(g.handle, g.tid[name], shape)
-    if args.mode != "dp":
-        # a baseline schedule of the same kernels
-        o = I.ios_sched_opts_default()
-        o.mode = I.IOS_SCHED_SEQUENTIAL if args.mode == "sequential" else I.IOS_SCHED_GREEDY
-        t0 = time.perf_counter()
-        q, pred_ns = I.ios_schedule(g.handle, o)
-        search_s = time.perf_counter() - t0
-        states, transitions, measured = I.ios_schedule_stats(q)
-    elif args.plan_from:
-        # the earlier run's conv tile shapes and stages, no search
-        q = I.ios_schedule_from_stages(g.handle, [[g.tid[n] for n in st["units"]] for st in plan["schedule"]],
-                                       [I.IOS_MERGE if st["strategy"] == "merge" else I.IOS_CONCURRENT
-                                        for st in plan["schedule"]])
-        search_s, pred_ns = 0.0, plan["search"]["predicted_ns"]
-        states, transitions, measured = 0, 0, 0
-    else:
-        # Algorithm 1 with on-device stage profiling
-        opts = I.ios_sched_opts_default()
-        opts.r, opts.s = args.r, args.s
-        t0 = time.perf_counter()
-        q, pred_ns = I.ios_schedule(g.handle, opts)
-        search_s = time.perf_counter() - t0
-        states, transitions, measured = I.ios_schedule_stats(q)
-        # conv tile shapes per stage, in the stage's company
-        tuned_ns = I.ios_schedule_tune_tiles(g.handle, q)
-    tiles = {n: I.ios_get_conv_tile(g.handle, g.tid[n]) for n in conv_units}
-    if args.dump_costs:
+        plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{") and '"tiling"' in l][-1]
+        if args.mode != "dp":
+            # a baseline schedule of the same kernels, with the plan's tile choices
+            spec, g, ins, outs = _setup(I, W, torch, args.config, args.batch, args.seed)
+            set_unit_tiling(I, g, plan["tiling"])
+            o = I.ios_sched_opts_default()
+            o.mode = I.IOS_SCHED_SEQUENTIAL if args.mode == "sequential" else I.IOS_SCHED_GREEDY
+            q, _ = I.ios_schedule(g.handle, o, cost=lambda b, m, ids, t: 1000)
+            stream = torch.cuda.current_stream().cuda_stream
+            us = statistics.median(timed_repeats(I, g, q, ins, outs, stream, args.warmup, args.steps, torch))
+            stages = I.ios_schedule_get(q)
+            print(json.dumps({"value": round(us, 3), "unit": "us", "stages": len(stages), "steps": args.steps,
+                              "mode": args.mode,
+                              "schedule": [{"units": g.names(ids), "strategy": "merge" if t else "concurrent"}
+                                           for ids, t in stages]}), flush=True)
+            return
+    spec, g, q, ins, outs, head = measure_config(
+        I, W, torch, args.config, args.batch, args.seed, args.steps, args.warmup, args, plan=plan,
+        baselines=not (args.no_baselines or args.no_stage_times))
+    if args.dump_costs and not plan:
         I.ios_schedule_dump_costs(g.handle, args.dump_costs)
-    stages = I.ios_schedule_get(q)
-    print(f"[bench] search {search_s:.2f}s, {len(stages)} stages, predicted {pred_ns} ns, "
-          f"tuned {tuned_ns} ns",
-          file=sys.stderr, flush=True)
-
-    us = time_steps(I, g, q, ins, outs, stream, args.warmup, args.steps, torch)
-    assert I.ios_device_status(g.handle, stream) == 0
-    print(f"[bench] IOS {us:.2f} us/step", file=sys.stderr, flush=True)
+    if args.save_plan:
+        with open(args.save_plan, "w") as f:
+            f.write(json.dumps({k: head[k] for k in ("config", "batch", "schedule", "tiling", "search")}) + "\n")
+    us = head["us"]
+    n_launch = head["launches"]
 
     if args.no_stage_times:
         if args.copy_mb:
-            src = torch.ones(args.copy_mb << 18, device=dev)
+            src = torch.ones(args.copy_mb << 18, device="cuda:0")
             dst = torch.empty_like(src)
             dst.copy_(src)
             torch.cuda.synchronize()
-        print(json.dumps({"value": round(us, 3), "unit": "us", "stages": len(stages),
-                          "steps": args.steps, "copy_mb": args.copy_mb, "mode": args.mode,
-                          "schedule": [{"units": g.names(ids), "strategy": "merge" if strat else "concurrent"}
-                                       for ids, strat in stages]}), flush=True)
+        print(json.dumps({"value": us, "unit": "us", "stages": n_launch, "steps": args.steps,
+                          "copy_mb": args.copy_mb, "mode": args.mode, "schedule": head["schedule"],
+                          "kernel_sha": kernel_sha()}), flush=True)
         return
 
-    # the timing protocol's repeats: 5 x 100 back-to-back steps (median, min, stdev)
-    rep_us = [time_steps(I, g, q, ins, outs, stream, 0, 100, torch) for _ in range(5)]
-
-    # per-stage roofline on the stage kernel
-    work = unit_work(spec, args.batch)
-    st_ns, _ = stage_times(I, g, q, ins, outs, stream, max(20, min(args.steps, 100)))
-    stage_rows = []
-    tot_mfma = tot_valu = tot_bytes = 0
-    for (ids, strat), ns in zip(stages, st_ns):
-        names = g.names(ids)
-        f_m = sum(work[n][0] for n in names)
-        f_v = sum(work[n][1] for n in names)
-        by = stage_bytes(spec, args.batch, set(names)) + sum(work[n][2] for n in names)
-        tot_mfma += f_m
-        tot_valu += f_v
-        tot_bytes += by
-        t_roof = max(f_m / (PEAK_FP32_TFLOPS * 1e12), f_v / (PEAK_FP32_TFLOPS * 1e12),
-                     by / (PEAK_HBM_GBS * 1e9)) * 1e9
-        stage_rows.append({"units": names, "strategy": "merge" if strat else "concurrent",
-                           "ns": ns, "mfma_flop": f_m, "valu_flop": f_v, "bytes": by,
-                           "tflops": f_m / ns / 1e3 if ns else None,
-                           "frac_of_roofline": t_roof / ns if ns else None})
-    kern_ns = sum(st_ns)
-    n_launch = len(stages)
-    achieved = (tot_mfma / n_launch) / (kern_ns / n_launch) / 1e3     # TFLOP/s
+    workload = f"{args.config}_bs{args.batch}"
     sha = kernel_sha()
-    traffic = load_traffic(f"{args.config}_bs{args.batch}", sha)
-
+    mfma = head["mfma_flop_per_step"]
+    roof = {"bound": "mfma", "achieved": head["tflops"], "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+            "frac": head["frac_of_fp32_mfma_peak"], "traffic": load_traffic(workload, sha),
+            "kernel": "ios_stage_kernel", "launches_per_step": n_launch,
+            "mean_launch_ns": round(us * 1e3 / n_launch, 1),
+            "mfma_flop_per_launch": mfma / n_launch, "kernel_sha": sha,
+            "duration_basis": "HIP events over the timed region on the launch stream: step time / launches "
+                              "per step (inter-kernel dispatch gaps included)"}
+    tr = load_trace(workload, sha)
+    if tr:
+        roof["trace"] = tr
     result = {
         "metric": "batch-1 network latency (us) + achieved fp32 TFLOP/s per stage vs MFMA peak",
-        "value": round(us, 3), "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "value": us, "unit": "us", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(us / 1e3, 6), "higher_is_better": False,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{args.config} block (seeded synthetic, random-init weights)",
+        "config": {"workload": f"{args.config} (seeded synthetic inputs, random-init weights; "
+                               f"{head['gflop']} GFLOP per image)",
                    "batch": args.batch, "seed": args.seed, "pruning": {"r": args.r, "s": args.s},
                    "parallelism": "single GPU, inter-operator (IOS stages)"},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 4), "peak": PEAK_FP32_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 5),
-                     "traffic": traffic, "kernel": "ios_stage_kernel",
-                     "mean_launch_ns": round(kern_ns / n_launch, 1),
-                     "mfma_flop_per_launch": tot_mfma / n_launch, "kernel_sha": sha},
-        "schedule": stage_rows,
-        "tiles": tiles,
-        "search": {"seconds": round(search_s, 3), "states": states, "transitions": transitions,
-                   "stages_measured": measured, "predicted_ns": pred_ns, "tuned_ns": tuned_ns},
+        "roofline": roof,
+        "schedule": head.get("stages", head["schedule"]),
+        "tiling": head["tiling"],
+        "search": head["search"],
+        "repeats": head["repeats"],
         "throughput_img_per_s": round(args.batch / us * 1e6, 1),
-        "repeats": {"n": 5, "steps": 100, "median_us": round(statistics.median(rep_us), 3),
-                    "min_us": round(min(rep_us), 3), "stdev_us": round(statistics.stdev(rep_us), 3)},
     }
-    if not args.no_baselines:
-        base = {}
-        for name, mode in (("sequential", I.IOS_SCHED_SEQUENTIAL), ("greedy", I.IOS_SCHED_GREEDY)):
-            o = I.ios_sched_opts_default()
-            o.mode = mode
-            for u, t in iso.items():
-                I.ios_set_conv_tile(g.handle, u, t)
-            qb, _ = I.ios_schedule(g.handle, o)
-            tune_for(I, g, qb, iso)
-            ub = time_steps(I, g, qb, ins, outs, stream, args.warmup, args.steps, torch)
-            base[name] = {"us": round(ub, 3), "launches": len(I.ios_schedule_get(qb)),
-                          "speedup_of_ios": round(ub / us, 3)}
-            I.ios_schedule_destroy(qb)
-            print(f"[bench] {name} {ub:.2f} us/step", file=sys.stderr, flush=True)
-        result["gpu_baselines"] = base
+    if "gpu_baselines" in head:
+        result["gpu_baselines"] = head["gpu_baselines"]
+    I.ios_schedule_destroy(q)
+    g.close()
+    del ins, outs
+    torch.cuda.empty_cache()
+    if not args.headline_only and args.batch == 1:
+        others = {}
+        for config in BATCH1:
+            if config == args.config:
+                continue
+            steps = 100 if config in LARGE_SEARCH else 500
+            _, g2, q2, i2, o2, r2 = measure_config(I, W, torch, config, 1, args.seed, steps, args.warmup, args,
+                                                   baselines=not args.no_baselines)
+            keep = ("us", "launches", "gflop", "tflops", "frac_of_fp32_mfma_peak", "repeats", "gpu_baselines",
+                    "schedule", "search")
+            others[config] = {k: r2[k] for k in keep if k in r2}
+            I.ios_schedule_destroy(q2)
+            g2.close()
+            del i2, o2
+            torch.cuda.empty_cache()
+        result["other_batch1_configs"] = others
     if not args.no_cpu:
-        cpu_us, n = cpu_oracle(spec, ten, args.cpu_seconds)
+        cpu_us, n = cpu_oracle(spec, W.make(args.config, args.batch, args.seed)[1], args.cpu_seconds)
         result["cpu_baseline"] = {"value": round(cpu_us, 1), "unit": "us", "cores": 1, "kind": "oracle",
-                                  "sample": f"{n} full evaluations of the {args.config} block at batch "
+                                  "sample": f"{n} full evaluations of the {args.config} workload at batch "
                                             f"{args.batch} (fp64 direct loops, single thread)",
                                   "host": host_cpu()}
         print(f"[bench] cpu oracle {cpu_us:.0f} us/eval", file=sys.stderr, flush=True)
-    I.ios_schedule_destroy(q)
-    g.close()
     line = json.dumps(result)
     if args.report:
         with open(args.report, "w") as f:

@@ -90,8 +90,11 @@ int ios_graph_create(int32_t batch, ios_graph **out);
  * be destroyed first.  NULL is ignored. */
 void ios_graph_destroy(ios_graph *g);
 
-/* Declare a graph input of shape [batch][c][h][w] (float32 NCHW).  Inputs
- * are numbered 0, 1, ... in call order; ios_run takes them in that order.
+/* Declare a graph input of shape [batch][c][h][w] (float32 NCHW): a tensor
+ * of the computation graph G = (V, E) that no operator of G produces
+ * (Sec. 3, "Computation Graph": edges carry tensors between operators; the
+ * block's input feeds its first operators).  Inputs are numbered 0, 1, ...
+ * in call order; ios_run takes them in that order.
  * *tensor_id receives the input's tensor id.
  * Errors: IOS_E_ARG (non-positive size, NULL), IOS_E_STATE (after finalize). */
 int ios_add_input(ios_graph *g, int32_t c, int32_t h, int32_t w, int32_t *tensor_id);
@@ -174,6 +177,21 @@ int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t 
 enum { IOS_CONV_TILE_SHAPES = 6 };
 int ios_get_conv_tile(ios_graph *g, int32_t unit_id, int32_t *shape);
 int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
+
+/* Every tuning choice of one unit, so that a tuned schedule can be replayed
+ * exactly: `tile` is a CONV's tile shape (as above) or a SEPCONV's
+ * 16-channel output blocks per tile (1 .. its maximum), 0 for the other
+ * kinds; `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
+ * unit sends to one XCD (0, 2 or 4), or -1 to let the library's L2-fill
+ * model choose (ios_schedule_tune_tiles sets both per stage).  A stage whose
+ * units disagree on xcd_lg uses the model.  These are implementation
+ * choices of this library's stage kernel, not part of the paper's method;
+ * like ios_set_conv_tile they apply to stages compiled afterwards, and both
+ * calls set up the device first if no earlier call has.
+ * Errors: IOS_E_ARG (bad unit, value out of range, null pointer),
+ * IOS_E_STATE, IOS_E_HIP. */
+int ios_get_unit_tiling(ios_graph *g, int32_t unit_id, int32_t *tile, int32_t *xcd_lg);
+int ios_set_unit_tiling(ios_graph *g, int32_t unit_id, int32_t tile, int32_t xcd_lg);
 
 /* Cost provider for the dynamic program: latency of stage `stage_mask`
  * (block-local bits, see ios_block_units; unit_ids lists the same units,
@@ -269,12 +287,18 @@ void ios_schedule_destroy(ios_schedule_t *q);
 
 /* Write the stage-latency table of the graph's last ios_schedule call as JSON
  * lines {"block", "mask", "units", "concurrent_ns", "merge_ns" (null if not
- * measured)} to `path`, so that the search can be replayed.
+ * measured)} to `path`, so that the search can be replayed.  These are the
+ * latencies GenerateStage measures for each candidate stage S' under both
+ * strategies (Sec. 4.1, Algorithm 1), the only input of the recurrence
+ * besides the graph.
  * Errors: IOS_E_ARG, IOS_E_STATE (no table). */
 int ios_schedule_dump_costs(const ios_graph *g, const char *path);
 
-/* Execute graph g under schedule q: for each stage in order, one kernel
- * launch on `hip_stream` (a hipStream_t; NULL = the default stream).
+/* Execute graph g under schedule q: the stages run one after another, in
+ * schedule order, each with its own parallelization strategy (Sec. 3,
+ * "Schedule": Q = [(S_1, T_1), ..., (S_k, T_k)], stage i+1 starts after
+ * stage i ends), as one kernel launch per stage on `hip_stream` (a
+ * hipStream_t; NULL = the default stream).
  * d_inputs[i] points to input i, d_outputs[k] to output k, each a device
  * buffer of the declared shape owned by the caller.  Asynchronous: returns
  * after the launches are queued, without synchronising.  Runs of one schedule

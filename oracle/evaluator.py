@@ -110,39 +110,43 @@ def sepconv(inputs: Sequence[np.ndarray], dw, pw, bias, pad, pre_relu=True):
     return conv2d(t, pw, bias)
 
 
+def eval_op(op: dict, env: Dict[str, np.ndarray], tensors: Dict[str, np.ndarray]) -> np.ndarray:
+    """The output of one operator whose inputs are in ``env`` (float64)."""
+    k = op["kind"]
+    ins = [env[i] for i in op["in"]]
+    nm = op["name"]
+    if k == "conv":
+        return conv2d(ins[0], tensors[nm + ".w"], tensors.get(nm + ".b"),
+                      (op["sh"], op["sw"]), (op["ph"], op["pw"]),
+                      op.get("pre_relu", 0), op.get("post_relu", 0))
+    if k == "sepconv":
+        return sepconv(ins, tensors[nm + ".dw"], tensors[nm + ".pw"],
+                       tensors.get(nm + ".b"), (op["ph"], op["pw"]), op.get("pre_relu", 1))
+    if k in ("maxpool", "avgpool"):
+        assert op["kh"] == op["kw"] and op["sh"] == op["sw"] and op["ph"] == op["pw"]
+        return pool(ins[0], op["kh"], op["sh"], op["ph"], k == "maxpool")
+    if k == "add":
+        s = ins[0].copy()
+        for t in ins[1:]:
+            s = s + t
+        return s
+    if k == "mean":
+        s = ins[0].copy()
+        for t in ins[1:]:
+            s = s + t
+        return s / float(len(ins))
+    if k == "concat":
+        return np.concatenate(ins, axis=1)
+    if k == "identity":
+        return ins[0]
+    raise ValueError(k)
+
+
 def evaluate(spec: dict, tensors: Dict[str, np.ndarray]) -> Dict[str, np.ndarray]:
     """Every named tensor of the block, as float64 arrays."""
     env = {t["name"]: _f64(tensors[t["name"]]) for t in spec["inputs"]}
     for op in spec["ops"]:
-        k = op["kind"]
-        ins = [env[i] for i in op["in"]]
-        nm = op["name"]
-        if k == "conv":
-            env[nm] = conv2d(ins[0], tensors[nm + ".w"], tensors.get(nm + ".b"),
-                             (op["sh"], op["sw"]), (op["ph"], op["pw"]),
-                             op.get("pre_relu", 0), op.get("post_relu", 0))
-        elif k == "sepconv":
-            env[nm] = sepconv(ins, tensors[nm + ".dw"], tensors[nm + ".pw"],
-                              tensors.get(nm + ".b"), (op["ph"], op["pw"]), op.get("pre_relu", 1))
-        elif k in ("maxpool", "avgpool"):
-            assert op["kh"] == op["kw"] and op["sh"] == op["sw"] and op["ph"] == op["pw"]
-            env[nm] = pool(ins[0], op["kh"], op["sh"], op["ph"], k == "maxpool")
-        elif k == "add":
-            s = ins[0].copy()
-            for t in ins[1:]:
-                s = s + t
-            env[nm] = s
-        elif k == "mean":
-            s = ins[0].copy()
-            for t in ins[1:]:
-                s = s + t
-            env[nm] = s / float(len(ins))
-        elif k == "concat":
-            env[nm] = np.concatenate(ins, axis=1)
-        elif k == "identity":
-            env[nm] = ins[0]
-        else:
-            raise ValueError(k)
+        env[op["name"]] = eval_op(op, env, tensors)
     return env
 
 

@@ -48,6 +48,7 @@ INT64_MAX = (1 << 63) - 1
 EXPORTED = ["ios_graph_create", "ios_graph_destroy", "ios_add_input", "ios_add_op",
             "ios_mark_output", "ios_graph_finalize", "ios_graph_blocks", "ios_block_units",
             "ios_stage_mergeable", "ios_profile_stage", "ios_get_conv_tile", "ios_set_conv_tile",
+            "ios_get_unit_tiling", "ios_set_unit_tiling",
             "ios_sched_opts_default", "ios_schedule",
             "ios_schedule_from_stages", "ios_schedule_get", "ios_schedule_stats",
             "ios_schedule_tune_tiles", "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_timed",
@@ -94,6 +95,8 @@ _sig = {
     "ios_profile_stage": (ctypes.c_int, [_P, _pi32, _i32, _i32, _i32, _i32, _i32, _pi64]),
     "ios_get_conv_tile": (ctypes.c_int, [_P, _i32, _pi32]),
     "ios_set_conv_tile": (ctypes.c_int, [_P, _i32, _i32]),
+    "ios_get_unit_tiling": (ctypes.c_int, [_P, _i32, _pi32, _pi32]),
+    "ios_set_unit_tiling": (ctypes.c_int, [_P, _i32, _i32, _i32]),
     "ios_sched_opts_default": (None, [ctypes.POINTER(ios_sched_opts)]),
     "ios_schedule": (ctypes.c_int, [_P, ctypes.POINTER(ios_sched_opts), COST_FN, _P,
                                     ctypes.POINTER(_P), _pi64]),
@@ -209,6 +212,16 @@ def ios_get_conv_tile(g: int, unit_id: int) -> int:
 
 def ios_set_conv_tile(g: int, unit_id: int, shape: int) -> None:
     _check(_lib.ios_set_conv_tile(g, unit_id, shape))
+
+
+def ios_get_unit_tiling(g: int, unit_id: int) -> Tuple[int, int]:
+    t, x = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.ios_get_unit_tiling(g, unit_id, ctypes.byref(t), ctypes.byref(x)))
+    return t.value, x.value
+
+
+def ios_set_unit_tiling(g: int, unit_id: int, tile: int, xcd_lg: int) -> None:
+    _check(_lib.ios_set_unit_tiling(g, unit_id, tile, xcd_lg))
 
 
 def ios_sched_opts_default() -> ios_sched_opts:

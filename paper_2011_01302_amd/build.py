@@ -25,7 +25,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result"]
 # first three argument words (table pointer and size) preloaded into SGPRs
 DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
           "-packed-fp32-ops", "-munsafe-fp-atomics", "-mllvm", "-amdgpu-kernarg-preload-count=3"]
-SOURCES = ["graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_kernel.hip"]
+# the stage kernel variants build as separate translation units, in parallel
+SOURCES = ["stage_kernel_full.hip", "stage_kernel_full_persist.hip", "stage_kernel_sep.hip",
+           "stage_kernel_sep_persist.hip", "stage_kernel_light.hip", "stage_kernel_light_persist.hip",
+           "graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_launch.cpp"]
 
 
 def _compile(src: str) -> str:

@@ -185,6 +185,36 @@ int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape) {
   });
 }
 
+int ios_get_unit_tiling(ios_graph *g, int32_t unit_id, int32_t *tile, int32_t *xcd_lg) {
+  return guarded([&] {
+    need_final(g);
+    need(tile != nullptr && xcd_lg != nullptr, "null argument");
+    const Op &op = g->ops[unit_op_of_tensor(g, unit_id)];
+    ensure_device(g);
+    *tile = op.d.kind == IOS_CONV ? op.tcfg : op.d.kind == IOS_SEPCONV ? op.sep_nbt : 0;
+    *xcd_lg = op.xcd_lg;
+  });
+}
+
+int ios_set_unit_tiling(ios_graph *g, int32_t unit_id, int32_t tile, int32_t xcd_lg) {
+  return guarded([&] {
+    need_final(g);
+    Op &op = g->ops[unit_op_of_tensor(g, unit_id)];
+    need(xcd_lg == -1 || xcd_lg == 0 || xcd_lg == 2 || xcd_lg == 4, "xcd_lg must be -1, 0, 2 or 4");
+    ensure_device(g);
+    if (op.d.kind == IOS_CONV) {
+      need(tile >= 0 && tile < TC_COUNT, "conv tile shape out of range");
+      op.tcfg = tile;
+    } else if (op.d.kind == IOS_SEPCONV) {
+      need(tile >= 1 && tile <= max_sep_nbt(op), "SEPCONV tile choice out of range");
+      op.sep_nbt = tile;
+    } else {
+      need(tile == 0, "this unit kind has no tile choice (tile must be 0)");
+    }
+    op.xcd_lg = xcd_lg;
+  });
+}
+
 void ios_sched_opts_default(ios_sched_opts *o) {
   if (!o) return;
   o->mode = IOS_SCHED_DP;

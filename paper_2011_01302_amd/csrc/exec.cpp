@@ -466,6 +466,15 @@ int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, i
     hip_check(hipEventElapsedTime(&ms, g->ev0, g->ev1), "hipEventElapsedTime");
     per.push_back((double)ms * 1e6 / reps);
   }
+  // a bounded intra-stage wait that gave up during the measurement makes the
+  // latency meaningless: fail here (and clear the flag) rather than let a
+  // later ios_device_status report it against ios_run
+  int32_t err = 0;
+  hip_check(hipMemcpy(&err, g->d_err, sizeof(err), hipMemcpyDeviceToHost), "hipMemcpy(err)");
+  if (err) {
+    hip_check(hipMemset(g->d_err, 0, sizeof(int32_t)), "hipMemset(err)");
+    fail(IOS_E_DEVICE, "a stage kernel reported an error while the stage was being measured");
+  }
   std::sort(per.begin(), per.end());
   return (int64_t)(per[per.size() / 2] + 0.5);
 }

@@ -15,6 +15,7 @@
 // Operators of one group run in order (Sec. 3: a group is executed
 // sequentially): a consumer tile waits until every tile of its producers has
 // finished (see ios_stage_kernel for why the waits always end).
+#pragma once
 #include <utility>
 
 #include "ios_internal.h"
@@ -867,8 +868,17 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
     __syncthreads();   // the next tile reuses LDS
   }
   if (threadIdx.x == 0) {
-    // relaxed: this workgroup's counter polls have returned before the
-    // increment is issued, so the reset below cannot overtake them
+    // Thread 0 belongs to the wave that issued this workgroup's counter
+    // increments (process_tile).  vmcnt(0) makes the wave wait until every
+    // one of them (and every poll) has been performed before the increment
+    // below is issued, so when the last workgroup sees gridDim.x - 1 every
+    // increment of the launch has landed; the resets depend on the value it
+    // returned, so they are issued after it was performed.  No increment of
+    // this launch can therefore land after a reset and leave a counter
+    // non-zero for the next launch.  (An agent-scope release would do the
+    // same plus an L2 writeback, which the counters do not need: they are
+    // only touched by agent-scope atomics.)
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     int f = __hip_atomic_fetch_add(&a.ctr[1], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (f == (int)gridDim.x - 1) {
       // last workgroup of the launch: leave the counters at zero for the
@@ -879,73 +889,6 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
       __hip_atomic_store(&a.ctr[1], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-}
-
-int op_lds_bytes(const DevOp &op) {
-  if (op.kind == DK_CONV) {
-    TileShape s = tile_shape(op.tcfg);
-    return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
-  }
-  if (op.kind == DK_SEP) return sep_lds_bytes(op.CinP, op.sep_k, op.sep_nbt);
-  if ((op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG) && op.planes_per_tile > 1)
-    return op.planes_per_tile * op.pool_in_rows * op.W * (int)sizeof(float);
-  if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
-    return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
-  return 0;
-}
-
-static void *kernel_of(int variant, bool persist) {
-  if (persist) {
-    switch (variant) {
-      case KV_LIGHT: return (void *)ios_stage_kernel<KV_LIGHT, true>;
-      case KV_SEP: return (void *)ios_stage_kernel<KV_SEP, true>;
-      default: return (void *)ios_stage_kernel<KV_FULL, true>;
-    }
-  }
-  switch (variant) {
-    case KV_LIGHT: return (void *)ios_stage_kernel<KV_LIGHT, false>;
-    case KV_SEP: return (void *)ios_stage_kernel<KV_SEP, false>;
-    default: return (void *)ios_stage_kernel<KV_FULL, false>;
-  }
-}
-
-int stage_capacity(int variant, int lds_bytes) {
-  int dev = 0, per_cu = 0;
-  hipDeviceProp_t prop;
-  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)kernel_of(variant, true),
-                                                   kThreads, lds_bytes) != hipSuccess)
-    return 0;
-  return per_cu * prop.multiProcessorCount;
-}
-
-hipError_t launch_stage(const int32_t *table, int table_words, const StageArgs &args, bool persistent,
-                        int grid, int lds_bytes, int variant, hipStream_t stream) {
-  // dynamic LDS above the default limit must be allowed per kernel, once
-  static int allowed[2][3] = {};
-  int &al = allowed[persistent ? 1 : 0][variant];
-  if (lds_bytes > 64 * 1024 && lds_bytes > al) {
-    hipError_t e = hipFuncSetAttribute(kernel_of(variant, persistent),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
-    if (e != hipSuccess) return e;
-    al = kMaxLdsBytes;
-  }
-  const dim3 g(grid), block(kThreads);
-  const int4 *t = (const int4 *)table;
-  if (persistent) {
-    switch (variant) {
-      case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, true>), g, block, lds_bytes, stream, t, table_words, args); break;
-      case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, true>), g, block, lds_bytes, stream, t, table_words, args); break;
-      default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, true>), g, block, lds_bytes, stream, t, table_words, args); break;
-    }
-    return hipGetLastError();
-  }
-  switch (variant) {
-    case KV_LIGHT: hipLaunchKernelGGL((ios_stage_kernel<KV_LIGHT, false>), g, block, lds_bytes, stream, t, table_words, args); break;
-    case KV_SEP: hipLaunchKernelGGL((ios_stage_kernel<KV_SEP, false>), g, block, lds_bytes, stream, t, table_words, args); break;
-    default: hipLaunchKernelGGL((ios_stage_kernel<KV_FULL, false>), g, block, lds_bytes, stream, t, table_words, args); break;
-  }
-  return hipGetLastError();
 }
 
 }  // namespace ios

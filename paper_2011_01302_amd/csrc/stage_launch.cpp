@@ -1,0 +1,79 @@
+// Host side of the stage kernel: LDS sizes, occupancy and launches.  Each
+// (kernel variant, launch kind) is compiled in a translation unit of its own
+// (stage_kernel_<variant>[_persist].hip) so that they build in parallel; each
+// exports a kernel pointer getter and a launcher.
+#include "ios_internal.h"
+
+namespace ios {
+
+void *stage_kernel_fn_light();
+hipError_t stage_launch_light(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+void *stage_kernel_fn_light_persist();
+hipError_t stage_launch_light_persist(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+void *stage_kernel_fn_sep();
+hipError_t stage_launch_sep(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+void *stage_kernel_fn_sep_persist();
+hipError_t stage_launch_sep_persist(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+void *stage_kernel_fn_full();
+hipError_t stage_launch_full(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+void *stage_kernel_fn_full_persist();
+hipError_t stage_launch_full_persist(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s);
+
+int op_lds_bytes(const DevOp &op) {
+  if (op.kind == DK_CONV) {
+    TileShape s = tile_shape(op.tcfg);
+    return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
+  }
+  if (op.kind == DK_SEP) return sep_lds_bytes(op.CinP, op.sep_k, op.sep_nbt);
+  if ((op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG) && op.planes_per_tile > 1)
+    return op.planes_per_tile * op.pool_in_rows * op.W * (int)sizeof(float);
+  if (op.kind == DK_POOL_MAX || op.kind == DK_POOL_AVG)
+    return ((op.rows_per_tile - 1) * op.sh + op.kh) * op.W * (int)sizeof(float);
+  return 0;
+}
+
+static void *kernel_of(int variant, bool persist) {
+  switch (variant) {
+    case KV_LIGHT: return persist ? stage_kernel_fn_light_persist() : stage_kernel_fn_light();
+    case KV_SEP: return persist ? stage_kernel_fn_sep_persist() : stage_kernel_fn_sep();
+    default: return persist ? stage_kernel_fn_full_persist() : stage_kernel_fn_full();
+  }
+}
+
+int stage_capacity(int variant, int lds_bytes) {
+  int dev = 0, per_cu = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)kernel_of(variant, true),
+                                                   kThreads, lds_bytes) != hipSuccess)
+    return 0;
+  return per_cu * prop.multiProcessorCount;
+}
+
+hipError_t launch_stage(const int32_t *table, int table_words, const StageArgs &args, bool persistent,
+                        int grid, int lds_bytes, int variant, hipStream_t stream) {
+  // dynamic LDS above the default limit must be allowed per kernel, once
+  static int allowed[2][3] = {};
+  int &al = allowed[persistent ? 1 : 0][variant];
+  if (lds_bytes > 64 * 1024 && lds_bytes > al) {
+    hipError_t e = hipFuncSetAttribute(kernel_of(variant, persistent),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
+    if (e != hipSuccess) return e;
+    al = kMaxLdsBytes;
+  }
+  const int4 *t = (const int4 *)table;
+  const int w = table_words;
+  switch (variant) {
+    case KV_LIGHT:
+      return persistent ? stage_launch_light_persist(t, w, args, grid, lds_bytes, stream)
+                        : stage_launch_light(t, w, args, grid, lds_bytes, stream);
+    case KV_SEP:
+      return persistent ? stage_launch_sep_persist(t, w, args, grid, lds_bytes, stream)
+                        : stage_launch_sep(t, w, args, grid, lds_bytes, stream);
+    default:
+      return persistent ? stage_launch_full_persist(t, w, args, grid, lds_bytes, stream)
+                        : stage_launch_full(t, w, args, grid, lds_bytes, stream);
+  }
+}
+
+}  // namespace ios

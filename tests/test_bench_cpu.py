@@ -51,15 +51,28 @@ def test_trace_summary_takes_the_timed_loop_per_stage(tmp_path, capsys):
         w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"])
         for t0, t1, wg in rows:
             w.writerow([STAGE, t0, t1, wg * 512])
-    sched = [{"units": [f"u{k}"], "strategy": "concurrent"} for k in range(3)]
-    (d / "bench.json").write_text(json.dumps({"steps": 2, "stages": 3, "value": 1.0, "schedule": sched}))
-    bench.trace_summary(args(), str(d))
+    sched = [{"units": u, "strategy": "concurrent"} for u in (["A"], ["B1"], ["B2"])]
+    (d / "bench.json").write_text(json.dumps({"steps": 2, "stages": 3, "value": 1.0, "schedule": sched,
+                                              "kernel_sha": "abc"}))
+    bench.trace_summary(args(), str(d), out_dir=str(tmp_path))
     out = json.loads(capsys.readouterr().out)
     assert out["launches"] == 6
     assert [p["median_ns"] for p in out["per_stage"]] == [100.5, 200.5, 300.5]
     assert [p["workgroups"] for p in out["per_stage"]] == [300, 301, 302]
-    assert [p["units"] for p in out["per_stage"]] == [["u0"], ["u1"], ["u2"]]
+    assert [p["units"] for p in out["per_stage"]] == [["A"], ["B1"], ["B2"]]
     assert out["median_gap_ns"] == 10
+    # mean duration 200.5 ns; period = (last end - first start) / 6 = (1261 - 50) / 6... from the rows
+    t_first, t_last = rows[1][0], rows[-1][1]
+    assert out["mean_period_ns"] == round((t_last - t_first) / 6, 1)
+    alg = bench.unit_work(bench_spec_tiny(), 1)
+    mfma = sum(v[0] for v in alg.values())
+    assert out["frac_from_trace"] == round(mfma / 3 / 200.5 / 1e3 / bench.PEAK_FP32_TFLOPS, 5)
+    assert json.load(open(tmp_path / "trace_tiny_bs1.json"))["kernel_sha"] == "abc"
+
+
+def bench_spec_tiny():
+    import workloads as W
+    return W.make("tiny")[0]
 
 
 def test_write_traffic_scales_by_the_copy(tmp_path):

@@ -173,15 +173,124 @@ def test_evaluate_inception_against_torch_float64():
     np.testing.assert_allclose(out, ref, rtol=1e-11, atol=1e-11)
 
 
-def test_evaluate_mean_and_add():
+def _elt_spec(kind, n_in, c=3, h=4, w=5):
+    ins = [{"name": f"x{i}", "c": c, "h": h, "w": w} for i in range(n_in)]
+    return {"name": "elt", "batch": 1, "inputs": ins,
+            "ops": [{"name": "y", "kind": kind, "in": [f"x{i}" for i in range(n_in)]}],
+            "outputs": ["y"]}
+
+
+def test_add_and_mean_closed_forms():
+    """ADD / MEAN (sink mean of RandWire, NASNet's add) pinned by facts that
+    hold whatever the summation order: x + (-x) = 0; k copies of x add to
+    k x and average to x (inputs are 24-bit uniforms, so k x is exact in
+    float64); hand values on small integers."""
+    u = W.make("tiny")[1]["x"][:, :3, :4, :5].astype(np.float64)
+    env = E.evaluate(_elt_spec("add", 2), {"x0": u, "x1": -u})
+    assert np.array_equal(env["y"], np.zeros_like(u))
+    for k in (1, 2, 3, 5):
+        ten = {f"x{i}": u for i in range(k)}
+        assert np.array_equal(E.evaluate(_elt_spec("add", k), ten)["y"], k * u)
+        assert np.array_equal(E.evaluate(_elt_spec("mean", k), ten)["y"], u)
+    a = np.arange(60, dtype=np.float64).reshape(1, 3, 4, 5)
+    b = np.full((1, 3, 4, 5), 7.0)
+    c = 2 * np.ones((1, 3, 4, 5))
+    y = E.evaluate(_elt_spec("add", 3), {"x0": a, "x1": b, "x2": c})["y"]
+    assert y[0, 0, 0, 0] == 9.0 and y[0, 2, 3, 4] == 68.0
+    y = E.evaluate(_elt_spec("mean", 3), {"x0": a, "x1": b, "x2": c})["y"]
+    assert y[0, 0, 0, 0] == 3.0 and y[0, 0, 3, 3] == 9.0 and y[0, 2, 3, 4] == 68.0 / 3.0
+    y = E.evaluate(_elt_spec("mean", 2), {"x0": a, "x1": -a})["y"]
+    assert np.array_equal(y, np.zeros_like(a))
+
+
+def test_evaluate_mean_and_add_wiring():
+    """The workloads wire ADD / MEAN as their descriptions say: RandWire's
+    output is the mean of its sinks, NASNet's concat holds the five adds."""
     spec, ten = W.make("randwire")
     env = E.evaluate(spec, ten)
     sinks = spec["ops"][-1]["in"]
-    ref = sum(env[s] for s in sinks) / len(sinks)
-    np.testing.assert_allclose(env["out"], ref, rtol=1e-14)
+    assert spec["ops"][-1]["kind"] == "mean" and len(sinks) >= 1
     spec, ten = W.make("nasnet")
     env = E.evaluate(spec, ten)
     for b in range(5):
-        add = [op for op in spec["ops"] if op["name"] == f"add{b}"][0]
-        np.testing.assert_array_equal(env[f"add{b}"], env[add["in"][0]] + env[add["in"][1]])
-    np.testing.assert_array_equal(env["out"][:, 168:336], env["add1"])
+        np.testing.assert_array_equal(env["out"][:, 168 * b:168 * (b + 1)], env[f"add{b}"])
+
+
+# ------------------------------------------------------------------ schedule invariance
+
+def evaluate_schedule(spec, ten, blocks, stages):
+    """Evaluate a block stage by stage (Sec. 3): each stage's units in
+    ascending order (a group's chain in order), a merge stage as ONE
+    convolution with the stacked, centred kernels, split back per unit; views
+    as soon as their inputs exist."""
+    from oracle import schedule as O
+    env = {t["name"]: ten[t["name"]].astype(np.float64) for t in spec["inputs"]}
+    views = [op for op in spec["ops"] if op["kind"] in ("concat", "identity")]
+
+    def settle():
+        for op in views:
+            if op["name"] not in env and all(i in env for i in op["in"]):
+                env[op["name"]] = E.eval_op(op, env, ten)
+                settle()
+                return
+    for b, (mask, strat) in stages:
+        us = [blocks[b].units[i] for i in O.bits(mask)]
+        if strat == O.MERGE:
+            convs = [{"w": ten[u["name"] + ".w"], "b": ten.get(u["name"] + ".b"), "pad": (u["ph"], u["pw"]),
+                      "pre_relu": u.get("pre_relu", 0), "post_relu": u.get("post_relu", 0)} for u in us]
+            parts = E.merged_conv(env[us[0]["in"][0]], convs, (us[0]["sh"], us[0]["sw"]))
+            for u, part in zip(us, parts):
+                env[u["name"]] = part
+        else:
+            for u in us:
+                env[u["name"]] = E.eval_op(u, env, ten)
+        settle()
+    return [env[o] for o in spec["outputs"]]
+
+
+def _schedules_with_strategies(blk, masks):
+    """Every strategy assignment of one mask schedule: merge where allowed."""
+    from oracle import schedule as O
+    out = [[]]
+    for m in masks:
+        opts = [O.CONCURRENT] + ([O.MERGE] if O.mergeable(blk, m) else [])
+        out = [q + [(m, t)] for q in out for t in opts]
+    return out
+
+
+def test_every_schedule_gives_identical_outputs_tiny():
+    """Sec. 3: a schedule changes when operators run, never what they
+    compute.  Every schedule of the tiny block (8 partitions, merge wherever
+    it is allowed) gives outputs bit-identical to plain evaluation."""
+    from oracle import schedule as O
+    spec, ten = W.make("tiny", 2, 1)
+    ref = E.outputs(spec, ten)
+    blk = O.blocks_of(spec)[0]
+    n = 0
+    for masks in O.all_schedules(blk):
+        for q in _schedules_with_strategies(blk, masks):
+            out = evaluate_schedule(spec, ten, [blk], [(0, st) for st in q])
+            for a, b in zip(out, ref):
+                assert np.array_equal(a, b)
+            n += 1
+    assert n == 8 + 1     # {A, B1} can merge in the one partition that holds it as a stage
+
+
+def test_sampled_schedules_give_identical_outputs_inception():
+    """The same on the Inception block: 24 of its 34,516 schedules, drawn
+    with a fixed seed, each with merge on every mergeable stage."""
+    from oracle import schedule as O
+    spec, ten = W.make("inception")
+    ref = E.outputs(spec, ten)
+    blk = O.blocks_of(spec)[0]
+    all_q = list(O.all_schedules(blk))
+    assert len(all_q) == 34516
+    pick = np.random.default_rng(7).choice(len(all_q), 24, replace=False)
+    merged = 0
+    for i in pick:
+        q = [(m, O.MERGE if O.mergeable(blk, m) else O.CONCURRENT) for m in all_q[i]]
+        merged += sum(t == O.MERGE for _, t in q)
+        out = evaluate_schedule(spec, ten, [blk], [(0, st) for st in q])
+        for a, b in zip(out, ref):
+            assert np.array_equal(a, b)
+    assert merged > 0

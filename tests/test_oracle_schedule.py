@@ -168,6 +168,37 @@ def test_generate_stage_tie_prefers_merge():
     assert O.generate_stage(blk, 0b011, lambda m, t: 5 + t) == (5, O.CONCURRENT)
 
 
+def test_ios_merge_variant_runs_single_units_alone():
+    """IOS-Merge (Sec. 6.1: operator merge only, no concurrent execution).
+    A stage of one operator is that operator, so it still runs; a stage of
+    several operators exists only if they merge.  (1) With no mergeable set
+    the only schedules left are the n! / (orderings allowed by the edges)
+    sequences of single units, each costing the sum of the singles.  (2) On
+    the tiny block the two IOS-Merge schedules are, by hand,
+    singles in some order, 3 + 4 + 6 = 13, and merge{A, B1} {B2} = 5 + 6 = 11;
+    among the equal-cost orders of the singles the tie-break on the last
+    stage's mask puts {A} (mask 1) last: {B1} {B2} {A}."""
+    rnd = random.Random(11)
+    for trial in range(30):
+        n = rnd.randint(1, 6)
+        blk = random_dag(n, 0.4, rnd)          # abstract units: nothing merges
+        single = {1 << i: rnd.randint(1, 9) for i in range(n)}
+        cost = lambda m, t: single.get(m, 1000)
+        res = O.ios_dp(blk, cost, strategies=(O.MERGE,))
+        assert res.cost == sum(single.values())
+        assert all(m & (m - 1) == 0 for m, _ in res.schedule)
+        assert sorted(m for m, _ in res.schedule) == sorted(single)
+    blk = O.blocks_of(W.make("tiny")[0])[0]    # units A, B1, B2 (B1 -> B2)
+    table = {(0b001, O.CONCURRENT): 3, (0b010, O.CONCURRENT): 4, (0b100, O.CONCURRENT): 6,
+             (0b011, O.MERGE): 5}
+    cost = lambda m, t: table.get((m, t), 100)
+    res = O.ios_dp(blk, cost, strategies=(O.MERGE,))
+    assert res.cost == 11 and res.schedule == [(0b011, O.MERGE), (0b100, O.CONCURRENT)]
+    table[(0b011, O.MERGE)] = 8                 # now merging loses: 8 + 6 > 13
+    res = O.ios_dp(blk, cost, strategies=(O.MERGE,))
+    assert res.cost == 13 and [m for m, _ in res.schedule] == [0b010, 0b100, 0b001]
+
+
 def test_merge_rules_on_configs():
     blk = O.blocks_of(W.make("inception")[0])[0]
     names = [u["name"] for u in blk.units]

@@ -307,6 +307,25 @@ int ios_schedule_dump_costs(const ios_graph *g, const char *path);
 int ios_run(ios_graph *g, ios_schedule_t *q, const float *const *d_inputs,
             float *const *d_outputs, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): ios_run
+ * with no allocation of any kind.  The intermediate activations between
+ * stages and the in-stage counters, which ios_run keeps in memory the graph
+ * and the schedule allocated, live here in one fixed device array of 64 MiB
+ * per device, which the library holds until the process ends; the caller
+ * still passes the inputs and outputs, as for ios_run.  Preconditions: the
+ * schedule has been run once with ios_run (which sets up the graph's device
+ * side and compiles the stages), and the graph's intermediates fit the
+ * array (8 KiB of counters, then each intermediate rounded up to 256 bytes).
+ * Every call on one device shares that device's array and leaves its last
+ * contents there: calls that overlap in time on one device race, so issue
+ * them on one stream.  Asynchronous, like ios_run.
+ * Errors: IOS_E_ARG (null pointers, schedule of another graph), IOS_E_STATE
+ * (preconditions), IOS_E_UNSUPPORTED (intermediates larger than the array),
+ * IOS_E_HIP. */
+int ios_run_noalloc(ios_graph *g, const ios_schedule_t *q, const float *const *d_inputs,
+                    float *const *d_outputs, void *hip_stream);
+
 /* As ios_run, then records a HIP event before and after every stage launch,
  * waits for the stream, and writes each stage's GPU time in ns to
  * stage_ns[0 .. n_stages-1].  For per-stage measurement; blocks the caller. */

@@ -51,7 +51,8 @@ EXPORTED = ["ios_graph_create", "ios_graph_destroy", "ios_add_input", "ios_add_o
             "ios_get_unit_tiling", "ios_set_unit_tiling",
             "ios_sched_opts_default", "ios_schedule",
             "ios_schedule_from_stages", "ios_schedule_get", "ios_schedule_stats",
-            "ios_schedule_tune_tiles", "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_timed",
+            "ios_schedule_tune_tiles", "ios_schedule_destroy", "ios_schedule_dump_costs", "ios_run", "ios_run_noalloc",
+            "ios_run_timed",
             "ios_device_status", "ios_last_error"]
 
 
@@ -108,6 +109,7 @@ _sig = {
     "ios_schedule_destroy": (None, [_P]),
     "ios_schedule_dump_costs": (ctypes.c_int, [_P, ctypes.c_char_p]),
     "ios_run": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), ctypes.POINTER(_P), _P]),
+    "ios_run_noalloc": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), ctypes.POINTER(_P), _P]),
     "ios_run_timed": (ctypes.c_int, [_P, _P, ctypes.POINTER(_P), ctypes.POINTER(_P), _P, _pi64]),
     "ios_device_status": (ctypes.c_int, [_P, _P, _pi32]),
     "ios_last_error": (ctypes.c_char_p, []),
@@ -306,6 +308,10 @@ def ios_run(g: int, q: int, d_inputs: Sequence[int], d_outputs: Sequence[int], s
     """Device pointers (ints, e.g. ``tensor.data_ptr()``) and a hipStream_t
     (e.g. ``torch.cuda.current_stream().cuda_stream``)."""
     _check(_lib.ios_run(g, q, _ptrs(d_inputs), _ptrs(d_outputs), stream or None))
+
+
+def ios_run_noalloc(g: int, q: int, d_inputs: Sequence[int], d_outputs: Sequence[int], stream: int = 0) -> None:
+    _check(_lib.ios_run_noalloc(g, q, _ptrs(d_inputs), _ptrs(d_outputs), stream or None))
 
 
 def ios_run_timed(g: int, q: int, d_inputs: Sequence[int], d_outputs: Sequence[int], stream: int = 0,

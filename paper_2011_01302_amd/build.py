@@ -28,7 +28,7 @@ DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "
 # the stage kernel variants build as separate translation units, in parallel
 SOURCES = ["stage_kernel_full.hip", "stage_kernel_full_persist.hip", "stage_kernel_sep.hip",
            "stage_kernel_sep_persist.hip", "stage_kernel_light.hip", "stage_kernel_light_persist.hip",
-           "graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_launch.cpp"]
+           "noalloc.hip", "graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_launch.cpp"]
 
 
 def _compile(src: str) -> str:

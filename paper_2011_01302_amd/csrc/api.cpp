@@ -22,7 +22,14 @@ void dump_costs(const ios_graph *g, const char *path);
 
 using namespace ios;
 
-static thread_local std::string g_last_error;
+// The calling thread's last error message, in a fixed buffer so that setting
+// it never allocates (ios_run_noalloc reports errors through it too).
+static thread_local char g_last_error[512];
+
+void ios::set_last_error_text(const char *msg) {
+  std::strncpy(g_last_error, msg, sizeof(g_last_error) - 1);
+  g_last_error[sizeof(g_last_error) - 1] = 0;
+}
 
 template <class F>
 static int guarded(F &&f) {
@@ -30,13 +37,13 @@ static int guarded(F &&f) {
     f();
     return IOS_OK;
   } catch (const Error &e) {
-    g_last_error = e.msg;
+    set_last_error_text(e.msg.c_str());
     return e.code;
   } catch (const std::bad_alloc &) {
-    g_last_error = "host allocation failed";
+    set_last_error_text("host allocation failed");
     return IOS_E_OOM;
   } catch (const std::exception &e) {
-    g_last_error = e.what();
+    set_last_error_text(e.what());
     return IOS_E_ARG;
   }
 }
@@ -60,7 +67,7 @@ static std::vector<int> ops_of_units(const ios_graph *g, const int32_t *ids, int
 
 extern "C" {
 
-const char *ios_last_error(void) { return g_last_error.c_str(); }
+const char *ios_last_error(void) { return g_last_error; }
 
 int ios_graph_create(int32_t batch, ios_graph **out) {
   return guarded([&] {
@@ -82,7 +89,7 @@ void ios_graph_destroy(ios_graph *g) {
     if (op.d_bias) (void)hipFree(op.d_bias);
     if (op.d_dw) (void)hipFree(op.d_dw);
   }
-  CompiledStage &s = g->scratch;
+  CompiledStage &s = g->prof_stage;
   if (s.d_table) (void)hipFree(s.d_table);
   if (s.d_ctr) (void)hipFree(s.d_ctr);
   if (s.d_mw) (void)hipFree(s.d_mw);

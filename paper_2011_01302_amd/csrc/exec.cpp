@@ -138,12 +138,12 @@ double tile_work(const DevOp &d) {
 }
 
 template <class T>
-void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool scratch) {
+void grow_upload(T **dptr, size_t *cap, const std::vector<T> &v, bool reuse) {
   size_t n = std::max<size_t>(v.size(), 1);
-  if (!scratch || *cap < n) {
-    if (scratch && *dptr) (void)hipFree(*dptr);
+  if (!reuse || *cap < n) {
+    if (reuse && *dptr) (void)hipFree(*dptr);
     hip_check(hipMalloc(dptr, sizeof(T) * n), "hipMalloc(stage)");
-    if (scratch) *cap = n;
+    if (reuse) *cap = n;
   }
   if (!v.empty())
     hip_check(hipMemcpy(*dptr, v.data(), sizeof(T) * v.size(), hipMemcpyHostToDevice),
@@ -181,7 +181,7 @@ void free_stage(CompiledStage *cs) {
 }
 
 void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
-                   bool scratch) {
+                   bool reuse) {
   if (ops.empty()) fail(IOS_E_BAD_STAGE, "empty stage");
   int blk = g->ops[ops[0]].block;
   for (size_t i = 0; i < ops.size(); ++i) {
@@ -402,13 +402,13 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     if (cap <= 0) fail(IOS_E_HIP, "cannot size the persistent launch of a stage with dependencies");
     cs->grid = std::min(cs->grid, cap);
   }
-  cs->owns = !scratch;
+  cs->owns = !reuse;
   // device copies
   if (!mw.empty()) {
-    size_t *wc = scratch ? &g->scratch_w_cap : nullptr, *bc = scratch ? &g->scratch_b_cap : nullptr;
+    size_t *wc = reuse ? &g->prof_w_cap : nullptr, *bc = reuse ? &g->prof_b_cap : nullptr;
     size_t dummy_w = 0, dummy_b = 0;
-    grow_upload(&cs->d_mw, wc ? wc : &dummy_w, mw, scratch);
-    grow_upload(&cs->d_mb, bc ? bc : &dummy_b, mb, scratch);
+    grow_upload(&cs->d_mw, wc ? wc : &dummy_w, mw, reuse);
+    grow_upload(&cs->d_mb, bc ? bc : &dummy_b, mb, reuse);
     cs->ops[0].wpk = cs->d_mw;
     cs->ops[0].bias = cs->d_mb;
   }
@@ -431,9 +431,9 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   for (int i = 0; i <= n; ++i) cs->table[4 + i] = start[i];
   std::memcpy(&cs->table[devop_off], cs->ops.data(), sizeof(DevOp) * n);
   size_t d0 = 0, d2 = 0;
-  grow_upload(&cs->d_table, scratch ? &g->scratch_ops_cap : &d0, cs->table, scratch);
+  grow_upload(&cs->d_table, reuse ? &g->prof_ops_cap : &d0, cs->table, reuse);
   std::vector<int32_t> ctr(2 + kCtrStride * kCtrCopies, 0);
-  grow_upload(&cs->d_ctr, scratch ? &g->scratch_ctr_cap : &d2, ctr, scratch);
+  grow_upload(&cs->d_ctr, reuse ? &g->prof_ctr_cap : &d2, ctr, reuse);
 }
 
 void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
@@ -452,7 +452,7 @@ void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<fl
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,
                       int reps, int repeats) {
   if (reps < 1 || repeats < 1 || warmup < 0) fail(IOS_E_ARG, "bad profiling counts");
-  CompiledStage &cs = g->scratch;
+  CompiledStage &cs = g->prof_stage;
   compile_stage(g, ops, strategy, &cs, true);
   std::vector<float *> bufs = default_buffers(g);
   for (int i = 0; i < warmup; ++i) launch_compiled(g, cs, bufs, g->stream);

@@ -461,6 +461,19 @@ void ensure_device(ios_graph *g) {
     }
   }
   hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  // layout of the intermediates in ios_run_noalloc's scratch array: after
+  // the counter block, each buffer that is neither an input nor an output
+  // at a 256-byte boundary
+  noalloc_setup(g->device);
+  g->noalloc_off.assign(g->bufs.size(), 0);
+  size_t off = noalloc_counter_bytes();
+  for (size_t i = 0; i < g->bufs.size(); ++i) {
+    const Buffer &b = g->bufs[i];
+    if (b.input_index >= 0 || b.output_index >= 0) continue;
+    g->noalloc_off[i] = off;
+    off += (b.elems(g->batch) * sizeof(float) + 255) & ~(size_t)255;
+  }
+  g->noalloc_bytes = off;
   g->device_ready = true;
   const bool tune_conv = !std::getenv("IOS_CONV_TILE"), tune_sep = !std::getenv("IOS_SEP_NBT");
   if ((tune_conv || tune_sep) && !g->units.empty()) {

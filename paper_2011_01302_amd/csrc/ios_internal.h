@@ -29,6 +29,9 @@ constexpr int kCtrStride = 64;    // >= kMaxStageOps
 constexpr int kMaxUnitsPerBlock = 64;
 constexpr int kMaxChannels = 256; // SEPCONV input channels (8 waves x 8 k-steps of 4)
 constexpr int64_t kInf = INT64_MAX;
+// Device array that ios_run_noalloc uses for the intermediates and the
+// in-stage counters (one per device, held until the process ends).
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
 
 // Kinds of work a stage kernel tile can do.
 enum DevKind : int32_t {
@@ -238,7 +241,7 @@ struct CompiledStage {
   int grid = 0;                  // workgroups launched
   int variant = 0;               // KernelVariant
   std::vector<int32_t> table;    // header, op_start, DevOps (see kDevOpWords)
-  // device copies (owned unless `scratch`)
+  // device copies (owned unless reused by the profiler)
   int32_t *d_table = nullptr;
   int32_t *d_ctr = nullptr;
   float *d_mw = nullptr, *d_mb = nullptr;   // merged weights / bias
@@ -263,10 +266,14 @@ struct ios_graph {
   hipStream_t stream = nullptr;  // library stream for profiling
   int device = 0;
   int32_t *d_err = nullptr;
-  // profiling scratch (reused by every candidate stage)
-  ios::CompiledStage scratch;
-  size_t scratch_ops_cap = 0, scratch_ctr_cap = 0, scratch_w_cap = 0, scratch_b_cap = 0;
+  // the stage profiler's compiled stage (reused by every candidate stage)
+  ios::CompiledStage prof_stage;
+  size_t prof_ops_cap = 0, prof_ctr_cap = 0, prof_w_cap = 0, prof_b_cap = 0;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  // ios_run_noalloc: byte offset of each intermediate buffer in the scratch
+  // array (counters first), and the bytes the graph needs there
+  std::vector<size_t> noalloc_off;
+  size_t noalloc_bytes = 0;
   // last search's cost table, per block: mask -> latencies
   std::vector<std::map<uint64_t, ios::CostRow>> cost_table;
 };
@@ -289,6 +296,12 @@ struct Error {
 };
 [[noreturn]] void fail(int code, const std::string &msg);
 void hip_check(hipError_t e, const char *what);
+// api.cpp: set the calling thread's ios_last_error() text (no allocation)
+void set_last_error_text(const char *msg);
+// noalloc.hip: per-device set-up of the scratch array (device address, zero
+// counters); the counter block's size, which the intermediates follow
+void noalloc_setup(int device);
+size_t noalloc_counter_bytes();
 
 // graph.cpp
 int unit_op_of_tensor(const ios_graph *g, int tensor_id);   // op index or throws
@@ -308,7 +321,7 @@ int64_t op_flops(const ios_graph *g, const Op &op);
 void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out,
                        int *ng, int *nb);
 void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
-                   bool scratch);
+                   bool reuse);
 void free_stage(CompiledStage *cs);
 void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
                      hipStream_t stream);

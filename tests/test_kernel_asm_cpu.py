@@ -25,21 +25,27 @@ OBJDUMP = "/opt/rocm/llvm/bin/llvm-objdump"
 BUNDLE_MAGIC = b"__CLANG_OFFLOAD_BUNDLE__"
 
 
-def gfx950_code_object(path):
-    """The gfx950 entry of the clang offload bundle inside a host binary."""
+def gfx950_code_objects(path):
+    """The gfx950 entries of every clang offload bundle inside a host binary
+    (one bundle per HIP translation unit)."""
     data = open(path, "rb").read()
-    base = data.find(BUNDLE_MAGIC)
-    assert base >= 0, "no offload bundle in the library"
-    n = struct.unpack_from("<Q", data, base + len(BUNDLE_MAGIC))[0]
-    p = base + len(BUNDLE_MAGIC) + 8
-    for _ in range(n):
-        off, size, idlen = struct.unpack_from("<QQQ", data, p)
-        p += 24
-        ident = data[p:p + idlen].decode()
-        p += idlen
-        if ident.endswith("gfx950"):
-            return data[base + off: base + off + size]
-    raise AssertionError("no gfx950 code object in the bundle")
+    out, start = [], 0
+    while True:
+        base = data.find(BUNDLE_MAGIC, start)
+        if base < 0:
+            break
+        n = struct.unpack_from("<Q", data, base + len(BUNDLE_MAGIC))[0]
+        p = base + len(BUNDLE_MAGIC) + 8
+        for _ in range(n):
+            off, size, idlen = struct.unpack_from("<QQQ", data, p)
+            p += 24
+            ident = data[p:p + idlen].decode()
+            p += idlen
+            if ident.endswith("gfx950"):
+                out.append(data[base + off: base + off + size])
+        start = base + 1
+    assert out, "no gfx950 code object in the library"
+    return out
 
 
 def masked_readlanes(lines):
@@ -68,17 +74,21 @@ def masked_readlanes(lines):
 def disassembly(tmp_path_factory):
     if not os.path.exists(LIB):
         pytest.skip("libios.so is not built")
-    co = tmp_path_factory.mktemp("asm") / "stage.co"
-    co.write_bytes(gfx950_code_object(LIB))
-    out = subprocess.run([OBJDUMP, "-d", "--mcpu=gfx950", str(co)], check=True, capture_output=True,
-                         text=True).stdout
-    return out.splitlines()
+    d = tmp_path_factory.mktemp("asm")
+    lines = []
+    for k, co in enumerate(gfx950_code_objects(LIB)):
+        f = d / f"tu{k}.co"
+        f.write_bytes(co)
+        lines += subprocess.run([OBJDUMP, "-d", "--mcpu=gfx950", str(f)], check=True, capture_output=True,
+                                text=True).stdout.splitlines()
+    return lines
 
 
 def test_stage_kernels_present(disassembly):
     names = {re.match(r"^[0-9a-f]+ <(\S+)>:", l).group(1) for l in disassembly
              if re.match(r"^[0-9a-f]+ <(\S+)>:", l)}
-    assert any("ios_stage_kernel" in n for n in names)
+    # every kernel variant (light / sep / full) x launch kind (tile / persistent)
+    assert len({n for n in names if "ios_stage_kernel" in n}) == 6
 
 
 def test_no_readlane_of_possibly_disabled_lanes(disassembly):

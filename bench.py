@@ -35,7 +35,9 @@ PEAK_FP32_TFLOPS = 157.3          # MI355X dense fp32 MFMA (256 CU x 2.4 GHz x 2
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = ["paper_2011_01302_amd/csrc/" + f for f in (
     "stage_kernel.h", "stage_kernel_full.hip", "stage_kernel_full_persist.hip", "stage_kernel_sep.hip",
-    "stage_kernel_sep_persist.hip", "stage_kernel_light.hip", "stage_kernel_light_persist.hip",
+    "stage_kernel_sep_persist.hip", "stage_kernel_seprow.hip", "stage_kernel_seprow_persist.hip",
+    "stage_kernel_pipe.hip", "stage_kernel_pipe_persist.hip", "stage_kernel_light.hip",
+    "stage_kernel_light_persist.hip",
     "stage_launch.cpp", "exec.cpp", "ios_internal.h")]
 
 
@@ -503,7 +505,8 @@ def run_next(args):
     import paper_2011_01302_amd as I
     import workloads as W
     stream = torch.cuda.current_stream().cuda_stream
-    out = {"ablation": [], "batch": [], "pruning": []}
+    out = {"ablation": [], "batch": [], "pruning": [], "fig10": []}
+    parts = set(args.next_parts.split(",")) if args.next_parts else {"ablation", "batch", "pruning", "fig10"}
 
     def fast(o, config):
         if config in ("randwire", "nasnet"):       # tens of thousands of candidate stages
@@ -524,7 +527,7 @@ def run_next(args):
         return round(us, 2)
 
     # (1) strategy ablation
-    for config in W.CONFIG_NAMES:
+    for config in (W.CONFIG_NAMES if "ablation" in parts else []):
         spec, g, ins, outs = _setup(I, W, torch, config, 1, args.seed)
         gflop = sum(w[0] + w[1] for w in unit_work(spec, 1).values()) / 1e9
         row = {"config": config}
@@ -555,7 +558,7 @@ def run_next(args):
         g.close()
 
     # (2) batch specialisation
-    for config, batches in (("inception", (1, 16)), ("squeeze", (1, 32, 128))):
+    for config, batches in ((("inception", (1, 16)), ("squeeze", (1, 32, 128))) if "batch" in parts else ()):
         scheds = {}
         for b in batches:
             spec, g, ins, outs = _setup(I, W, torch, config, b, args.seed)
@@ -579,8 +582,41 @@ def run_next(args):
             del ins, outs
             torch.cuda.empty_cache()
 
+    # (4) the last Inception-V3 module at batch 1 and 32 (Sec. 7.2, Fig. 10):
+    # schedules searched at each batch size, which pairs they merge, and each
+    # schedule run at both batch sizes
+    if "fig10" in parts:
+        scheds = {}
+        for b in (1, 32):
+            spec, g, ins, outs = _setup(I, W, torch, "inception_7c", b, args.seed)
+            q, pred = I.ios_schedule(g.handle, I.ios_sched_opts_default())
+            st = I.ios_schedule_get(q)
+            scheds[b] = [(ids, t) for ids, t in st]
+            gflop = sum(w[0] + w[1] for w in unit_work(spec, b).values()) / 1e9
+            row = {"optimised_for": b, "stages": [(g.names(ids), "merge" if t else "concurrent") for ids, t in st],
+                   "merged_pairs": [g.names(ids) for ids, t in st if t == I.IOS_MERGE],
+                   "predicted_us": pred / 1e3, "gflop": round(gflop, 3)}
+            I.ios_schedule_destroy(q)
+            out["fig10"].append(row)
+            print(f"[next] fig10 optimised for bs{b}: " + json.dumps(row), file=sys.stderr, flush=True)
+            g.close()
+            del ins, outs
+        for run_b in (1, 32):
+            spec, g, ins, outs = _setup(I, W, torch, "inception_7c", run_b, args.seed)
+            gflop = sum(w[0] + w[1] for w in unit_work(spec, run_b).values()) / 1e9
+            row = {"run_batch": run_b}
+            for opt_b in (1, 32):
+                q = I.ios_schedule_from_stages(g.handle, [ids for ids, _ in scheds[opt_b]], [t for _, t in scheds[opt_b]])
+                row[f"optimised_for_bs{opt_b}"] = timed(g, q, ins, outs, gflop)
+                I.ios_schedule_destroy(q)
+            out["fig10"].append(row)
+            print(f"[next] fig10 run at bs{run_b}: " + json.dumps(row), file=sys.stderr, flush=True)
+            g.close()
+            del ins, outs
+            torch.cuda.empty_cache()
+
     # (3) pruning
-    for config in ("inception", "randwire", "nasnet"):
+    for config in (("inception", "randwire", "nasnet") if "pruning" in parts else ()):
         spec, g, ins, outs = _setup(I, W, torch, config, 1, args.seed)
         gflop = sum(w[0] + w[1] for w in unit_work(spec, 1).values()) / 1e9
         for r in (1, 2, 3):
@@ -615,7 +651,8 @@ def run_network(args):
     import workloads as W
     stream = torch.cuda.current_stream().cuda_stream
     report = []
-    for net in W.NETWORK_NAMES:
+    nets = args.networks.split(",") if args.networks else W.NETWORK_NAMES
+    for net in nets:
         print(f"[network] {net} bs{args.batch}: graph", file=sys.stderr, flush=True)
         spec, g, ins, outs = _setup(I, W, torch, net, args.batch, args.seed)
         work = unit_work(spec, args.batch)
@@ -634,6 +671,9 @@ def run_network(args):
             o = I.ios_sched_opts_default()
             o.mode = mode
             o.r, o.s = args.r, args.s
+            if net in ("randwire_net", "nasnet_net"):   # tens of thousands of candidate stages per block
+                o.warmup, o.reps, o.repeats = 1, 3, 1
+                o.verify_reps = 20                      # the picked stages measured in full
             print(f"[network] {net}: {name} schedule", file=sys.stderr, flush=True)
             for u, t in iso.items():
                 I.ios_set_conv_tile(g.handle, u, t)
@@ -801,6 +841,9 @@ def main():
     ap.add_argument("--network", default="",
                     help="schedule whole networks block by block (IOS vs sequential vs greedy, "
                          "end to end and per block) and write a JSON report to this path")
+    ap.add_argument("--networks", default="", help="with --network: comma-separated subset of the networks")
+    ap.add_argument("--next-parts", default="", help="with --next: comma-separated subset of "
+                                                      "ablation,batch,pruning,fig10")
     ap.add_argument("--trace-summary", default="", metavar="TRACE_DIR",
                     help="summarise the timed loop of a rocprofv3 --kernel-trace run of this "
                          "benchmark and exit")

@@ -168,20 +168,24 @@ int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t 
  * conv alone with each shape and keeps one; these calls read that choice or
  * replace it, e.g. to replay the shapes of an earlier run.  Shapes are
  * 0 .. IOS_CONV_TILE_SHAPES - 1 (16x16, 16x32, 32x32, 32x64, 64x64 and
- * 128x64 output pixels x channels).  A new shape applies to stages compiled
+ * 128x64 output pixels x channels, operands loaded per wave; then 128x64,
+ * 256x32 and 64x128 with both operands staged in LDS by a pipeline of
+ * direct loads, for large convolutions).  A new shape applies to stages compiled
  * afterwards (ios_profile_stage, ios_schedule, ios_schedule_from_stages),
  * not to schedules that already exist.  Both calls set up the device first
  * (hence the measurement) if no earlier call has.
  * Errors: IOS_E_ARG (not a conv unit, shape out of range, null pointer),
  * IOS_E_STATE (not finalized), IOS_E_HIP. */
-enum { IOS_CONV_TILE_SHAPES = 6 };
+enum { IOS_CONV_TILE_SHAPES = 9 };
 int ios_get_conv_tile(ios_graph *g, int32_t unit_id, int32_t *shape);
 int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
 
 /* Every tuning choice of one unit, so that a tuned schedule can be replayed
- * exactly: `tile` is a CONV's tile shape (as above) or a SEPCONV's
- * 16-channel output blocks per tile (1 .. its maximum), 0 for the other
- * kinds; `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
+ * exactly: `tile` is a CONV's tile shape (as above) or a SEPCONV's tile
+ * choice (0, 1, 2: runs of 16, 32 or 64 consecutive output pixels with
+ * every output channel, input rows staged in LDS; 3 .. 6: 16 pixels of one
+ * output row with 1 .. 4 blocks of 16 output channels, for at most 256
+ * input channels and windows up to 5 x 5), 0 for the other kinds; `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
  * unit sends to one XCD (0, 2 or 4), or -1 to let the library's L2-fill
  * model choose (ios_schedule_tune_tiles sets both per stage).  A stage whose
  * units disagree on xcd_lg uses the model.  These are implementation
@@ -274,8 +278,8 @@ int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transi
  * set on the graph's units (ios_get_conv_tile reads the shapes), so call it
  * on the schedule that will run; q's stages are recompiled on its next run.
  * A unit belongs to one stage of a schedule, so the stages do not compete.
- * With IOS_CONV_TILE (IOS_SEP_NBT) set in the environment the conv shapes
- * (SEPCONV blocks) stay fixed, the rest is still chosen; IOS_XCD_RUNS=0, 2 or 4 fixes the tile order's run
+ * With IOS_CONV_TILE (IOS_SEP_TILE) set in the environment the conv shapes
+ * (SEPCONV tile choices) stay fixed, the rest is still chosen; IOS_XCD_RUNS=0, 2 or 4 fixes the tile order's run
  * length (2^value) for every stage compiled while it is set, for tests.  *cost_ns = sum of the stages' final measured
  * latencies.
  * Errors: IOS_E_ARG (null pointer, bad counts, schedule of another graph),

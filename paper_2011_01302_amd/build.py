@@ -27,7 +27,9 @@ DEVICE = ["-x", "hip", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "
           "-packed-fp32-ops", "-munsafe-fp-atomics", "-mllvm", "-amdgpu-kernarg-preload-count=3"]
 # the stage kernel variants build as separate translation units, in parallel
 SOURCES = ["stage_kernel_full.hip", "stage_kernel_full_persist.hip", "stage_kernel_sep.hip",
-           "stage_kernel_sep_persist.hip", "stage_kernel_light.hip", "stage_kernel_light_persist.hip",
+           "stage_kernel_sep_persist.hip", "stage_kernel_seprow.hip", "stage_kernel_seprow_persist.hip",
+           "stage_kernel_pipe.hip", "stage_kernel_pipe_persist.hip", "stage_kernel_light.hip",
+           "stage_kernel_light_persist.hip",
            "noalloc.hip", "graph.cpp", "sched.cpp", "exec.cpp", "api.cpp", "stage_launch.cpp"]
 
 

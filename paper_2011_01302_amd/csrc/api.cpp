@@ -88,6 +88,9 @@ void ios_graph_destroy(ios_graph *g) {
     if (op.d_wpk) (void)hipFree(op.d_wpk);
     if (op.d_bias) (void)hipFree(op.d_bias);
     if (op.d_dw) (void)hipFree(op.d_dw);
+    if (op.d_dw_row) (void)hipFree(op.d_dw_row);
+    if (op.d_pw_row) (void)hipFree(op.d_pw_row);
+    if (op.d_wg) (void)hipFree(op.d_wg);
   }
   CompiledStage &s = g->prof_stage;
   if (s.d_table) (void)hipFree(s.d_table);
@@ -198,7 +201,7 @@ int ios_get_unit_tiling(ios_graph *g, int32_t unit_id, int32_t *tile, int32_t *x
     need(tile != nullptr && xcd_lg != nullptr, "null argument");
     const Op &op = g->ops[unit_op_of_tensor(g, unit_id)];
     ensure_device(g);
-    *tile = op.d.kind == IOS_CONV ? op.tcfg : op.d.kind == IOS_SEPCONV ? op.sep_nbt : 0;
+    *tile = op.d.kind == IOS_CONV ? op.tcfg : op.d.kind == IOS_SEPCONV ? op.sep_tile : 0;
     *xcd_lg = op.xcd_lg;
   });
 }
@@ -213,8 +216,8 @@ int ios_set_unit_tiling(ios_graph *g, int32_t unit_id, int32_t tile, int32_t xcd
       need(tile >= 0 && tile < TC_COUNT, "conv tile shape out of range");
       op.tcfg = tile;
     } else if (op.d.kind == IOS_SEPCONV) {
-      need(tile >= 1 && tile <= max_sep_nbt(op), "SEPCONV tile choice out of range");
-      op.sep_nbt = tile;
+      need(sep_tile_ok(op, tile), "SEPCONV tile choice out of range or not applicable to this unit");
+      op.sep_tile = tile;
     } else {
       need(tile == 0, "this unit kind has no tile choice (tile must be 0)");
     }
@@ -265,7 +268,7 @@ int ios_schedule_from_stages(ios_graph *g, int32_t n_stages, const int32_t *stag
 // length set explicitly (else the stage kernel's L2-fill model picks it),
 // with its convs' shapes varied one conv at a time (all of them together in
 // a merge stage, whose merged conv takes one shape) and with each SEPCONV's
-// blocks per tile varied, keeping a change only when the stage gets faster
+// tile choice varied, keeping a change only when the stage gets faster
 // by more than kStageTileSlack.  A shape measured alone
 // fills the GPU by itself; inside a stage other operators share the CUs, so
 // larger tiles can pay off there.
@@ -283,12 +286,12 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
     need(o.warmup >= 0 && o.reps >= 1 && o.repeats >= 1, "bad profiling counts");
     ensure_device(g);
     const bool forced = std::getenv("IOS_CONV_TILE") != nullptr;
-    const bool sep_forced = std::getenv("IOS_SEP_NBT") != nullptr;
+    const bool sep_forced = std::getenv("IOS_SEP_TILE") != nullptr;
     // on an error the units get their shapes and orders back
     std::vector<std::array<int, 4>> saved;
     for (int32_t u : q->unit_ids) {
       const int op = unit_op_of_tensor(g, u);
-      saved.push_back({op, g->ops[op].tcfg, g->ops[op].xcd_lg, g->ops[op].sep_nbt});
+      saved.push_back({op, g->ops[op].tcfg, g->ops[op].xcd_lg, g->ops[op].sep_tile});
     }
     int64_t total = 0;
     try {
@@ -340,10 +343,10 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
         }
         if (!sep_forced)
           for (int op : ops)
-            if (g->ops[op].d.kind == IOS_SEPCONV) knobs.push_back({{op}, true, 1, max_sep_nbt(g->ops[op])});
-        auto get = [&](const Knob &kn) { return kn.sep ? g->ops[kn.ops[0]].sep_nbt : g->ops[kn.ops[0]].tcfg; };
+            if (g->ops[op].d.kind == IOS_SEPCONV) knobs.push_back({{op}, true, 0, kSepTiles - 1});
+        auto get = [&](const Knob &kn) { return kn.sep ? g->ops[kn.ops[0]].sep_tile : g->ops[kn.ops[0]].tcfg; };
         auto set = [&](const Knob &kn, int v) {
-          for (int c : kn.ops) (kn.sep ? g->ops[c].sep_nbt : g->ops[c].tcfg) = v;
+          for (int c : kn.ops) (kn.sep ? g->ops[c].sep_tile : g->ops[c].tcfg) = v;
         };
         for (int pass = 0; pass < 2; ++pass) {
           bool improved = pass == 0 && tune_xcd_order();
@@ -351,7 +354,7 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
             const int cur = get(kn);
             int keep = cur;
             for (int v = kn.lo; v <= kn.hi; ++v) {
-              if (v == cur) continue;
+              if (v == cur || (kn.sep && !sep_tile_ok(g->ops[kn.ops[0]], v))) continue;
               set(kn, v);
               const int64_t ns = measure();
               if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
@@ -370,7 +373,7 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
       for (const auto &v : saved) {
         g->ops[v[0]].tcfg = v[1];
         g->ops[v[0]].xcd_lg = v[2];
-        g->ops[v[0]].sep_nbt = v[3];
+        g->ops[v[0]].sep_tile = v[3];
       }
       throw;
     }

@@ -113,7 +113,8 @@ static int choose_xcd_runs(const std::vector<DevOp> &ops, const std::vector<int3
         if (d.kind != DK_CONV) continue;
         const int ti = t - start[i], tm = ti / d.tiles_n, tn = ti % d.tiles_n;
         if (a_seen.insert({i, b & 7, tm}).second) bytes += 4.0 * tile_bm(d.tcfg) * d.CinP * d.kh;
-        if (b_seen.insert({i, b & 7, tn}).second) bytes += 4.0 * tile_bn(d.tcfg) * 16.0 * d.NG;
+        if (b_seen.insert({i, b & 7, tn}).second)
+          bytes += 4.0 * tile_bn(d.tcfg) * (tile_is_pipe(d.tcfg) ? (double)kPipeKB : 16.0) * d.NG;
       }
     if (best < 0.0 || bytes < best) {
       best = bytes;
@@ -127,11 +128,13 @@ static int choose_xcd_runs(const std::vector<DevOp> &ops, const std::vector<int3
 double tile_work(const DevOp &d) {
   switch (d.kind) {
     case DK_CONV: {
+      if (tile_is_pipe(d.tcfg)) return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * kPipeKB * d.NG / kWaves;
       TileShape s = tile_shape(d.tcfg);
       return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * 16.0 * d.NG / s.wk;
     }
     case DK_SEP:
-      return 16.0 * d.CinP * (d.sep_k * d.sep_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
+      if (d.sep_row) return 16.0 * d.CinP * (d.row_k * d.row_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
+      return (double)d.sep_bm * d.CinP * (d.kh * d.kw + 16.0 * d.sep_nbt) / kWaves;
     default:
       return (double)kEltPerTile * (d.kind <= DK_POOL_AVG ? d.kh * d.kw : d.n_in) / 4.0;
   }
@@ -168,6 +171,44 @@ void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::v
           }
   *ng = groups;
   *nb = blocks;
+}
+
+void pack_conv_pipe(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out, int *nkb) {
+  const int taps = kh * kw, K = taps * cin, ldw = round_up(cout, 128), nb = cdiv(K, kPipeKB);
+  out.assign((size_t)nb * kPipeKB * ldw, 0.f);
+  for (int n = 0; n < cout; ++n)
+    for (int c = 0; c < cin; ++c)
+      for (int t = 0; t < taps; ++t) out[((size_t)t * cin + c) * ldw + n] = w[((size_t)n * cin + c) * taps + t];
+  *nkb = nb;
+}
+
+SepGeom sep_geometry(int tile, int cin, int cout, int w, int ho, int wo, int kh, int kw) {
+  SepGeom g;
+  const int cinp = round_up(cin, 16), nb = round_up(cout, 16) / 16;
+  for (int bm = 16 << std::max(0, std::min(tile, kSepStagedTiles - 1)); bm >= 16; bm >>= 1) {
+    // rows of the image a run of bm consecutive output pixels can touch,
+    // plus the window's halo
+    const int span = std::min(ho, (wo - 1 + bm - 1) / wo + 1);
+    const int rows = span + kh - 1;
+    const int mb = bm / 16;
+    // the largest chunk (a multiple of 16 channels) whose staging fits the
+    // registers and LDS, then the same number of chunks made even; output
+    // channels split into groups of at most nbt blocks so that a wave has at
+    // most kSepPairs pairs and a chunk's pointwise weights fit the registers
+    for (int ck = std::min(kSepMaxCk, cinp); ck >= 16; ck -= 16) {
+      if (ck * rows * w > kSepStagePerThread * kThreads || ck * kh * kw > kSepDwPerThread * kThreads) continue;
+      int nbt = std::min({nb, kSepPairs * kWaves / mb, kSepAPerThread * kThreads / 64 / (ck / 16)});
+      if (nbt < 1) continue;
+      nbt = cdiv(nb, cdiv(nb, nbt));                 // balance the channel groups
+      if (sep_lds_floats(bm, ck, rows, w, kh * kw, nbt) * (int)sizeof(float) > kSepMaxLds) continue;
+      const int nck = cdiv(cinp, ck);
+      const int cke = round_up(cdiv(cinp, nck), 16);
+      g.bm = bm; g.ck = cke; g.rows = rows; g.nck = nck; g.nbt = nbt;
+      g.lds = sep_lds_floats(bm, cke, rows, w, kh * kw, nbt) * (int)sizeof(float);
+      return g;
+    }
+  }
+  return g;
 }
 
 void free_stage(CompiledStage *cs) {
@@ -229,15 +270,21 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       set_route(g, d, (int)r, n0, o.out, sm);
       n0 += o.d.cout;
     }
-    int nb = 0;
-    pack_conv_weights(wm.data(), total, o0.cin, KH, KW, mw, &d.NG, &nb);
-    d.Npad = nb * 16;
     // tile shape: forced one, else the measured choice of the largest conv
     int largest = ops[0];
     for (int i : ops)
       if (op_flops(g, g->ops[i]) > op_flops(g, g->ops[largest])) largest = i;
     d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total)
                                            : g->ops[largest].tcfg;
+    int nb = 0;
+    if (tile_is_pipe(d.tcfg)) {
+      pack_conv_pipe(wm.data(), total, o0.cin, KH, KW, mw, &d.NG);
+      d.pipe_ldw = round_up(total, 128);
+      d.Npad = round_up(total, 16);
+    } else {
+      pack_conv_weights(wm.data(), total, o0.cin, KH, KW, mw, &d.NG, &nb);
+      d.Npad = nb * 16;
+    }
     set_inputs(g, o0, d, sm);
     d.route_n0[d.n_routes] = total;
     d.w_bytes = (int32_t)(mw.size() * sizeof(float));
@@ -254,20 +301,43 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.route_n0[1] = d.Cout;
       switch (o.d.kind) {
         case IOS_CONV:
-          d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad; d.NG = o.NG;
-          d.wpk = o.d_wpk; d.bias = o.d_bias;
-          d.w_bytes = (int32_t)((size_t)(o.Npad / 16) * o.NG * 256 * sizeof(float));
+          d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad;
+          d.bias = o.d_bias;
+          if (tile_is_pipe(o.tcfg)) {
+            d.NG = o.pipe_nkb;
+            d.pipe_ldw = round_up(o.d.cout, 128);
+            d.wpk = o.d_wg;
+            d.w_bytes = (int32_t)((size_t)o.pipe_nkb * kPipeKB * d.pipe_ldw * sizeof(float));
+          } else {
+            d.NG = o.NG;
+            d.wpk = o.d_wpk;
+            d.w_bytes = (int32_t)((size_t)(o.Npad / 16) * o.NG * 256 * sizeof(float));
+          }
           break;
-        case IOS_SEPCONV:
-          d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad;
+        case IOS_SEPCONV: {
+          if (o.sep_tile >= kSepStagedTiles) {
+            // row tile (see the stage kernel)
+            if (!sep_tile_ok(o, o.sep_tile)) fail(IOS_E_UNSUPPORTED, "SEPCONV row tile does not apply");
+            d.kind = DK_SEP; d.sep_row = 1;
+            d.CinP = round_up(o.cin, 4); d.Npad = o.Npad;
+            d.wpk = o.d_pw_row; d.bias = o.d_bias; d.dw = o.d_dw_row;
+            d.w_bytes = (int32_t)((size_t)d.CinP * o.Npad * sizeof(float));
+            d.row_k = sep_row_window(o.d.kh, o.d.kw);
+            d.sep_nbt = o.sep_tile - kSepStagedTiles + 1;
+            d.dw_bytes = (int32_t)((size_t)d.CinP * sep_kkp(d.row_k) * sizeof(float));
+            break;
+          }
+          d.kind = DK_SEP; d.CinP = o.CinP; d.Npad = o.Npad; d.NG = o.NG;
           d.wpk = o.d_wpk; d.bias = o.d_bias; d.dw = o.d_dw;
-          d.w_bytes = (int32_t)((size_t)o.CinP * o.Npad * sizeof(float));
-          d.sep_k = sep_window(o.d.kh, o.d.kw);
-          d.sep_nbt = std::min(o.sep_nbt, o.Npad / 16);
-          d.dw_bytes = (int32_t)((size_t)o.CinP * sep_kkp(d.sep_k) * sizeof(float));
-          if (sep_lds_bytes(d.CinP, d.sep_k, d.sep_nbt) > kSepMaxLds)
-            fail(IOS_E_UNSUPPORTED, "SEPCONV tile exceeds its LDS budget");
+          d.w_bytes = (int32_t)((size_t)(o.Npad / 16) * o.NG * 256 * sizeof(float));
+          d.dw_bytes = (int32_t)((size_t)o.CinP * o.d.kh * o.d.kw * sizeof(float));
+          const SepGeom sg = sep_geometry(o.sep_tile, o.cin, o.d.cout, o.wd, o.ho, o.wo, o.d.kh, o.d.kw);
+          if (sg.bm == 0) fail(IOS_E_UNSUPPORTED, "SEPCONV tile does not fit");
+          d.sep_bm = sg.bm;
+          d.sep_lbm = 31 - __builtin_clz((unsigned)sg.bm);
+          d.sep_ck = sg.ck; d.sep_nck = sg.nck; d.sep_rows = sg.rows; d.sep_nbt = sg.nbt;
           break;
+        }
         case IOS_POOL_MAX: d.kind = DK_POOL_MAX; break;
         case IOS_POOL_AVG: d.kind = DK_POOL_AVG; break;
         case IOS_ADD: d.kind = DK_ADD; break;
@@ -299,11 +369,17 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     if (d.kind == DK_CONV) {
       d.tiles_m = cdiv(M, tile_bm(d.tcfg));
       d.tiles_n = cdiv(d.Cout, tile_bn(d.tcfg));
-    } else if (d.kind == DK_SEP) {
-      // tiles: (image, output row, 16-pixel block of the row) x groups of
+    } else if (d.kind == DK_SEP && d.sep_row) {
+      // row tile: (image, output row, 16-pixel block of the row) x groups of
       // sep_nbt 16-channel output blocks
-      d.sep_bpr = cdiv(d.Wo, 16);
-      d.tiles_m = d.N * d.Ho * d.sep_bpr;
+      d.row_bpr = cdiv(d.Wo, 16);
+      d.tiles_m = d.N * d.Ho * d.row_bpr;
+      d.tiles_n = cdiv(d.Npad / 16, d.sep_nbt);
+    } else if (d.kind == DK_SEP) {
+      // tiles: (image, run of sep_bm output pixels) x groups of sep_nbt
+      // 16-channel output blocks
+      d.tiles_per_plane = cdiv((int64_t)d.Ho * d.Wo, d.sep_bm);
+      d.tiles_m = d.N * d.tiles_per_plane;
       d.tiles_n = cdiv(d.Npad / 16, d.sep_nbt);
     } else if (d.kind == DK_POOL_MAX || d.kind == DK_POOL_AVG) {
       // output rows per tile: as many as fit (with halo) in the LDS budget
@@ -351,8 +427,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.fd_wo = fd(d.Wo);
     d.fd_spt = fd(d.CinP / 4);
     d.fd_kw = fd(d.kw);
-    d.fd_pimg = fd(d.Ho * d.sep_bpr);
-    d.fd_bpr = fd(d.sep_bpr);
+    d.fd_pimg = fd(d.kind == DK_SEP && d.sep_row ? d.Ho * d.row_bpr : d.tiles_per_plane);
+    d.fd_rbpr = fd(d.row_bpr);
+    d.fd_cin = fd(d.Cin);
+    d.fd_rw = fd(d.sep_rows * d.W);
+    d.fd_w = fd(d.W);
     d.fd_tpp = fd(d.tiles_per_plane);
     d.fd_c = fd(d.Cout);
     d.fd_pin = fd(d.pool_in_rows * d.W);
@@ -374,7 +453,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   for (int i = 0; i < n; ++i) pos[order[i]] = i;
   std::vector<DevOp> sorted;
   std::vector<int32_t> start{0};
-  bool persistent = false, big_conv = false, has_sep = false;
+  bool persistent = false, big_conv = false, has_sep = false, has_row = false, has_pipe = false;
   int lds = 0;
   for (int i : order) {
     DevOp d = dops[i];
@@ -382,8 +461,10 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     sorted.push_back(d);
     start.push_back(start.back() + d.n_tiles);
     persistent |= d.n_deps > 0;
-    big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg);
-    has_sep |= d.kind == DK_SEP;
+    big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg) && !tile_is_pipe(d.tcfg);
+    has_pipe |= d.kind == DK_CONV && tile_is_pipe(d.tcfg);
+    has_sep |= d.kind == DK_SEP && !d.sep_row;
+    has_row |= d.kind == DK_SEP && d.sep_row;
     lds = std::max(lds, op_lds_bytes(d));
   }
   cs->ops = sorted;
@@ -395,7 +476,12 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   cs->lds_bytes = (kSlotWords + table_words) * (int)sizeof(int32_t) + lds;
   if (cs->lds_bytes > kMaxLdsBytes) fail(IOS_E_UNSUPPORTED, "stage needs more LDS than a workgroup has");
   cs->persistent = persistent;
-  cs->variant = big_conv ? KV_FULL : has_sep ? KV_SEP : KV_LIGHT;
+  const int kinds = (int)has_sep + (int)has_row + (int)has_pipe;
+  cs->variant = big_conv || kinds > 1 ? KV_FULL
+                : has_sep            ? KV_SEP
+                : has_row            ? KV_SEPROW
+                : has_pipe           ? KV_PIPE
+                                     : KV_LIGHT;
   cs->grid = start.back();
   if (persistent) {
     int cap = stage_capacity(cs->variant, cs->lds_bytes);

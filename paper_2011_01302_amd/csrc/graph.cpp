@@ -127,10 +127,11 @@ int add_op(ios_graph *g, const ios_op_desc *d, const int32_t *in_ids, int n_in,
         op.w.assign(weights, weights + nw);
         op.b.assign((size_t)d->cout, 0.f);
         if (bias) std::memcpy(op.b.data(), bias, sizeof(float) * d->cout);
-        if (kind == IOS_SEPCONV && t0.c > kMaxChannels)
-          fail(IOS_E_UNSUPPORTED, "SEPCONV supports at most 256 input channels");
-        if (kind == IOS_SEPCONV && sep_window(d->kh, d->kw) == 0)
-          fail(IOS_E_UNSUPPORTED, "SEPCONV depthwise window larger than 5x5");
+        if (kind == IOS_SEPCONV && (d->kh > kSepMaxWindow || d->kw > kSepMaxWindow))
+          fail(IOS_E_UNSUPPORTED, "SEPCONV depthwise window larger than 7x7");
+        if (kind == IOS_SEPCONV && sep_geometry(0, t0.c, d->cout, t0.w, oh, ow, d->kh, d->kw).bm == 0)
+          fail(IOS_E_UNSUPPORTED, "SEPCONV input rows too wide for the staged tile");
+        // (the row tile is an alternative where it applies, never the only one)
       }
       break;
     }
@@ -353,19 +354,23 @@ static T *upload(const std::vector<T> &v) {
   return p;
 }
 
-// Largest number of 16-channel output blocks a SEPCONV tile can take (LDS).
-int max_sep_nbt(const Op &op) {
-  const int K = sep_window(op.d.kh, op.d.kw);
-  int n = std::min(kSepMaxNB, op.Npad / 16);
-  while (n > 1 && sep_lds_bytes(op.CinP, K, n) > kSepMaxLds) --n;
-  return n;
+bool sep_tile_ok(const Op &op, int tile) {
+  if (tile < 0 || tile >= kSepTiles) return false;
+  if (tile < kSepStagedTiles)
+    return sep_geometry(tile, op.cin, op.d.cout, op.wd, op.ho, op.wo, op.d.kh, op.d.kw).bm == (16 << tile);
+  const int K = sep_row_window(op.d.kh, op.d.kw), nbt = tile - kSepStagedTiles + 1;
+  return K != 0 && op.cin <= kSepRowMaxChannels && nbt <= round_up(op.d.cout, 16) / 16 &&
+         sep_row_lds_bytes(round_up(op.cin, 4), K, nbt) <= kSepMaxLds;
 }
 
-// Output blocks per SEPCONV tile before measurement (IOS_SEP_NBT forces it).
-static int choose_sep_nbt(const Op &op) {
-  int v = 2;
-  if (const char *e = std::getenv("IOS_SEP_NBT")) v = std::atoi(e);
-  return std::max(1, std::min(v, max_sep_nbt(op)));
+// SEPCONV tile choice before measurement (IOS_SEP_TILE=<0..6> forces one;
+// a choice the operator cannot use falls back to the staged tile of 16
+// pixels).
+static int choose_sep_tile(const Op &op) {
+  int v = 1;
+  if (const char *e = std::getenv("IOS_SEP_TILE")) v = std::atoi(e);
+  v = std::max(0, std::min(v, kSepTiles - 1));
+  return sep_tile_ok(op, v) ? v : 0;
 }
 
 // Conv tile shape for an M x N output before measurement.  IOS_CONV_TILE=<0..5>
@@ -403,9 +408,9 @@ void finalize_graph(ios_graph *g) {
       op.Npad = round_up(op.d.cout, 16);
       op.tcfg = choose_conv_tile((int64_t)g->batch * op.ho * op.wo, op.d.cout);
     } else if (op.d.kind == IOS_SEPCONV) {
-      op.CinP = round_up(op.cin, 4);
+      op.CinP = round_up(op.cin, 16);
       op.Npad = round_up(op.d.cout, 16);
-      op.sep_nbt = choose_sep_nbt(op);
+      op.sep_tile = choose_sep_tile(op);
     }
   }
   g->cost_table.assign(g->blocks.size(), {});
@@ -440,24 +445,38 @@ void ensure_device(ios_graph *g) {
       std::copy(op.b.begin(), op.b.end(), bias.begin());
       op.d_wpk = upload(wpk);
       op.d_bias = upload(bias);
+      std::vector<float> wg;
+      pack_conv_pipe(op.w.data(), op.d.cout, op.cin, op.d.kh, op.d.kw, wg, &op.pipe_nkb);
+      op.d_wg = upload(wg);
     } else if (op.d.kind == IOS_SEPCONV) {
-      // depthwise taps at the top left of a K x K window (the rest zero),
-      // KKP floats per channel, channels past cin zero
-      const int taps = op.d.kh * op.d.kw, K = sep_window(op.d.kh, op.d.kw), kkp = sep_kkp(K);
-      std::vector<float> dw((size_t)op.CinP * kkp, 0.f);
-      for (int c = 0; c < op.cin; ++c)
-        for (int u = 0; u < op.d.kh; ++u)
-          for (int v = 0; v < op.d.kw; ++v)
-            dw[(size_t)c * kkp + u * K + v] = op.w[(size_t)c * taps + u * op.d.kw + v];
-      std::vector<float> pw((size_t)op.CinP * op.Npad, 0.f);
-      const float *src = op.w.data() + (size_t)op.cin * taps;
-      for (int co = 0; co < op.d.cout; ++co)
-        for (int ci = 0; ci < op.cin; ++ci) pw[(size_t)ci * op.Npad + co] = src[(size_t)co * op.cin + ci];
-      std::vector<float> bias(op.Npad, 0.f);
+      // depthwise [CinP][kh * kw] (channels past cin zero); pointwise packed
+      // like a 1x1 conv's weights (groups of 4 k-steps = 16 input channels)
+      const int taps = op.d.kh * op.d.kw;
+      std::vector<float> dw((size_t)op.CinP * taps, 0.f);
+      std::copy(op.w.begin(), op.w.begin() + (size_t)op.cin * taps, dw.begin());
+      std::vector<float> pwk, bias(op.Npad, 0.f);
+      int nb = 0;
+      pack_conv_weights(op.w.data() + (size_t)op.cin * taps, op.d.cout, op.cin, 1, 1, pwk, &op.NG, &nb);
       std::copy(op.b.begin(), op.b.end(), bias.begin());
       op.d_dw = upload(dw);
-      op.d_wpk = upload(pw);
+      op.d_wpk = upload(pwk);
       op.d_bias = upload(bias);
+      // the row tile's layouts, where it applies: depthwise taps at the top
+      // left of a K x K window, [CinP4][kkp(K)]; pointwise [CinP4][Npad]
+      const int K = sep_row_window(op.d.kh, op.d.kw);
+      if (K != 0 && op.cin <= kSepRowMaxChannels) {
+        const int cp4 = round_up(op.cin, 4), kkp = sep_kkp(K);
+        std::vector<float> dwr((size_t)cp4 * kkp, 0.f), pwr((size_t)cp4 * op.Npad, 0.f);
+        for (int c = 0; c < op.cin; ++c)
+          for (int u = 0; u < op.d.kh; ++u)
+            for (int v = 0; v < op.d.kw; ++v)
+              dwr[(size_t)c * kkp + u * K + v] = op.w[(size_t)c * taps + u * op.d.kw + v];
+        const float *pw = op.w.data() + (size_t)op.cin * taps;
+        for (int co = 0; co < op.d.cout; ++co)
+          for (int ci = 0; ci < op.cin; ++ci) pwr[(size_t)ci * op.Npad + co] = pw[(size_t)co * op.cin + ci];
+        op.d_dw_row = upload(dwr);
+        op.d_pw_row = upload(pwr);
+      }
     }
   }
   hip_check(hipDeviceSynchronize(), "hipDeviceSynchronize");
@@ -475,7 +494,7 @@ void ensure_device(ios_graph *g) {
   }
   g->noalloc_bytes = off;
   g->device_ready = true;
-  const bool tune_conv = !std::getenv("IOS_CONV_TILE"), tune_sep = !std::getenv("IOS_SEP_NBT");
+  const bool tune_conv = !std::getenv("IOS_CONV_TILE"), tune_sep = !std::getenv("IOS_SEP_TILE");
   if ((tune_conv || tune_sep) && !g->units.empty()) {
     // keep the GPU busy for a while first, so that the measurements below
     // are taken at the clocks the stages will run at
@@ -511,19 +530,20 @@ void ensure_device(ios_graph *g) {
       op.tcfg = best;
     }
   }
-  // Output blocks per SEPCONV tile, likewise measured (unless IOS_SEP_NBT).
+  // SEPCONV tile choice, likewise measured (unless IOS_SEP_TILE forces it).
   if (tune_sep) {
     for (int oi : g->units) {
       Op &op = g->ops[oi];
       if (op.d.kind != IOS_SEPCONV) continue;
-      int best = op.sep_nbt;
+      int best = op.sep_tile;
       int64_t best_ns = INT64_MAX;
-      for (int nbt = 1; nbt <= max_sep_nbt(op); ++nbt) {
-        op.sep_nbt = nbt;
+      for (int t = 0; t < kSepTiles; ++t) {
+        if (!sep_tile_ok(op, t)) continue;
+        op.sep_tile = t;
         int64_t ns = profile_stage(g, {oi}, IOS_CONCURRENT, 2, 10, 3);
-        if (ns < best_ns) { best_ns = ns; best = nbt; }
+        if (ns < best_ns) { best_ns = ns; best = t; }
       }
-      op.sep_nbt = best;
+      op.sep_tile = best;
     }
   }
 }

@@ -27,7 +27,6 @@ constexpr int kMaxStageOps = 64;  // operators of one stage (a block holds at mo
 constexpr int kCtrCopies = 32;
 constexpr int kCtrStride = 64;    // >= kMaxStageOps
 constexpr int kMaxUnitsPerBlock = 64;
-constexpr int kMaxChannels = 256; // SEPCONV input channels (8 waves x 8 k-steps of 4)
 constexpr int64_t kInf = INT64_MAX;
 // Device array that ios_run_noalloc uses for the intermediates and the
 // in-stage counters (one per device, held until the process ends).
@@ -52,7 +51,12 @@ enum TileCfg : int32_t {
   TC_32x64_K4 = 3,   // FM2 FN2 WM1 WN2 WK4
   TC_64x64_K2 = 4,   // FM2 FN2 WM2 WN2 WK2
   TC_128x64 = 5,     // FM2 FN2 WM4 WN2 WK1
-  TC_COUNT = 6,
+  // pipelined tiles (see the stage kernel): 8 waves of 32x32 outputs on
+  // v_mfma_f32_32x32x2_f32, operands staged in LDS by direct loads
+  TC_P128x64 = 6,    // 4 (pixels) x 2 (channels) waves
+  TC_P256x32 = 7,    // 8 x 1
+  TC_P64x128 = 8,    // 2 x 4
+  TC_COUNT = 9,
 };
 static_assert(TC_COUNT == IOS_CONV_TILE_SHAPES, "tile shapes of the public API");
 
@@ -69,30 +73,81 @@ inline TileShape tile_shape(int cfg) {
 }
 // Tile shapes the light kernel variant contains (one 16-pixel block per wave).
 inline bool tile_is_light(int cfg) { return cfg == TC_16x16_K8 || cfg == TC_16x32_K8; }
-inline int tile_bm(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fm * s.wm; }
-inline int tile_bn(int cfg) { TileShape s = tile_shape(cfg); return 16 * s.fn * s.wn; }
+inline bool tile_is_pipe(int cfg) { return cfg >= TC_P128x64 && cfg < TC_COUNT; }
+// pipelined tiles: waves along pixels and along channels
+inline int pipe_wm(int cfg) { return cfg == TC_P128x64 ? 4 : cfg == TC_P256x32 ? 8 : 2; }
+inline int tile_bm(int cfg) {
+  if (tile_is_pipe(cfg)) return 32 * pipe_wm(cfg);
+  TileShape s = tile_shape(cfg);
+  return 16 * s.fm * s.wm;
+}
+inline int tile_bn(int cfg) {
+  if (tile_is_pipe(cfg)) return 32 * (kWaves / pipe_wm(cfg));
+  TileShape s = tile_shape(cfg);
+  return 16 * s.fn * s.wn;
+}
+// Pipelined tiles: reduction blocks of kPipeKB (tap, channel) pairs, a ring of
+// kPipeStages blocks of both operands in LDS; weights packed [k][round128(Cout)]
+// with k = (u kw + v) Cin + c, zero past K and Cout.
+constexpr int kPipeKB = 16;
+constexpr int kPipeStages = 5;
+inline int pipe_lds_bytes(int cfg) {
+  return kPipeStages * kPipeKB * (tile_bm(cfg) + tile_bn(cfg)) * (int)sizeof(float);
+}
 
-// SEPCONV tile: 16 output pixels of one output row x sep_nbt blocks of 16
-// output channels (sep_nbt <= kSepMaxNB).  The depthwise window is padded to
-// K x K, K = 3 or 5 (sep_k); its weights are packed [CinP][sep_kkp(K)].
-constexpr int kSepMaxNB = 4;
-constexpr int kSepMaxLds = 64 * 1024;   // bytes of LDS one SEPCONV tile may use
-inline int sep_window(int kh, int kw) {
+// SEPCONV tile: BM = 16 << tile consecutive output pixels of one image x
+// sep_nbt blocks of 16 output channels; the input channels are reduced in
+// chunks of sep_ck (32 or 16), whose input rows (with the window's halo) are
+// staged in LDS.  The shape follows from the tile choice and the operator's
+// sizes (sep_geometry), within these limits.
+// Tile choices: 0 .. kSepStagedTiles - 1 the staged tile (BM = 16 << choice),
+// then kSepRowMaxNB choices of the row tile (16 output pixels of one output
+// row x 1 .. kSepRowMaxNB channel blocks; Cin <= 256, windows up to 5 x 5).
+constexpr int kSepStagedTiles = 3;       // BM = 16, 32, 64
+constexpr int kSepRowMaxNB = 4;
+constexpr int kSepTiles = kSepStagedTiles + kSepRowMaxNB;
+constexpr int kSepRowMaxChannels = 256;
+constexpr int kSepPairs = 4;             // (pixel block, channel block) pairs per wave at most
+constexpr int kSepStagePerThread = 8;   // staged input floats per thread and chunk at most
+constexpr int kSepMaxLds = 64 * 1024;    // bytes of LDS one SEPCONV tile may use
+constexpr int kSepMaxWindow = 7;         // depthwise windows up to 7 x 7
+constexpr int kSepMaxCk = 64;            // input channels per chunk at most
+constexpr int kSepDwPerThread = 4;       // depthwise weights per thread and chunk at most
+constexpr int kSepAPerThread = 2;        // 16-byte pointwise weight loads per thread and chunk at most
+struct SepGeom {
+  int bm = 0, ck = 0, rows = 0, nck = 0, nbt = 0, lds = 0;
+};
+// Tile geometry of a SEPCONV for tile choice `tile` (BM = 16 << tile, lowered
+// until the staging fits); bm = 0 if nothing fits.
+SepGeom sep_geometry(int tile, int cin, int cout, int w, int ho, int wo, int kh, int kw);
+// Whether SEPCONV tile choice `tile` can run `op` (graph.cpp).
+struct Op;
+bool sep_tile_ok(const Op &op, int tile);
+__host__ __device__ inline int sep_pitch(int bm) { return (bm & 31) == 16 ? bm : bm + 16; }
+// Row tile: the depthwise window padded to K x K, K = 3 or 5 (0 = too
+// large); its weights packed [CinP][sep_kkp(K)].
+inline int sep_row_window(int kh, int kw) {
   int k = kh > kw ? kh : kw;
   return k <= 3 ? 3 : k <= 5 ? 5 : 0;
 }
 __host__ __device__ inline int sep_kkp(int K) { return (K * K + 3) & ~3; }
-// LDS of one wave of a SEPCONV tile (floats, a multiple of 64): depthwise and
+// LDS of one wave of a row tile (floats, a multiple of 64): depthwise and
 // pointwise weights of its k-steps, plus 64 floats so that no 64-lane copy
 // can reach the next wave's region; the tile's LDS also holds the
 // [wave][16 nbt columns][17] partial sums afterwards.
-__host__ __device__ inline int sep_wave_floats(int CinP, int K, int nbt) {
+__host__ __device__ inline int sep_row_wave_floats(int CinP, int K, int nbt) {
   const int ksw = (CinP / 4 + 7) / 8;
   return ((ksw * 4 * (sep_kkp(K) + 16 * nbt) + 63) & ~63) + 64;
 }
-__host__ __device__ inline int sep_lds_bytes(int CinP, int K, int nbt) {
-  const int w = 8 * sep_wave_floats(CinP, K, nbt), r = 8 * kSepMaxNB * 16 * 17;
+__host__ __device__ inline int sep_row_lds_bytes(int CinP, int K, int nbt) {
+  const int w = 8 * sep_row_wave_floats(CinP, K, nbt), r = 8 * kSepRowMaxNB * 16 * 17;
   return (w > r ? w : r) * 4;
+}
+// LDS of a SEPCONV tile in floats: the staged input and depthwise weights of
+// one chunk, two pointwise weight buffers, the depthwise outputs and the
+// tile's biases (whole copies of 64 floats).
+__host__ __device__ inline int sep_lds_floats(int bm, int ck, int rows, int w, int kk, int nbt) {
+  return ck * rows * w + ck * kk + 2 * nbt * (ck / 16) * 256 + ck * sep_pitch(bm) + (nbt * 16 + 63) / 64 * 64;
 }
 // Elementwise tiles: add / mean handle up to kEltPerTile contiguous outputs of
 // one channel plane; a pool tile handles a band of output rows of one plane
@@ -124,9 +179,9 @@ struct alignas(16) DevOp {
   int32_t Cout, Ho, Wo;        // output
   int32_t kh, kw, sh, sw, ph, pw;
   int32_t pre_relu, post_relu;
-  int32_t CinP;                // Cin rounded up to 4 (reduction per tap)
-  int32_t Npad;                // SEP: row length of the pointwise weights; CONV: 16 x blocks
-  int32_t NG;                  // CONV: groups of 4 k-steps (K = taps x CinP = 16 NG, padded)
+  int32_t CinP;                // CONV: Cin rounded up to 4 (reduction per tap); SEP: up to 16
+  int32_t Npad;                // Cout rounded up to 16
+  int32_t NG;                  // groups of 4 k-steps of the packed weights (CONV: K = taps x CinP; SEP: pointwise)
   int32_t tiles_m, tiles_n, n_tiles;
   int32_t n_routes;            // output column ranges -> destination buffers
   int32_t route_n0[kMaxRoutes + 1];
@@ -139,21 +194,27 @@ struct alignas(16) DevOp {
   int32_t tiles_per_plane;     // POOL / ADD / MEAN: tiles per (image, channel) plane
   int32_t planes_per_tile;     // POOL: whole planes per tile when a plane is small (else 1)
   int32_t pool_in_rows;        // POOL with planes_per_tile > 1: input rows staged per plane
-  int32_t sep_k;               // SEP: depthwise window K (3, 5 or 7)
+  int32_t sep_bm, sep_lbm;     // SEP: output pixels per tile, log2
+  int32_t sep_ck, sep_nck;     // SEP: input channels per chunk, chunks
+  int32_t sep_rows;            // SEP: input rows staged per chunk
   int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
-  int32_t sep_bpr;             // SEP: 16-pixel blocks per output row
+  int32_t sep_row;             // SEP: 1 = row tile, 0 = staged tile
+  int32_t row_k, row_bpr;      // SEP row tile: padded window K, 16-pixel blocks per output row
+  int32_t pipe_ldw;            // CONV pipelined tile: row length of the packed weights (NG = k-blocks)
   int32_t w_bytes;             // size of wpk in bytes
   int32_t dw_bytes;            // SEP: size of dw in bytes
   // divisors of the tile and pixel decompositions (see FDiv)
   FDiv fd_tn;                  // tiles_n
   FDiv fd_howo, fd_wo;         // Ho * Wo, Wo
   FDiv fd_spt, fd_kw;          // CONV: k-steps per tap, kw
-  FDiv fd_pimg, fd_bpr;        // SEP: 16-pixel blocks per image, per row
+  FDiv fd_pimg, fd_rw, fd_w;   // SEP: pixel tiles (row tile: 16-pixel blocks) per image, staged floats per channel, W
+  FDiv fd_rbpr;                // SEP row tile: 16-pixel blocks per row
+  FDiv fd_cin;                 // CONV pipelined tile: Cin
   FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
   FDiv fd_pin;                 // POOL with planes_per_tile > 1: floats staged per plane
-  const float *wpk;            // CONV: see pack_conv_weights; SEP: pointwise [CinP][Npad]
+  const float *wpk;            // CONV: see pack_conv_weights; SEP: the pointwise weights packed the same way
   const float *bias;           // [Npad]
-  const float *dw;             // SEP: depthwise [CinP][sep_kkp(K)], kh x kw taps at the top left of K x K
+  const float *dw;             // SEP: depthwise [round16(Cin)][kh * kw], channels past Cin zero
 };
 
 // A compiled stage's table in device memory (int32 words): a header
@@ -179,7 +240,7 @@ struct StageArgs {
 // Launch one stage (defined in the HIP translation unit).
 // Kernel variant of a stage (see the stage kernel): the smallest one that
 // contains every tile kind the stage uses.
-enum KernelVariant { KV_LIGHT = 0, KV_SEP = 1, KV_FULL = 2 };
+enum KernelVariant { KV_LIGHT = 0, KV_SEP = 1, KV_FULL = 2, KV_SEPROW = 3, KV_PIPE = 4, KV_COUNT = 5 };
 // table / table_words: the compiled stage's table (a multiple of 4 words);
 // lds_bytes: the dynamic LDS, slots and table included.
 hipError_t launch_stage(const int32_t *table, int table_words, const StageArgs &args, bool persistent,
@@ -221,9 +282,12 @@ struct Op {
   int cin = 0, h = 0, wd = 0, ho = 0, wo = 0;
   // device copies (units only)
   int CinP = 0, Npad = 0, NG = 0, tcfg = TC_16x32_K8;
-  int sep_nbt = 1;               // SEPCONV: output blocks of 16 channels per tile
+  int sep_tile = 1;              // SEPCONV: tile choice (16 << sep_tile output pixels per tile)
   int xcd_lg = -1;               // XCD run length 2^xcd_lg of the stage holding it; -1: modelled
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
+  float *d_dw_row = nullptr, *d_pw_row = nullptr;   // SEPCONV row tile: [CinP4][kkp(K)], [CinP4][Npad]
+  float *d_wg = nullptr;         // CONV, pipelined tiles: [nkb * kPipeKB][round128(Cout)]
+  int pipe_nkb = 0;
 };
 
 struct Block {
@@ -320,12 +384,14 @@ int64_t op_flops(const ios_graph *g, const Op &op);
 // channels.  Sets *ng = groups, *nb = blocks.
 void pack_conv_weights(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out,
                        int *ng, int *nb);
+// Conv weights for the pipelined tiles: [nkb * kPipeKB][round128(cout)], row
+// k = (u kw + v) cin + c, zero past the kernel and past cout.
+void pack_conv_pipe(const float *w, int cout, int cin, int kh, int kw, std::vector<float> &out, int *nkb);
 void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, CompiledStage *cs,
                    bool reuse);
 void free_stage(CompiledStage *cs);
 void launch_compiled(ios_graph *g, const CompiledStage &cs, const std::vector<float *> &buf_ptr,
                      hipStream_t stream);
-int max_sep_nbt(const Op &op);
 int64_t profile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, int warmup,
                       int reps, int repeats);
 std::vector<float *> default_buffers(const ios_graph *g);

@@ -330,7 +330,399 @@ __device__ __forceinline__ void conv_tile(const Slots &sl, const DevOp &op, cons
   }
 }
 
+// ------------------------------------------------------------------ pipelined conv
+
+// Direct global -> LDS load of one float per lane: lane i of the wave writes
+// l[i] (l the same for every lane), through no register.  The compiler does
+// not see this write: readers wait for vmcnt(0) (and a barrier) first.
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float *l, int voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)l, 4, voff, 0, 0, 0);
+}
+
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ floatx16 mfma32x32x2(float a, float b, floatx16 c) {
+  // D[32x32] += A[32x2] * B[2x32]; lane l supplies A[l%32][l/32] and
+  // B[l/32][l%32]; lane l, element r holds D[8 (r/4) + 4 (l/32) + r%4][l%32].
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// s_waitcnt with vmcnt = N (gfx9 encoding, see kWaitVmcnt0), other counters free.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+template <int MAX>
+__device__ __forceinline__ void wait_vmcnt_upto(int n) {   // n <= MAX, uniform
+  if constexpr (MAX > 0) {
+    if (n >= MAX) { wait_vmcnt<MAX>(); return; }
+    wait_vmcnt_upto<MAX - 1>(n);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+// Implicit-GEMM convolution tile with both operands staged in LDS through a
+// pipeline of direct global -> LDS loads: BM = 32 WMW output pixels (over the
+// whole batch, flattened) x BN = 32 WNW output channels, 8 waves of one
+// 32x32 block each on v_mfma_f32_32x32x2_f32 (output channels as rows,
+// pixels as columns).  The reduction index k = (u kw + v) Cin + c runs in
+// blocks of KB = kPipeKB; a ring of kPipeStages block slots holds, per
+// block, the weights [KB][BN] (rows of the packed [k][n] matrix) and the
+// im2col'd input [KB][BM] (per lane: one pixel, the tap and channel of the
+// row; taps outside the image read 0).  kPipeStages - 1 blocks are in flight
+// while one is multiplied, so the loads' latency is hidden behind the MFMAs
+// of the blocks before them; one barrier per block.  The writes to LDS go
+// through no register and the compiler does not see them: every wave counts
+// its own loads (vmcnt) and the barrier publishes them.
+template <int WMW, bool COH>
+__device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, KB = kPipeKB, D = kPipeStages;
+  constexpr int HB = BM / 64;                        // 64-pixel segments of a row of the input block
+  constexpr int A_DMA = KB * BN / 64 / kWaves, B_DMA = KB * BM / 64 / kWaves, PER = A_DMA + B_DMA;
+  static_assert(A_DMA * 64 * kWaves == KB * BN && B_DMA * 64 * kWaves == KB * BM, "whole copies");
+  static_assert(B_DMA == 2 * HB, "each wave stages two rows of the input block");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % WMW, wn = wave / WMW;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo, H = o.H, W = o.W, HW = H * W;
+  const int Cin = o.Cin, kh = o.kh, kw = o.kw, K = Cin * kh * kw, nkb = o.NG, ldw = o.pipe_ldw;
+  float *aring = lds, *bring = lds + D * KB * BN;
+
+  // this lane's pixels of the input block (segment h: pixel m0 + 64 h + lane):
+  // offset of tap (0, 0) of channel 0, and the tap rows / columns in the image
+  int pbase[HB], rmask[HB], cmask[HB];
+#pragma unroll
+  for (int h = 0; h < HB; ++h) {
+    const int m = m0 + 64 * h + lane;
+    pbase[h] = 0; rmask[h] = 0; cmask[h] = 0;
+    if (m < M) {
+      const int img = fdiv(m, o.fd_howo), r = m - img * howo, oh = fdiv(r, o.fd_wo), ow = r - oh * Wo;
+      const int ih0 = oh * o.sh - o.ph, iw0 = ow * o.sw - o.pw;
+      pbase[h] = ((img * o.in_ctot[0] + o.in_coff[0]) * H + ih0) * W + iw0;
+      for (int u = 0; u < kh; ++u) rmask[h] |= (ih0 + u >= 0 && ih0 + u < H) << u;
+      for (int v = 0; v < kw; ++v) cmask[h] |= (iw0 + v >= 0 && iw0 + v < W) << v;
+    }
+  }
+  // biases of this lane's accumulator rows
+  float bias[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    bias[r] = n < o.Cout ? o.bias[n] : 0.f;
+  }
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
+
+  auto issue = [&](int kb) {
+    const int slot = kb % D;
+    float *a = aring + slot * KB * BN, *b = bring + slot * KB * BM;
+#pragma unroll
+    for (int i = 0; i < A_DMA; ++i) {
+      const int sg = wave * A_DMA + i, f = sg * 64 + lane, r = f / BN, col = f % BN;
+      lds_dma(wr, a + sg * 64, ((kb * KB + r) * ldw + n0 + col) * 4);
+    }
+#pragma unroll
+    for (int i = 0; i < B_DMA; ++i) {
+      const int r = 2 * wave + i / HB, h = i % HB;   // block row, 64-pixel segment
+      const int k = kb * KB + r;
+      const int tap = fdiv(k, o.fd_cin), c = k - tap * Cin, u = fdiv(tap, o.fd_kw), v = tap - u * kw;
+      const bool ok = k < K && ((rmask[h] >> u) & (cmask[h] >> v) & 1);
+      lds_dma(xr, b + r * BM + h * 64, ok ? (pbase[h] + c * HW + u * W + v) * 4 : kOOB);
+    }
+  };
+
+  floatx16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  const bool relu_in = o.pre_relu != 0;
+  for (int kb = 0; kb < D - 1 && kb < nkb; ++kb) issue(kb);
+  for (int kb = 0; kb < nkb; ++kb) {
+    // this wave's loads of block kb have landed once at most those of the
+    // blocks issued after it are in flight; the barrier makes every wave's
+    // visible and guarantees that block kb - 1's slot is no longer read
+    wait_vmcnt_upto<(D - 2) * PER>(min(D - 2, nkb - 1 - kb) * PER);
+    __syncthreads();
+    if (kb + D - 1 < nkb) issue(kb + D - 1);
+    const float *a = aring + (kb % D) * KB * BN + (lane >> 5) * BN + wn * 32 + (lane & 31);
+    const float *b = bring + (kb % D) * KB * BM + (lane >> 5) * BM + wm * 32 + (lane & 31);
+    float av[KB / 2], bv[KB / 2];
+#pragma unroll
+    for (int p = 0; p < KB / 2; ++p) {
+      av[p] = a[2 * p * BN];
+      bv[p] = b[2 * p * BM];
+    }
+#pragma unroll
+    for (int p = 0; p < KB / 2; ++p) acc = mfma32x32x2(av[p], relu_in ? fmaxf(bv[p], 0.f) : bv[p], acc);
+  }
+  // epilogue: element r of lane l is channel n0 + 32 wn + 8 (r/4) + 4 (l/32) + r%4 of pixel m0 + 32 wm + l%32
+  const int m = m0 + wm * 32 + (lane & 31);
+  if (m < M) {
+    const int img = fdiv(m, o.fd_howo), pix = m - img * howo;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (n < o.Cout) {
+        float v = acc[r] + bias[r];
+        if (o.post_relu) v = fmaxf(v, 0.f);
+        st<COH>(route_ptr(sl, op, o, n, img, pix, howo), v);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ sepconv
+
+// One depthwise output from staged rows: tap (u, v) at column iw0 + v of row
+// xrow + u W, columns outside the image counting zero.  Every LDS read of
+// the window (inputs and weights) is issued before the first product: one
+// LDS round trip per output.
+template <int KH, int KW>
+__device__ __forceinline__ float dw_point(const float *xrow, const float *w, int iw0, int W, float d = 0.f) {
+  float x[KH * KW], c[KH * KW];
+#pragma unroll
+  for (int u = 0; u < KH; ++u)
+#pragma unroll
+    for (int v = 0; v < KW; ++v) {
+      const int iw = iw0 + v;
+      const bool ok = iw >= 0 && iw < W;
+      x[u * KW + v] = xrow[u * W + (ok ? iw : 0)];
+      c[u * KW + v] = ok ? w[u * KW + v] : 0.f;
+    }
+#pragma unroll
+  for (int i = 0; i < KH * KW; ++i) d = fmaf(c[i], x[i], d);
+  return d;
+}
+
+// The pointwise MFMAs of one SEPCONV chunk for a wave with NP (pixel block,
+// channel block) pairs: per group of 4 k-steps, the NP A operands (16 bytes
+// per lane each) and the 4 B values are read from LDS together, then the
+// 4 NP MFMAs run (one LDS round trip per group, no branch between MFMAs).
+template <int NP>
+__device__ __forceinline__ void sep_mma(floatx4 *acc, const float *as, const float *bs, int c, int gpc, int NG,
+                                        int pitch, int wave, int MB, int mb, int lane) {
+  for (int gi = 0; gi < gpc; ++gi) {
+    if (c * gpc + gi >= NG) break;                   // uniform: a short last chunk
+    floatx4 a[NP];
+    float b[4];
+#pragma unroll
+    for (int r = 0; r < NP; ++r) a[r] = *(const floatx4 *)(as + (((wave + r * kWaves) / MB) * gpc + gi) * 256 + lane * 4);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) b[s] = bs[(gi * 16 + 4 * s + (lane >> 4)) * pitch + mb * 16 + (lane & 15)];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int r = 0; r < NP; ++r) acc[r] = mfma16x16x4(a[r][s], b[s], acc[r]);
+  }
+}
+
+// "Relu-SepConv" unit (Table 2): sum of the inputs -> ReLU -> depthwise
+// kh x kw (stride 1, no bias) -> pointwise 1x1 (+ bias), on BM = sep_bm
+// consecutive output pixels of one image (flattened, so a tile may span
+// image rows) x sep_nbt blocks of 16 output channels.  The reduction over
+// input channels runs in chunks of CK = sep_ck channels.  Everything a chunk
+// needs arrives in one batch of loads, issued while the previous chunk runs
+// on the MFMA units:
+//   - the input rows its pixels read (the window's halo included; rows
+//     outside the image staged as zeros) and its depthwise weights:
+//     coalesced loads to registers, stored to LDS once the previous chunk's
+//     MFMAs are issued (one LDS buffer: the previous chunk's depthwise pass
+//     has finished by then); the inputs after the first (a RandWire node's
+//     other producers) are loaded and added at that point, then the sum is
+//     ReLU'd;
+//   - its pointwise weights (packed like a 1x1 conv's: per 16-channel output
+//     block and group of 4 k-steps, 64 lanes x 4 floats): 16-byte loads to
+//     registers, then LDS (two buffers, as the MFMAs read the previous
+//     chunk's meanwhile).
+// Then
+//   dw      every (pixel, channel) of the chunk from LDS -> Bs[channel][pixel];
+//   mfma    output channels as MFMA rows, pixels as columns:
+//           D[16 ch][16 px] += A[16 ch][4 k] B[4 k][16 px], A and B both read
+//           from LDS.  Wave w owns the (pixel block, channel block) pairs w,
+//           w + 8, ...; as the tile's pixel-block count divides 8 they share
+//           one pixel block, so one Bs read feeds every MFMA of the wave.
+// A thread's staging elements and depthwise outputs sit at the same places
+// of every chunk, so their index arithmetic is done once per tile.  The
+// epilogue adds the bias (staged with the first chunk) and writes each
+// accumulator row straight to the output: 16 lanes hold 16 consecutive
+// pixels of one channel.
+template <bool COH>
+__device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int BM = o.sep_bm, LBM = o.sep_lbm, MB = BM >> 4, CK = o.sep_ck, W = o.W, H = o.H;
+  const int Wo = o.Wo, howo = o.Ho * Wo, kh = o.kh, kw = o.kw, KK = kh * kw, HW = H * W;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
+  const int img = fdiv(tm, o.fd_pimg), p0 = (tm - img * o.tiles_per_plane) * BM;
+  const int oh0 = fdiv(p0, o.fd_wo), r_lo = oh0 - o.ph;   // first staged input row (may be < 0)
+  const int RW = o.sep_rows * W, plane = CK * RW;   // staged floats per channel / per chunk
+  const int n_chunks = o.sep_nck, NG = o.NG, gpc = CK >> 4, NBT = o.sep_nbt, Cin = o.Cin;
+  const int nb0 = tn * NBT, nbc = min(NBT, (o.Npad >> 4) - nb0);
+  const int ablk = NBT * gpc * 256;                  // pointwise weights of one chunk (floats)
+  const int pitch = sep_pitch(BM);
+  float *xs = lds, *wd = xs + plane;
+  float *as0 = wd + CK * KK, *as1 = as0 + ablk;
+  float *bs = as1 + ablk, *bias = bs + CK * pitch;
+  const int mb = wave & (MB - 1);                   // this wave's pixel block
+  int np = 0;                                        // pairs of this wave: channel blocks nb0 + (wave + 8 r) / MB
+  for (int i = wave; i < MB * nbc && np < kSepPairs; i += kWaves) ++np;
+  np = __builtin_amdgcn_readfirstlane(np);
+
+  // staging: element e = tid + 512 j of a chunk's CK x rows x W block
+  // (channel, staged row, column) lies at soff[j] of the chunk's first input
+  // channel, or outside the image / block (-1)
+  constexpr int SE = kSepStagePerThread;
+  const int ne = (plane + kThreads - 1) >> 9, nw = (CK * KK + kThreads - 1) >> 9;
+  int soff[SE];
+#pragma unroll
+  for (int j = 0; j < SE; ++j) {
+    const int e = tid + j * kThreads;
+    const int ch = fdiv(e, o.fd_rw), rem = e - ch * RW;
+    const int sr = fdiv(rem, o.fd_w), col = rem - sr * W, ih = r_lo + sr;
+    soff[j] = (j < ne && e < plane && ih >= 0 && ih < H) ? ch * HW + ih * W + col : -1;
+  }
+  float sv[SE], wv[kSepDwPerThread];
+  auto issue = [&](int c, int k, float (&dst)[SE]) {
+    const __amdgpu_buffer_rsrc_t xr = rsrc(sl[U(op.in_slot[k])], U(op.in_bytes[k]));
+    const int base = (img * U(op.in_ctot[k]) + U(op.in_coff[k]) + c * CK) * HW;
+    const int elim = min(plane, (Cin - c * CK) * RW);   // elements of channels that exist
+#pragma unroll
+    for (int jb = 0; jb < SE; jb += 4) {
+      if (jb >= ne) break;                           // uniform
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int j = jb + jj, e = tid + j * kThreads;
+        dst[j] = bld(xr, soff[j] >= 0 && e < elim ? (soff[j] + base) * 4 : kOOB, 0);
+      }
+    }
+  };
+  const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes), dr = rsrc(o.dw, o.dw_bytes);
+  // pointwise weights of chunk c: float4 f = tid + 512 k of the chunk's
+  // nbc x gpc blocks (nb, g) of 64 lanes x 4 floats, to registers now and to
+  // LDS with the inputs (groups past the packed ones read 0, never used)
+  const int na4 = nbc * gpc * 64;
+  floatx4 av[kSepAPerThread];
+  auto stage_issue = [&](int c) {
+#pragma unroll
+    for (int k = 0; k < kSepAPerThread; ++k) {
+      const int f = tid + k * kThreads, bi = f >> 6, nbl = bi / gpc, gl = bi - nbl * gpc, g = c * gpc + gl;
+      av[k] = bld4(wr, f < na4 && g < NG ? (((nb0 + nbl) * NG + g) * 64 + (f & 63)) * 16 : kOOB, 0);
+    }
+    issue(c, 0, sv);
+#pragma unroll
+    for (int j = 0; j < kSepDwPerThread; ++j) {
+      if (j >= nw) break;
+      const int e = tid + j * kThreads;
+      wv[j] = bld(dr, e < CK * KK ? (c * CK * KK + e) * 4 : kOOB, 0);   // past the buffer: 0
+    }
+  };
+  auto stage_store = [&](int c, float *as) {
+    for (int k = 1; k < o.n_in; ++k) {              // a RandWire node's further producers
+      float sx[SE];
+      issue(c, k, sx);
+#pragma unroll
+      for (int j = 0; j < SE; ++j) sv[j] += sx[j];
+    }
+#pragma unroll
+    for (int j = 0; j < SE; ++j) {
+      if (j >= ne) break;
+      const int e = tid + j * kThreads;
+      if (e < plane) xs[e] = o.pre_relu ? fmaxf(sv[j], 0.f) : sv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kSepDwPerThread; ++j) {
+      if (j >= nw) break;
+      const int e = tid + j * kThreads;
+      if (e < CK * KK) wd[e] = wv[j];
+    }
+#pragma unroll
+    for (int k = 0; k < kSepAPerThread; ++k) {
+      const int f = tid + k * kThreads;
+      if (f < na4) *(floatx4 *)(as + f * 4) = av[k];
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);        // the biases' copy to LDS has landed
+  };
+
+  // depthwise: this thread's pixel p (the same in every pass, as BM divides
+  // 512) and channels ch0 + i 512 / BM of each chunk
+  const int p = tid & (BM - 1), ch0 = tid >> LBM, chs = kThreads >> LBM;
+  const int qd = p0 + p;
+  const bool qv = qd < howo;
+  int xq = 0, iw0 = 0;
+  if (qv) {
+    const int oh = fdiv(qd, o.fd_wo), ow = qd - oh * Wo;
+    xq = (oh - oh0) * W;
+    iw0 = ow - o.pw;
+  }
+
+  floatx4 acc[kSepPairs];
+#pragma unroll
+  for (int r = 0; r < kSepPairs; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  if (wave == 0) {                                   // the tile's biases, with the first chunk
+    const __amdgpu_buffer_rsrc_t br = rsrc(o.bias, o.Npad * 4);
+    for (int e = 0; e < nbc * 16; e += 64) lds_dma(br, bias + e, (nb0 * 16 + e + lane) * 4);
+  }
+  stage_issue(0);
+  stage_store(0, as0);
+  __syncthreads();
+  for (int c = 0; c < n_chunks; ++c) {
+    const float *as = (c & 1) ? as1 : as0;
+    for (int ch = ch0; ch < CK; ch += chs) {
+      float d = 0.f;
+      if (qv) {
+        const float *xrow = xs + ch * RW + xq, *w = wd + ch * KK;
+        if (kh == 3 && kw == 3) d = dw_point<3, 3>(xrow, w, iw0, W);
+        else if (kh == 5 && kw == 5) {                // rows 0-2, then 3-4 (bounds the registers)
+          d = dw_point<3, 5>(xrow, w, iw0, W);
+          __builtin_amdgcn_sched_barrier(0);
+          d = dw_point<2, 5>(xrow + 3 * W, w + 15, iw0, W, d);
+        }
+        else
+          for (int u = 0; u < kh; ++u)
+            for (int v = 0; v < kw; ++v)
+              if (iw0 + v >= 0 && iw0 + v < W) d = fmaf(w[u * kw + v], xrow[u * W + iw0 + v], d);
+      }
+      bs[ch * pitch + p] = d;
+    }
+    __syncthreads();
+    if (c + 1 < n_chunks) stage_issue(c + 1);        // in flight during the MFMAs
+    // pointwise on MFMA over the chunk's groups of 4 k-steps (16 channels)
+    static_assert(kSepPairs == 4, "one case per pair count");
+    switch (np) {
+      case 1: sep_mma<1>(acc, as, bs, c, gpc, NG, pitch, wave, MB, mb, lane); break;
+      case 2: sep_mma<2>(acc, as, bs, c, gpc, NG, pitch, wave, MB, mb, lane); break;
+      case 3: sep_mma<3>(acc, as, bs, c, gpc, NG, pitch, wave, MB, mb, lane); break;
+      case 4: sep_mma<4>(acc, as, bs, c, gpc, NG, pitch, wave, MB, mb, lane); break;
+      default: break;
+    }
+    if (c + 1 < n_chunks) stage_store(c + 1, (c & 1) ? as0 : as1);
+    __syncthreads();
+  }
+  // epilogue: lane l, element j holds channel nb 16 + 4 (l / 16) + j of pixel mb 16 + l % 16
+  const int q = p0 + mb * 16 + (lane & 15);
+  float *out = sl[o.route_slot[0]];
+#pragma unroll
+  for (int r = 0; r < kSepPairs; ++r) {
+    if (r >= np) break;
+    const int nbl = (wave + r * kWaves) / MB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int nl = nbl * 16 + 4 * (lane >> 4) + j, n = nb0 * 16 + nl;
+      if (n < o.Cout && q < howo) {
+        float v = acc[r][j] + bias[nl];
+        if (o.post_relu) v = fmaxf(v, 0.f);
+        st<COH>(out + ((size_t)img * o.route_ctot[0] + o.route_coff[0] + n) * howo + q, v);
+      }
+    }
+  }
+}
+
 
 // Cross-lane moves inside each row of 16 lanes (DPP): lane i of a row takes
 // the value of lane i + N (from_right) or lane i - N (from_left) of the same
@@ -355,21 +747,17 @@ __device__ __forceinline__ float dw_taps(const float *w, float xa, float xb, flo
   return d;
 }
 
-// Direct global -> LDS load of one float per active lane: lane i of the wave
-// writes l[i] (l wave-uniform), no VGPR involved.  The compiler does not see
-// this write: readers must wait for vmcnt(0) themselves (lds_dma_wait).
-typedef __attribute__((address_space(3))) void lds_void;
-__device__ __forceinline__ void lds_dma(__amdgpu_buffer_rsrc_t r, float *l, int voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)l, 4, voff, 0, 0, 0);
-}
+// Waits for this wave's direct-to-LDS loads (the compiler does not see
+// their writes).
 __device__ __forceinline__ void lds_dma_wait() {
   __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   __builtin_amdgcn_wave_barrier();
 }
 
-// "Relu-SepConv" unit (sum of inputs -> ReLU -> depthwise -> pointwise) on 16
-// output pixels of one output row x sep_nbt blocks of 16 output channels.
+// "Relu-SepConv" unit, row tile (the alternative to the staged tile above,
+// chosen per operator by measurement): 16 output pixels of one output row x
+// sep_nbt blocks of 16 output channels.
 //
 // Lane l = 16 g + j of a wave computes the depthwise output of pixel j for
 // channel 4 ks + g: exactly the A operand lane l gives the 16x16x4 MFMA at
@@ -384,19 +772,19 @@ __device__ __forceinline__ void lds_dma_wait() {
 // with several inputs the next input's loads are in flight while the current
 // one is added.
 template <int K, bool SINGLE, bool COH>
-__device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+__device__ __forceinline__ void sep_row_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
   constexpr int KB = SINGLE ? (K == 3 ? 8 : 6) : (K == 3 ? 4 : 2);   // k-steps per batch
   constexpr int KKP = (K * K + 3) & ~3;               // floats per channel of depthwise weights
-  constexpr int NBT = kSepMaxNB;
+  constexpr int NBT = kSepRowMaxNB;
   constexpr int LDR = 16 + 1;                         // reduction buffer row pitch
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int j = lane & 15, g = lane >> 4;
   const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
   const int H = o.H, W = o.W, Ho = o.Ho, Wo = o.Wo, howo = Ho * Wo;
-  const int bpr = o.sep_bpr, per_img = Ho * bpr;
+  const int bpr = o.row_bpr, per_img = Ho * bpr;
   const int img = fdiv(tm, o.fd_pimg), rr = tm - img * per_img;
-  const int oh = fdiv(rr, o.fd_bpr), ow0 = (rr - oh * bpr) * 16;
+  const int oh = fdiv(rr, o.fd_rbpr), ow0 = (rr - oh * bpr) * 16;
   const int NKS = o.CinP >> 2;
   const int ks0 = NKS * wave / kWaves, nks = NKS * (wave + 1) / kWaves - ks0;
   const int nb0 = tn * o.sep_nbt, nbc = min(o.sep_nbt, (o.Npad >> 4) - nb0);
@@ -405,7 +793,7 @@ __device__ __forceinline__ void sep_tile(const Slots &sl, const DevOp &op, const
 
   // (1) this wave's weights -> its LDS region: depthwise [4 nks][KKP], then
   //     pointwise rows 4 ks0 .. 4 (ks0 + nks) - 1, columns of this tile
-  float *wl = lds + wave * sep_wave_floats(o.CinP, K, o.sep_nbt);
+  float *wl = lds + wave * sep_row_wave_floats(o.CinP, K, o.sep_nbt);
   float *pl = wl + nks * 4 * KKP;
   {
     const __amdgpu_buffer_rsrc_t dr = rsrc(o.dw, o.dw_bytes);
@@ -687,9 +1075,11 @@ __device__ __forceinline__ void sum_tile(const Slots &sl, const DevOp &op, const
 
 // Kernel variants, chosen per stage by the host so that a stage only pays
 // the registers of the tile kinds it contains:
-//   KV_LIGHT  16x16 and 16x32 conv tiles, pooling, add / mean
-//   KV_SEP    KV_LIGHT + SEPCONV tiles
-//   KV_FULL   every tile kind and conv tile shape
+//   KV_LIGHT   16x16 and 16x32 conv tiles, pooling, add / mean
+//   KV_SEP     KV_LIGHT + staged SEPCONV tiles
+//   KV_SEPROW  KV_LIGHT + row SEPCONV tiles
+//   KV_PIPE    KV_LIGHT + pipelined conv tiles
+//   KV_FULL    every tile kind and conv tile shape
 // A conv tile with the input ReLU and the channel check resolved at compile
 // time (no branch between its loads and MFMAs).
 template <int FM, int FN, int WM, int WN, int WK, bool COH>
@@ -708,6 +1098,16 @@ template <bool COH, int KV>
 __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const DevOp &o, int ti, float *lds) {
   switch (o.kind) {
     case DK_CONV:
+      if constexpr (KV == KV_PIPE || KV == KV_FULL) {
+        if (o.tcfg >= TC_P128x64) {
+          switch (o.tcfg) {
+            case TC_P128x64: conv_pipe_tile<4, COH>(sl, op, o, ti, lds); break;
+            case TC_P256x32: conv_pipe_tile<8, COH>(sl, op, o, ti, lds); break;
+            default: conv_pipe_tile<2, COH>(sl, op, o, ti, lds); break;
+          }
+          break;
+        }
+      }
       if constexpr (KV != KV_FULL) {
         if (o.tcfg == TC_16x16_K8) conv_any<1, 1, 1, 1, 8, COH>(sl, op, o, ti, lds);
         else conv_any<1, 2, 1, 1, 8, COH>(sl, op, o, ti, lds);
@@ -725,11 +1125,15 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
       }
     case DK_SEP:
       if constexpr (KV != KV_LIGHT) {
-        const bool one = o.n_in == 1;
-        if (o.sep_k == 3) {
-          if (one) sep_tile<3, true, COH>(sl, op, o, ti, lds); else sep_tile<3, false, COH>(sl, op, o, ti, lds);
-        } else {
-          if (one) sep_tile<5, true, COH>(sl, op, o, ti, lds); else sep_tile<5, false, COH>(sl, op, o, ti, lds);
+        if (!o.sep_row) {
+          if constexpr (KV != KV_SEPROW) sep_tile<COH>(sl, op, o, ti, lds);
+        } else if constexpr (KV != KV_SEP) {
+          const bool one = o.n_in == 1;
+          if (o.row_k == 3) {
+            if (one) sep_row_tile<3, true, COH>(sl, op, o, ti, lds); else sep_row_tile<3, false, COH>(sl, op, o, ti, lds);
+          } else {
+            if (one) sep_row_tile<5, true, COH>(sl, op, o, ti, lds); else sep_row_tile<5, false, COH>(sl, op, o, ti, lds);
+          }
         }
       }
       break;

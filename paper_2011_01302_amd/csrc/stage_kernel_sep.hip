@@ -1,4 +1,4 @@
-// Stage kernel variant KV_SEP, one workgroup per tile: the light tiles plus SEPCONV tiles.  One translation unit per
+// Stage kernel variant KV_SEP, one workgroup per tile: the light tiles plus staged SEPCONV tiles.  One translation unit per
 // (variant, launch kind) so that the kernels build in parallel (see
 // stage_kernel.h and stage_launch.cpp).
 #include "stage_kernel.h"

@@ -1,0 +1,15 @@
+// Stage kernel variant KV_SEPROW, persistent launch: the light tiles plus row SEPCONV tiles.  One translation unit per
+// (variant, launch kind) so that the kernels build in parallel (see
+// stage_kernel.h and stage_launch.cpp).
+#include "stage_kernel.h"
+
+namespace ios {
+
+void *stage_kernel_fn_seprow_persist() { return (void *)ios_stage_kernel<KV_SEPROW, true>; }
+
+hipError_t stage_launch_seprow_persist(const int4 *t, int words, const StageArgs &a, int grid, int lds, hipStream_t s) {
+  hipLaunchKernelGGL((ios_stage_kernel<KV_SEPROW, true>), dim3(grid), dim3(kThreads), lds, s, t, words, a);
+  return hipGetLastError();
+}
+
+}  // namespace ios

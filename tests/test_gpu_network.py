@@ -1,7 +1,9 @@
 """GPU parity on whole networks: Inception-V3 (3x299x299 -> 1000 logits,
-13 blocks, 109 schedule units) and SqueezeNet v1.0 (3x227x227 -> 1000, 12
-blocks, 28 units), random weights, through the C ABI against the fp64 oracle
-(max|gpu - oracle| / max|oracle| <= 1e-4 on the logits), under the baseline
+13 blocks, 109 schedule units), SqueezeNet v1.0 (3x227x227 -> 1000, 12
+blocks, 28 units), the RandWire stack (3 random-graph stages and 2
+transitions, 101 units) and the NASNet stack (6 cells and a strided conv,
+121 units), random weights, through the C ABI against the fp64 oracle
+(max|gpu - oracle| / max|oracle| <= 1e-4 on the outputs), under the baseline
 schedules and under the DP run block by block on the device, whose schedule
 must equal the oracle DP replayed on the dumped cost table."""
 import functools
@@ -81,6 +83,11 @@ def test_network_parity_baseline_schedules(net, batch):
     g.close()
 
 
+# pruning per network: the random-graph stages and the NASNet cells search
+# with r = 1 (the paper's fast setting, Sec. 7.1), which keeps the test short
+PRUNING = {"inception_v3": (3, 8), "squeezenet": (3, 8), "randwire_net": (1, 8), "nasnet_net": (1, 8)}
+
+
 @pytest.mark.parametrize("net", W.NETWORK_NAMES)
 def test_network_device_dp_replays_in_oracle(net, tmp_path):
     """Algorithm 1 on each block with on-device stage profiling
@@ -88,8 +95,10 @@ def test_network_device_dp_replays_in_oracle(net, tmp_path):
     oracle DP's on the dumped cost table, block by block."""
     spec, ten = case(net)
     g = I.Graph(spec, ten)
+    pr, ps = PRUNING[net]
     o = I.ios_sched_opts_default()
     o.warmup, o.reps, o.repeats = 1, 3, 1
+    o.r, o.s = pr, ps
     q, cost = I.ios_schedule(g.handle, o)
     check(run(g, q, spec, ten), reference(net), "dp")
     path = tmp_path / "costs.jsonl"
@@ -102,7 +111,7 @@ def test_network_device_dp_replays_in_oracle(net, tmp_path):
             table[(r["block"], r["mask"], 1)] = r["merge_ns"]
     total, stages = 0, []
     for b, blk in enumerate(O.blocks_of(spec)):
-        res = O.ios_dp(blk, lambda m, t: table[(b, m, t)], 3, 8)
+        res = O.ios_dp(blk, lambda m, t: table[(b, m, t)], pr, ps)
         total += res.cost
         stages += [(sorted(blk.units[i]["name"] for i in O.bits(m)), t) for m, t in res.schedule]
     lib = [(sorted(g.names(ids)), t) for ids, t in I.ios_schedule_get(q)]

@@ -159,7 +159,7 @@ def test_parity_operator_merge(config, groups):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5"])
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6", "7", "8"])
 def test_parity_every_conv_tile_shape(tile, monkeypatch):
     monkeypatch.setenv("IOS_CONV_TILE", tile)
     for config in ["tiny", "inception", "squeeze"]:
@@ -412,6 +412,21 @@ def test_parity_batched_every_image(config, batch, kinds):
     g.close()
 
 
+def test_parity_inception_7c_merged_pairs_bs32():
+    """The last Inception-V3 module at batch 32 with its two parallel
+    1x3 / 3x1 pairs each run as one merged 3x3 conv (Sec. 7.2: the schedule
+    the paper finds best at large batch), and with the three 1x1 convs on the
+    input merged: every image against the oracle."""
+    spec, ten, refs = batched_reference("inception_7c", 32)
+    g = I.Graph(spec, ten)
+    q = merge_schedule(g, spec, [["7c_1x1", "7c_3a", "7c_d3a"], ["7c_3b1", "7c_3b2"], ["7c_d3c1", "7c_d3c2"]])
+    st = I.ios_schedule_get(q)
+    assert sum(t == I.IOS_MERGE for _, t in st) == 3
+    check(run(g, q, spec, ten), refs, "inception_7c/bs32/merged pairs")
+    I.ios_schedule_destroy(q)
+    g.close()
+
+
 def test_device_dp_batched_replays_in_oracle(tmp_path):
     """A search at batch 16 (Sec. 7.2: schedules are specialised per batch
     size) replays bit for bit in the oracle DP on the dumped table."""
@@ -515,7 +530,7 @@ def ragged_spec(batch):
 # tile None: shapes chosen by measurement, else forced; offset: inputs start
 # 1 or 3 floats past a 16-byte boundary
 @pytest.mark.parametrize("batch,tile,offset", [(1, None, 0), (2, None, 0), (1, "1", 1), (1, "0", 3),
-                                               (2, "4", 1)])
+                                               (2, "4", 1), (2, "6", 1), (3, "7", 0), (1, "8", 3)])
 def test_parity_ragged_shapes(batch, tile, offset, monkeypatch):
     if tile is not None:
         monkeypatch.setenv("IOS_CONV_TILE", tile)
@@ -565,7 +580,7 @@ def test_parity_pool_planes(batch):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "4"])
+@pytest.mark.parametrize("tile", ["0", "1", "4", "6", "7", "8"])
 def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     """Forced conv tile shapes over several small images (the 16-pixel
     blocks of an 8x8 plane never span two images)."""
@@ -579,21 +594,39 @@ def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     g.close()
 
 
-@pytest.mark.parametrize("nbt", ["1", "2", "3", "4"])
-def test_parity_every_sepconv_block_count(nbt, monkeypatch):
-    # output blocks of 16 channels per SEPCONV tile, forced instead of measured
-    monkeypatch.setenv("IOS_SEP_NBT", nbt)
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6"])
+def test_parity_every_sepconv_tile(tile, monkeypatch):
+    # SEPCONV tile choice (staged: 16, 32 or 64 output pixels per tile; row:
+    # 1 to 4 channel blocks), forced instead of measured (the wide unit
+    # cannot use the row tile and falls back to the staged one)
+    monkeypatch.setenv("IOS_SEP_TILE", tile)
     for config in ["randwire", "nasnet"]:
         spec, ten = case(config)
         g = I.Graph(spec, ten)
         for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY)):
-            check(run(g, q, spec, ten), reference(config), f"{config}/nbt{nbt}")
+            check(run(g, q, spec, ten), reference(config), f"{config}/sep tile {tile}")
             I.ios_schedule_destroy(q)
         g.close()
-    spec = ragged_spec(2)
-    ten = W.make_tensors(spec, 4)
-    g = I.Graph(spec, ten)
-    q = sched(g, I.IOS_SCHED_GREEDY)
-    check(run(g, q, spec, ten), E.outputs(spec, ten), f"ragged/nbt{nbt}")
-    I.ios_schedule_destroy(q)
-    g.close()
+    for spec in (ragged_spec(2), wide_sep_spec(2)):
+        ten = W.make_tensors(spec, 4)
+        g = I.Graph(spec, ten)
+        for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+            check(run(g, q, spec, ten), E.outputs(spec, ten), f"{spec['name']}/sep tile {tile}")
+            I.ios_schedule_destroy(q)
+        g.close()
+
+
+def wide_sep_spec(batch):
+    """SEPCONVs past the old limits: 280 input channels (18 chunks of 16 or 9
+    of 32, a short last group), 7x7 and 1x5 windows, 180 output channels
+    (12 channel blocks, several channel groups per pixel run), an odd 19x23
+    plane, a chain of two and a three-input sum."""
+    sep = lambda n, ins, co, kh, kw: {"name": n, "kind": "sepconv", "in": ins, "cout": co, "kh": kh, "kw": kw,
+                                      "sh": 1, "sw": 1, "ph": kh // 2, "pw": kw // 2, "pre_relu": 1,
+                                      "post_relu": 0}
+    ops = [sep("w1", ["x"], 180, 7, 7),
+           sep("w2", ["w1", "x2", "w1"], 36, 1, 5),
+           sep("w3", ["x"], 20, 3, 3)]
+    return {"name": "wide_sep", "batch": batch,
+            "inputs": [{"name": "x", "c": 280, "h": 19, "w": 23}, {"name": "x2", "c": 180, "h": 19, "w": 23}],
+            "ops": ops, "outputs": ["w2", "w3"]}

@@ -87,8 +87,8 @@ def disassembly(tmp_path_factory):
 def test_stage_kernels_present(disassembly):
     names = {re.match(r"^[0-9a-f]+ <(\S+)>:", l).group(1) for l in disassembly
              if re.match(r"^[0-9a-f]+ <(\S+)>:", l)}
-    # every kernel variant (light / sep / full) x launch kind (tile / persistent)
-    assert len({n for n in names if "ios_stage_kernel" in n}) == 6
+    # every kernel variant (light / sep / seprow / pipe / full) x launch kind (tile / persistent)
+    assert len({n for n in names if "ios_stage_kernel" in n}) == 10
 
 
 def test_no_readlane_of_possibly_disabled_lanes(disassembly):

@@ -1,8 +1,12 @@
-"""Whole-network workloads (Inception-V3, SqueezeNet; scheduled block by block): the
-descriptions against the networks' published layer tables, and the oracle's
-block split and state spaces against closed forms.  No GPU."""
+"""Whole-network workloads (Inception-V3, SqueezeNet, the RandWire and NASNet
+stacks; scheduled block by block): the descriptions against the networks'
+published layer tables or their construction, and the oracle's block split
+and state spaces against closed forms.  No GPU."""
 import math
 
+import numpy as np
+
+from oracle import evaluator as E
 from oracle import schedule as O
 import workloads as W
 
@@ -134,3 +138,44 @@ def test_squeezenet_layer_table():
         if b.n == 3:
             assert O.mergeable(b, 0b110)
             assert O.ios_dp(b, lambda m, t: 1, 3, 8).states == 5    # a squeeze unit feeding two
+
+
+def test_randwire_net_layout():
+    """Three WS(32, 4, 0.75) stages of SEPCONV nodes with 78, 156 and 312
+    channels at 28x28, 14x14 and 7x7, each ending in the mean of its sinks,
+    joined by 1x1 stride-2 convs; five blocks (stage, transition, ...), each
+    stage's graph drawn from its own stream; the whole network evaluates in
+    the oracle to the last stage's mean."""
+    s, ten = W.make("randwire_net")
+    shp = W.infer_shapes(s)
+    assert [shp[f"s{k}out"] for k in (1, 2, 3)] == [(78, 28, 28), (156, 14, 14), (312, 7, 7)]
+    assert shp["down1"] == (156, 14, 14) and shp["down2"] == (312, 7, 7)
+    blocks = O.blocks_of(s)
+    assert [b.n for b in blocks] == [33, 1, 33, 1, 33]
+    assert len(s["block_names"]) == len(blocks)
+    edges = [sorted((a, b) for a in range(32) for b in range(32) if blk.succ[a] >> b & 1)
+             for blk in (blocks[0], blocks[2], blocks[4])]
+    assert edges[0] != edges[1] != edges[2]
+    for e in edges:
+        assert len(e) >= 64                      # 2n = 64 WS edges among the nodes, plus edges to the mean
+    out = E.outputs(s, ten)[0]
+    assert out.shape == (1, 312, 7, 7) and np.isfinite(out).all()
+
+
+def test_nasnet_net_layout():
+    """Six normal cells (168 channels at 42x42, then 336 at 21x21) around a
+    3x3 stride-2 conv; each cell's inputs pass through 1x1 convs to the cell
+    width (the first cell reads the stack's inputs directly); concat widths
+    5C; seven blocks; each cell drawn from its own stream."""
+    s, ten = W.make("nasnet_net")
+    shp = W.infer_shapes(s)
+    assert [shp[f"k{k}out"] for k in range(1, 7)] == [(840, 42, 42)] * 3 + [(1680, 21, 21)] * 3
+    assert shp["reduce"] == (336, 21, 21)
+    assert "k1h" not in shp and shp["k2h"] == (168, 42, 42) and shp["k6hp"] == (336, 21, 21)
+    blocks = O.blocks_of(s)
+    assert len(blocks) == 7 and blocks[3].n == 1
+    assert len(s["block_names"]) == len(blocks)
+    kinds = [[u["kind"] for u in b.units] for b in blocks]
+    assert len({tuple(k) for k in kinds}) > 2                   # cells differ
+    out = E.outputs(W.with_batch(s, 1), ten)[0]
+    assert out.shape == (1, 1680, 21, 21) and np.isfinite(out).all()

@@ -85,7 +85,7 @@ def test_noalloc_matches_ios_run_two_calls(make_q):
 def test_noalloc_errors(monkeypatch):
     print("\n[gpu-case] noalloc errors", flush=True)
     monkeypatch.setenv("IOS_CONV_TILE", "1")      # no tile measurement at set-up
-    monkeypatch.setenv("IOS_SEP_NBT", "1")
+    monkeypatch.setenv("IOS_SEP_TILE", "1")
     spec = chained_spec(1)
     ten = W.make_tensors(spec, 5)
     g = I.Graph(spec, ten)

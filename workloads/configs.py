@@ -16,6 +16,10 @@ and, for the block-wise whole-network runs (not one of the blocks above):
                  13 blocks (stem, eleven modules, head)
   squeezenet     the whole SqueezeNet v1.0 network, 3x227x227 -> 1000,
                  12 blocks (conv1 + pool, eight fire modules, two pools, head)
+  randwire_net   three RandWire stages (78, 156, 312 channels at 28, 14, 7)
+                 joined by strided 1x1 convs, 5 blocks
+  nasnet_net     six NASNet-A style normal cells (168 then 336 channels at 42
+                 then 21) around a strided conv, 7 blocks
 
 A workload is a plain description (``spec``) plus a dict of float32 numpy
 arrays (``tensors``).  The description lists the operators in insertion
@@ -128,59 +132,141 @@ def ws_edges(n: int, k: int, p: float, stream: rng.Stream) -> List[Tuple[int, in
     return edges
 
 
-def spec_randwire(batch: int = 1, seed: int = 0, nodes: int = 32, channels: int = 78,
-                  hw: int = 28) -> dict:
-    stream = rng.Stream(rng.key_of("randwire-graph", seed))
+def _randwire_block(ops, prefix, inp, channels, graph_key, nodes=32, block=-1):
+    """A WS(nodes, 4, 0.75) DAG of SEPCONV nodes reading `inp`; returns the
+    name of its output (the mean of the sinks) and the graph's edges."""
+    stream = rng.Stream(graph_key)
     edges = ws_edges(nodes, 4, 0.75, stream)
     preds = [[] for _ in range(nodes)]
     outdeg = [0] * nodes
     for a, b in edges:
         preds[b].append(a)
         outdeg[a] += 1
-    ops = []
     for v in range(nodes):
-        ins = [f"n{u}" for u in sorted(preds[v])] or ["x"]
-        ops.append(_sep(f"n{v}", ins, channels, 3))
-    sinks = [f"n{v}" for v in range(nodes) if outdeg[v] == 0]
-    ops.append({"name": "out", "kind": "mean", "in": sinks, "block": -1})
+        ins = [f"{prefix}n{u}" for u in sorted(preds[v])] or [inp]
+        ops.append(_sep(f"{prefix}n{v}", ins, channels, 3, block=block))
+    sinks = [f"{prefix}n{v}" for v in range(nodes) if outdeg[v] == 0]
+    ops.append({"name": f"{prefix}out", "kind": "mean", "in": sinks, "block": block})
+    return f"{prefix}out", edges
+
+
+def spec_randwire(batch: int = 1, seed: int = 0, nodes: int = 32, channels: int = 78,
+                  hw: int = 28) -> dict:
+    ops = []
+    _, edges = _randwire_block(ops, "", "x", channels, rng.key_of("randwire-graph", seed), nodes)
     return {"name": "randwire", "batch": batch, "seed": seed,
             "inputs": [{"name": "x", "c": channels, "h": hw, "w": hw}],
             "ops": ops, "outputs": ["out"], "ws_edges": edges}
 
 
+RANDWIRE_NET_BLOCKS = ["stage1", "down1", "stage2", "down2", "stage3"]
+
+
+def spec_randwire_net(batch: int = 1, seed: int = 0, channels: int = 78, hw: int = 28) -> dict:
+    """The three random-graph stages of a RandWire network (small regime):
+    WS(32, 4, 0.75) DAGs of SEPCONV nodes with C, 2C and 4C channels at 28x28,
+    14x14 and 7x7, each drawn from its own seeded stream, joined by 1x1
+    stride-2 convs (+ ReLU) that double the channels.  Blocks: each stage and
+    each transition."""
+    ops = []
+    cur = "x"
+    for k in range(3):
+        c = channels << k
+        if k:
+            ops.append(_conv(f"down{k}", cur, c, 1, 0, stride=2, block=2 * k - 1))
+            cur = f"down{k}"
+        cur, _ = _randwire_block(ops, f"s{k + 1}", cur, c, rng.key_of("randwire-net-graph", seed, k),
+                                 block=2 * k)
+    return {"name": "randwire_net", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": channels, "h": hw, "w": hw}],
+            "ops": ops, "outputs": [cur], "block_names": RANDWIRE_NET_BLOCKS}
+
+
 NASNET_OPS = ["sep3", "sep5", "avgpool", "maxpool", "identity"]
 
 
-def spec_nasnet(batch: int = 1, seed: int = 0, channels: int = 168, hw: int = 42) -> dict:
-    stream = rng.Stream(rng.key_of("nasnet-cell", seed))
-    ops = []
-    outs = []
-    choices = []
+def _nasnet_cell(ops, prefix, h, h_prev, channels, cell_key, block=-1):
+    """Five combine blocks, each adding two ops applied to inputs drawn from
+    {h, h_prev}, the ops drawn from NASNET_OPS (a separable conv is two
+    chained SEPCONV units); the adds are concatenated.  Returns the concat's
+    name and the draws."""
+    stream = rng.Stream(cell_key)
+    outs, choices = [], []
     for b in range(5):
         slot_out = []
         for s in range(2):
-            inp = ["h", "h_prev"][stream.randint(2)]
+            side = stream.randint(2)
+            inp = [h, h_prev][side]
             kind = NASNET_OPS[stream.randint(5)]
-            choices.append((b, s, inp, kind))
-            nm = f"c{b}s{s}"
+            choices.append((b, s, ["h", "h_prev"][side], kind))
+            nm = f"{prefix}c{b}s{s}"
             if kind in ("sep3", "sep5"):
                 k = 3 if kind == "sep3" else 5
-                ops.append(_sep(nm + "u1", [inp], channels, k))
-                ops.append(_sep(nm + "u2", [nm + "u1"], channels, k))
+                ops.append(_sep(nm + "u1", [inp], channels, k, block=block))
+                ops.append(_sep(nm + "u2", [nm + "u1"], channels, k, block=block))
                 slot_out.append(nm + "u2")
             elif kind in ("avgpool", "maxpool"):
-                ops.append(_pool(nm, inp, kind, 3, 1, 1))
+                ops.append(_pool(nm, inp, kind, 3, 1, 1, block=block))
                 slot_out.append(nm)
             else:
                 ops.append(_view(nm, "identity", [inp]))
                 slot_out.append(nm)
-        ops.append({"name": f"add{b}", "kind": "add", "in": slot_out, "block": -1})
-        outs.append(f"add{b}")
-    ops.append(_view("out", "concat", outs))
+        ops.append({"name": f"{prefix}add{b}", "kind": "add", "in": slot_out, "block": block})
+        outs.append(f"{prefix}add{b}")
+    ops.append(_view(f"{prefix}out", "concat", outs))
+    return f"{prefix}out", choices
+
+
+def spec_nasnet(batch: int = 1, seed: int = 0, channels: int = 168, hw: int = 42) -> dict:
+    ops = []
+    _, choices = _nasnet_cell(ops, "", "h", "h_prev", channels, rng.key_of("nasnet-cell", seed))
     return {"name": "nasnet", "batch": batch, "seed": seed,
             "inputs": [{"name": "h", "c": channels, "h": hw, "w": hw},
                        {"name": "h_prev", "c": channels, "h": hw, "w": hw}],
             "ops": ops, "outputs": ["out"], "choices": choices}
+
+
+NASNET_NET_BLOCKS = ["cell1", "cell2", "cell3", "reduce", "cell4", "cell5", "cell6"]
+
+
+def spec_nasnet_net(batch: int = 1, seed: int = 0, channels: int = 168, hw: int = 42) -> dict:
+    """A NASNet-A style stack: three normal cells with C channels at 42x42,
+    a 3x3 stride-2 conv (+ ReLU) to 2C channels at 21x21 in place of the
+    reduction cell, three normal cells with 2C channels.  A cell reads the
+    two previous cells' outputs (5C or 10C channels) through 1x1 convs to C
+    (its "reduce" inputs h and h_prev); the stack's inputs h, h_prev feed the
+    first cell, the strided conv's output both inputs of the cell after it.
+    Each cell's draws come from its own seeded stream.  Blocks: each cell
+    with its two 1x1 convs, and the strided conv."""
+    ops = []
+    outs = {}
+    block = 0
+
+    def cell(k, h_src, hp_src, c):
+        nonlocal block
+        pre = f"k{k}"
+        srcs = []
+        for nm, src in (("h", h_src), ("hp", hp_src)):
+            if src in ("h", "h_prev"):          # the stack's own inputs: already C channels
+                srcs.append(src)
+            else:
+                ops.append(_conv(f"{pre}{nm}", src, c, 1, 0, block=block))
+                srcs.append(f"{pre}{nm}")
+        out, _ = _nasnet_cell(ops, pre, srcs[0], srcs[1], c, rng.key_of("nasnet-net-cell", seed, k), block=block)
+        outs[k] = out
+        block += 1
+    cell(1, "h", "h_prev", channels)
+    cell(2, outs[1], "h", channels)
+    cell(3, outs[2], outs[1], channels)
+    ops.append(_conv("reduce", outs[3], 2 * channels, 3, 1, stride=2, block=block))
+    block += 1
+    cell(4, "reduce", "reduce", 2 * channels)
+    cell(5, outs[4], "reduce", 2 * channels)
+    cell(6, outs[5], outs[4], 2 * channels)
+    return {"name": "nasnet_net", "batch": batch, "seed": seed,
+            "inputs": [{"name": "h", "c": channels, "h": hw, "w": hw},
+                       {"name": "h_prev", "c": channels, "h": hw, "w": hw}],
+            "ops": ops, "outputs": [outs[6]], "block_names": NASNET_NET_BLOCKS}
 
 
 FIRE = [(16, 64), (16, 64), (32, 128), (32, 128), (48, 192), (48, 192), (64, 256), (64, 256)]
@@ -288,6 +374,18 @@ def _inception_e(ops, p, inp, block):
             _view(p, "concat", [f"{p}_1x1", f"{p}_3", f"{p}_d3", f"{p}_pp"])]
 
 
+def spec_inception_7c(batch: int = 1, seed: int = 0) -> dict:
+    """Inception-V3's last module (7c, an 8x8 module whose 3x3 branches end
+    in parallel 1x3 and 3x1 convs) as a block of its own, 2048x8x8 ->
+    2048x8x8: the block whose schedule the paper shows changing with the
+    batch size (merging a 1x3 / 3x1 pair into one 3x3 conv pays at large
+    batch)."""
+    ops = []
+    _inception_e(ops, "7c", "x", -1)
+    return {"name": "inception_7c", "batch": batch, "seed": seed,
+            "inputs": [{"name": "x", "c": 2048, "h": 8, "w": 8}], "ops": ops, "outputs": ["7c"]}
+
+
 INCEPTION_V3_BLOCKS = ["stem", "5b", "5c", "5d", "6a", "6b", "6c", "6d", "6e", "7a", "7b", "7c", "head"]
 
 
@@ -349,11 +447,12 @@ def spec_squeezenet(batch: int = 1, seed: int = 0) -> dict:
             "ops": ops, "outputs": ["gpool"], "block_names": names}
 
 
-NETWORK_NAMES = ["inception_v3", "squeezenet"]
+NETWORK_NAMES = ["inception_v3", "squeezenet", "randwire_net", "nasnet_net"]
 
 SPECS = {"tiny": spec_tiny, "inception": spec_inception, "randwire": spec_randwire,
          "nasnet": spec_nasnet, "squeeze": spec_squeeze, "inception_v3": spec_inception_v3,
-         "squeezenet": spec_squeezenet}
+         "squeezenet": spec_squeezenet, "randwire_net": spec_randwire_net, "nasnet_net": spec_nasnet_net,
+         "inception_7c": spec_inception_7c}
 
 
 # ---------------------------------------------------------------- shapes

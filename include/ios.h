@@ -170,13 +170,17 @@ int ios_profile_stage(ios_graph *g, const int32_t *unit_ids, int32_t n, int32_t 
  * 0 .. IOS_CONV_TILE_SHAPES - 1 (16x16, 16x32, 32x32, 32x64, 64x64 and
  * 128x64 output pixels x channels, operands loaded per wave; then 128x64,
  * 256x32 and 64x128 with both operands staged in LDS by a pipeline of
- * direct loads, for large convolutions).  A new shape applies to stages compiled
+ * direct loads shared by the workgroup, and the same three shapes with a
+ * private pipeline per wave, for large convolutions whose input channels are a multiple
+ * of 16, with at most 32 taps and no input ReLU; a merge stage whose
+ * merged window has more taps falls back to 16x32).  A new shape applies to stages compiled
  * afterwards (ios_profile_stage, ios_schedule, ios_schedule_from_stages),
  * not to schedules that already exist.  Both calls set up the device first
  * (hence the measurement) if no earlier call has.
- * Errors: IOS_E_ARG (not a conv unit, shape out of range, null pointer),
- * IOS_E_STATE (not finalized), IOS_E_HIP. */
-enum { IOS_CONV_TILE_SHAPES = 9 };
+ * Errors: IOS_E_ARG (not a conv unit, shape out of range or a pipelined
+ * shape the conv does not admit, null pointer), IOS_E_STATE (not
+ * finalized), IOS_E_HIP. */
+enum { IOS_CONV_TILE_SHAPES = 12 };
 int ios_get_conv_tile(ios_graph *g, int32_t unit_id, int32_t *shape);
 int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
 

@@ -42,7 +42,7 @@ ERRORS = {-1: "IOS_E_ARG", -2: "IOS_E_SHAPE", -3: "IOS_E_STATE", -4: "IOS_E_NOT_
 IOS_CONV, IOS_SEPCONV, IOS_POOL_MAX, IOS_POOL_AVG, IOS_ADD, IOS_MEAN, IOS_CONCAT, IOS_IDENTITY = range(8)
 IOS_CONCURRENT, IOS_MERGE = 0, 1
 IOS_SCHED_DP, IOS_SCHED_SEQUENTIAL, IOS_SCHED_GREEDY = 0, 1, 2
-IOS_CONV_TILE_SHAPES = 9
+IOS_CONV_TILE_SHAPES = 12
 INT64_MAX = (1 << 63) - 1
 
 EXPORTED = ["ios_graph_create", "ios_graph_destroy", "ios_add_input", "ios_add_op",

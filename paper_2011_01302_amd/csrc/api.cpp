@@ -190,6 +190,7 @@ int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape) {
     const int op = unit_op_of_tensor(g, unit_id);
     need(g->ops[op].d.kind == IOS_CONV, "not a conv unit");
     need(shape >= 0 && shape < TC_COUNT, "tile shape out of range");
+    need(conv_tile_ok(g->ops[op], shape), "pipelined tile shape not applicable to this conv");
     ensure_device(g);
     g->ops[op].tcfg = shape;
   });
@@ -211,16 +212,17 @@ int ios_set_unit_tiling(ios_graph *g, int32_t unit_id, int32_t tile, int32_t xcd
     need_final(g);
     Op &op = g->ops[unit_op_of_tensor(g, unit_id)];
     need(xcd_lg == -1 || xcd_lg == 0 || xcd_lg == 2 || xcd_lg == 4, "xcd_lg must be -1, 0, 2 or 4");
-    ensure_device(g);
     if (op.d.kind == IOS_CONV) {
       need(tile >= 0 && tile < TC_COUNT, "conv tile shape out of range");
-      op.tcfg = tile;
+      need(conv_tile_ok(op, tile), "pipelined tile shape not applicable to this conv");
     } else if (op.d.kind == IOS_SEPCONV) {
       need(sep_tile_ok(op, tile), "SEPCONV tile choice out of range or not applicable to this unit");
-      op.sep_tile = tile;
     } else {
       need(tile == 0, "this unit kind has no tile choice (tile must be 0)");
     }
+    ensure_device(g);
+    if (op.d.kind == IOS_CONV) op.tcfg = tile;
+    else if (op.d.kind == IOS_SEPCONV) op.sep_tile = tile;
     op.xcd_lg = xcd_lg;
   });
 }
@@ -354,7 +356,8 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
             const int cur = get(kn);
             int keep = cur;
             for (int v = kn.lo; v <= kn.hi; ++v) {
-              if (v == cur || (kn.sep && !sep_tile_ok(g->ops[kn.ops[0]], v))) continue;
+              if (v == cur || (kn.sep ? !sep_tile_ok(g->ops[kn.ops[0]], v) : !conv_tile_ok(g->ops[kn.ops[0]], v)))
+                continue;
               set(kn, v);
               const int64_t ns = measure();
               if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {

@@ -24,7 +24,7 @@
 
 namespace ios {
 
-int choose_conv_tile(int64_t M, int N);
+int choose_conv_tile(int64_t M, int N, bool pipe_ok);
 
 static int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 static int round_up(int a, int b) { return (a + b - 1) / b * b; }
@@ -274,8 +274,10 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     int largest = ops[0];
     for (int i : ops)
       if (op_flops(g, g->ops[i]) > op_flops(g, g->ops[largest])) largest = i;
-    d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total)
+    const bool pipe_ok = pipe_conv_ok(o0.cin, KH * KW, o0.d.pre_relu);
+    d.tcfg = std::getenv("IOS_CONV_TILE") ? choose_conv_tile((int64_t)g->batch * o0.ho * o0.wo, total, pipe_ok)
                                            : g->ops[largest].tcfg;
+    if (tile_is_pipe(d.tcfg) && !pipe_ok) d.tcfg = TC_16x32_K8;   // the merged window has more than 32 taps
     int nb = 0;
     if (tile_is_pipe(d.tcfg)) {
       pack_conv_pipe(wm.data(), total, o0.cin, KH, KW, mw, &d.NG);
@@ -290,6 +292,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.w_bytes = (int32_t)(mw.size() * sizeof(float));
     dops.push_back(d);
   } else if (strategy == IOS_CONCURRENT) {
+    // a pipelined conv tile's LDS rings beside the stage table must fit a
+    // workgroup; in a stage of very many operators such a conv takes 16x32
+    const int n_ops = (int)ops.size();
+    const bool pipe_fits = (kSlotWords + ((4 + n_ops + 1 + 3) & ~3) + n_ops * kDevOpWords) * (int)sizeof(int32_t) +
+                               pipe_lds_bytes(TC_W128x64) <= kMaxLdsBytes;
     for (size_t i = 0; i < ops.size(); ++i) {
       const Op &o = g->ops[ops[i]];
       DevOp d{};
@@ -303,7 +310,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
         case IOS_CONV:
           d.kind = DK_CONV; d.tcfg = o.tcfg; d.CinP = o.CinP; d.Npad = o.Npad;
           d.bias = o.d_bias;
-          if (tile_is_pipe(o.tcfg)) {
+          if (tile_is_pipe(d.tcfg) && !pipe_fits) d.tcfg = TC_16x32_K8;
+          if (tile_is_pipe(d.tcfg)) {
             d.NG = o.pipe_nkb;
             d.pipe_ldw = round_up(o.d.cout, 128);
             d.wpk = o.d_wg;

@@ -354,6 +354,11 @@ static T *upload(const std::vector<T> &v) {
   return p;
 }
 
+bool conv_tile_ok(const Op &op, int cfg) {
+  return cfg >= 0 && cfg < TC_COUNT &&
+         (!tile_is_pipe(cfg) || pipe_conv_ok(op.cin, op.d.kh * op.d.kw, op.d.pre_relu));
+}
+
 bool sep_tile_ok(const Op &op, int tile) {
   if (tile < 0 || tile >= kSepTiles) return false;
   if (tile < kSepStagedTiles)
@@ -373,18 +378,19 @@ static int choose_sep_tile(const Op &op) {
   return sep_tile_ok(op, v) ? v : 0;
 }
 
-// Conv tile shape for an M x N output before measurement.  IOS_CONV_TILE=<0..5>
+// Conv tile shape for an M x N output before measurement.  IOS_CONV_TILE=<0..8>
 // in the environment (read when a graph is finalized or a merged stage is
-// built) forces one shape for every conv, for tuning and for tests.
+// built) forces one shape for every conv, for tuning and for tests; a
+// pipelined shape is forced only on convs it applies to (pipe_ok).
 // Tuning: warm-up time before the first measurement, and the fraction of the
 // fastest time within which a conv tile shape with fewer workgroups is taken.
 constexpr int kTuneWarmMs = 50;
 constexpr double kTuneSlack = 0.03;
 
-int choose_conv_tile(int64_t M, int N) {
+int choose_conv_tile(int64_t M, int N, bool pipe_ok) {
   if (const char *e = std::getenv("IOS_CONV_TILE")) {
     int v = std::atoi(e);
-    if (v >= 0 && v < TC_COUNT) return v;
+    if (v >= 0 && v < TC_COUNT && (pipe_ok || !tile_is_pipe(v))) return v;
   }
   int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
   int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
@@ -406,7 +412,8 @@ void finalize_graph(ios_graph *g) {
     if (op.d.kind == IOS_CONV) {
       op.CinP = round_up(op.cin, 4);
       op.Npad = round_up(op.d.cout, 16);
-      op.tcfg = choose_conv_tile((int64_t)g->batch * op.ho * op.wo, op.d.cout);
+      op.tcfg = choose_conv_tile((int64_t)g->batch * op.ho * op.wo, op.d.cout,
+                                 pipe_conv_ok(op.cin, op.d.kh * op.d.kw, op.d.pre_relu));
     } else if (op.d.kind == IOS_SEPCONV) {
       op.CinP = round_up(op.cin, 16);
       op.Npad = round_up(op.d.cout, 16);
@@ -514,6 +521,7 @@ void ensure_device(ios_graph *g) {
       const int64_t M = (int64_t)g->batch * op.ho * op.wo;
       std::vector<std::pair<int64_t, int>> meas;   // (ns, cfg)
       for (int cfg = 0; cfg < TC_COUNT; ++cfg) {
+        if (!conv_tile_ok(op, cfg)) continue;
         op.tcfg = cfg;
         meas.push_back({profile_stage(g, {oi}, IOS_CONCURRENT, 3, 20, 5), cfg});
       }

@@ -52,11 +52,16 @@ enum TileCfg : int32_t {
   TC_64x64_K2 = 4,   // FM2 FN2 WM2 WN2 WK2
   TC_128x64 = 5,     // FM2 FN2 WM4 WN2 WK1
   // pipelined tiles (see the stage kernel): 8 waves of 32x32 outputs on
-  // v_mfma_f32_32x32x2_f32, operands staged in LDS by direct loads
+  // v_mfma_f32_32x32x2_f32, operands staged in LDS by direct loads; first
+  // through one ring shared by the workgroup (a barrier per block) ...
   TC_P128x64 = 6,    // 4 (pixels) x 2 (channels) waves
   TC_P256x32 = 7,    // 8 x 1
   TC_P64x128 = 8,    // 2 x 4
-  TC_COUNT = 9,
+  // ... then through a private ring per wave (no barrier)
+  TC_W128x64 = 9,
+  TC_W256x32 = 10,
+  TC_W64x128 = 11,
+  TC_COUNT = 12,
 };
 static_assert(TC_COUNT == IOS_CONV_TILE_SHAPES, "tile shapes of the public API");
 
@@ -74,8 +79,12 @@ inline TileShape tile_shape(int cfg) {
 // Tile shapes the light kernel variant contains (one 16-pixel block per wave).
 inline bool tile_is_light(int cfg) { return cfg == TC_16x16_K8 || cfg == TC_16x32_K8; }
 inline bool tile_is_pipe(int cfg) { return cfg >= TC_P128x64 && cfg < TC_COUNT; }
-// pipelined tiles: waves along pixels and along channels
-inline int pipe_wm(int cfg) { return cfg == TC_P128x64 ? 4 : cfg == TC_P256x32 ? 8 : 2; }
+inline bool tile_is_wave_ring(int cfg) { return cfg >= TC_W128x64 && cfg < TC_COUNT; }
+// pipelined tiles: waves along pixels (and kWaves / that along channels)
+inline int pipe_wm(int cfg) {
+  const int k = tile_is_wave_ring(cfg) ? cfg - TC_W128x64 : cfg - TC_P128x64;
+  return k == 0 ? 4 : k == 1 ? 8 : 2;
+}
 inline int tile_bm(int cfg) {
   if (tile_is_pipe(cfg)) return 32 * pipe_wm(cfg);
   TileShape s = tile_shape(cfg);
@@ -86,13 +95,26 @@ inline int tile_bn(int cfg) {
   TileShape s = tile_shape(cfg);
   return 16 * s.fn * s.wn;
 }
-// Pipelined tiles: reduction blocks of kPipeKB (tap, channel) pairs, a ring of
-// kPipeStages blocks of both operands in LDS; weights packed [k][round128(Cout)]
-// with k = (u kw + v) Cin + c, zero past K and Cout.
+// Pipelined tiles: reduction blocks of kPipeKB channels of one tap, a ring of
+// kPipeStages blocks of both operands in LDS (per workgroup or per wave);
+// weights packed [k][round128(Cout)]
+// with k = (u kw + v) Cin + c, zero past Cout.  They apply to convs whose Cin
+// is a multiple of kPipeKB (a block never spans two taps), with at most 32
+// taps (one bit per tap in a lane's mask) and no input ReLU (the operands
+// reach LDS through no register).
 constexpr int kPipeKB = 16;
-constexpr int kPipeStages = 5;
+constexpr int kPipeStages = 4;
+// Per-wave rings: blocks of kWaveKB channels, kWaveStages slots (64 KB per
+// workgroup, so that two workgroups fit on a CU).
+constexpr int kWaveKB = 8;
+constexpr int kWaveStages = 4;
 inline int pipe_lds_bytes(int cfg) {
+  if (tile_is_wave_ring(cfg))                        // a ring per wave: A and B of each slot
+    return kWaves * kWaveStages * 2 * kWaveKB * 32 * (int)sizeof(float);
   return kPipeStages * kPipeKB * (tile_bm(cfg) + tile_bn(cfg)) * (int)sizeof(float);
+}
+inline bool pipe_conv_ok(int cin, int taps, int pre_relu) {
+  return cin > 0 && cin % kPipeKB == 0 && taps <= 32 && !pre_relu;
 }
 
 // SEPCONV tile: BM = 16 << tile consecutive output pixels of one image x
@@ -123,6 +145,7 @@ SepGeom sep_geometry(int tile, int cin, int cout, int w, int ho, int wo, int kh,
 // Whether SEPCONV tile choice `tile` can run `op` (graph.cpp).
 struct Op;
 bool sep_tile_ok(const Op &op, int tile);
+bool conv_tile_ok(const Op &op, int cfg);
 __host__ __device__ inline int sep_pitch(int bm) { return (bm & 31) == 16 ? bm : bm + 16; }
 // Row tile: the depthwise window padded to K x K, K = 3 or 5 (0 = too
 // large); its weights packed [CinP][sep_kkp(K)].

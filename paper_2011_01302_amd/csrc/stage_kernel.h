@@ -355,29 +355,37 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
-template <int MAX>
-__device__ __forceinline__ void wait_vmcnt_upto(int n) {   // n <= MAX, uniform
-  if constexpr (MAX > 0) {
-    if (n >= MAX) { wait_vmcnt<MAX>(); return; }
-    wait_vmcnt_upto<MAX - 1>(n);
-  } else {
-    wait_vmcnt<0>();
-  }
+// Workgroup barrier for loops that keep direct-to-LDS loads in flight across
+// it.  __syncthreads() carries a release fence, for which the compiler waits
+// for every load in flight (vmcnt(0)), which would drain the whole ring at
+// each block.  Here each wave has already waited for its own loads of the
+// block about to be read (explicit vmcnt), and its LDS reads are complete
+// (lgkmcnt(0)); the memory clobber keeps the compiler from moving LDS
+// accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Implicit-GEMM convolution tile with both operands staged in LDS through a
-// pipeline of direct global -> LDS loads: BM = 32 WMW output pixels (over the
+// ring of direct global -> LDS loads: BM = 32 WMW output pixels (over the
 // whole batch, flattened) x BN = 32 WNW output channels, 8 waves of one
 // 32x32 block each on v_mfma_f32_32x32x2_f32 (output channels as rows,
 // pixels as columns).  The reduction index k = (u kw + v) Cin + c runs in
-// blocks of KB = kPipeKB; a ring of kPipeStages block slots holds, per
+// blocks of KB = kPipeKB channels of one tap (Cin is a multiple of KB, so
+// a block never spans two taps).  A ring of kPipeStages slots holds, per
 // block, the weights [KB][BN] (rows of the packed [k][n] matrix) and the
-// im2col'd input [KB][BM] (per lane: one pixel, the tap and channel of the
-// row; taps outside the image read 0).  kPipeStages - 1 blocks are in flight
-// while one is multiplied, so the loads' latency is hidden behind the MFMAs
-// of the blocks before them; one barrier per block.  The writes to LDS go
-// through no register and the compiler does not see them: every wave counts
-// its own loads (vmcnt) and the barrier publishes them.
+// im2col'd input [KB][BM]; kPipeStages - 1 blocks are in flight while one
+// is multiplied, one barrier per block.
+//
+// Every load's address is a per-lane part fixed for a tap (the pixel's tap
+// offset, or an out-of-range marker where the tap falls outside the image,
+// which the buffer range check turns into 0) plus a uniform part in the
+// scalar offset (the channel row, or the block's weight rows), which the
+// range check does not cover: a lane either reads an element of the input
+// or 0.  The walk over (tap, channel) is scalar; per block a wave spends no
+// vector instruction on addresses.  The writes to LDS go through no
+// register and the compiler does not see them: every wave counts its own
+// loads (vmcnt) and the barrier publishes them.
 template <int WMW, bool COH>
 __device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
   constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, KB = kPipeKB, D = kPipeStages;
@@ -385,80 +393,100 @@ __device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op,
   constexpr int A_DMA = KB * BN / 64 / kWaves, B_DMA = KB * BM / 64 / kWaves, PER = A_DMA + B_DMA;
   static_assert(A_DMA * 64 * kWaves == KB * BN && B_DMA * 64 * kWaves == KB * BM, "whole copies");
   static_assert(B_DMA == 2 * HB, "each wave stages two rows of the input block");
+  static_assert((D & (D - 1)) == 0 && (D - 2) * PER < 64, "ring of 2^n slots; vmcnt is 6 bits");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WMW, wn = wave / WMW;
   const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo, H = o.H, W = o.W, HW = H * W;
-  const int Cin = o.Cin, kh = o.kh, kw = o.kw, K = Cin * kh * kw, nkb = o.NG, ldw = o.pipe_ldw;
+  const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo, H = o.H, W = o.W;
+  const int Cin = o.Cin, kw = o.kw, nkb = o.NG, ldw = o.pipe_ldw;
+  const int hw4 = H * W * 4;
   float *aring = lds, *bring = lds + D * KB * BN;
 
   // this lane's pixels of the input block (segment h: pixel m0 + 64 h + lane):
-  // offset of tap (0, 0) of channel 0, and the tap rows / columns in the image
-  int pbase[HB], rmask[HB], cmask[HB];
+  // offset of tap (0, 0) of channel 0, and the taps inside the image (bit u kw + v)
+  int pbase[HB];
+  uint32_t tmask[HB];
 #pragma unroll
   for (int h = 0; h < HB; ++h) {
     const int m = m0 + 64 * h + lane;
-    pbase[h] = 0; rmask[h] = 0; cmask[h] = 0;
+    pbase[h] = 0;
+    tmask[h] = 0;
     if (m < M) {
       const int img = fdiv(m, o.fd_howo), r = m - img * howo, oh = fdiv(r, o.fd_wo), ow = r - oh * Wo;
       const int ih0 = oh * o.sh - o.ph, iw0 = ow * o.sw - o.pw;
       pbase[h] = ((img * o.in_ctot[0] + o.in_coff[0]) * H + ih0) * W + iw0;
-      for (int u = 0; u < kh; ++u) rmask[h] |= (ih0 + u >= 0 && ih0 + u < H) << u;
-      for (int v = 0; v < kw; ++v) cmask[h] |= (iw0 + v >= 0 && iw0 + v < W) << v;
+      uint32_t cm = 0;
+      for (int v = 0; v < kw; ++v) cm |= (uint32_t)(iw0 + v >= 0 && iw0 + v < W) << v;
+      for (int u = 0; u < o.kh; ++u)
+        if (ih0 + u >= 0 && ih0 + u < H) tmask[h] |= cm << (u * kw);
     }
   }
-  // biases of this lane's accumulator rows
-  float bias[16];
+  // per lane, byte offset of its weight element in each of its copies of a block
+  int aoff[A_DMA];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    bias[r] = n < o.Cout ? o.bias[n] : 0.f;
+  for (int i = 0; i < A_DMA; ++i) {
+    const int f = (wave * A_DMA + i) * 64 + lane;
+    aoff[i] = ((f / BN) * ldw + n0 + f % BN) * 4;
   }
   const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
 
-  auto issue = [&](int kb) {
-    const int slot = kb % D;
-    float *a = aring + slot * KB * BN, *b = bring + slot * KB * BM;
+  // scalar walk of the next block to issue: tap (u, v), first channel c
+  int tap = 0, tu = 0, tv = 0, c = 0;
+  int toff[HB];
+  auto set_tap = [&]() {
 #pragma unroll
-    for (int i = 0; i < A_DMA; ++i) {
-      const int sg = wave * A_DMA + i, f = sg * 64 + lane, r = f / BN, col = f % BN;
-      lds_dma(wr, a + sg * 64, ((kb * KB + r) * ldw + n0 + col) * 4);
-    }
+    for (int h = 0; h < HB; ++h) toff[h] = (tmask[h] >> tap) & 1 ? (pbase[h] + tu * W + tv) * 4 : kOOB;
+  };
+  set_tap();
+  auto issue = [&](int kb) {
+    const int slot = kb & (D - 1);
+    float *a = aring + slot * KB * BN, *b = bring + slot * KB * BM;
+    const int wsoff = kb * KB * ldw * 4;
+#pragma unroll
+    for (int i = 0; i < A_DMA; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void *)(a + (wave * A_DMA + i) * 64), 4, aoff[i], wsoff, 0, 0);
 #pragma unroll
     for (int i = 0; i < B_DMA; ++i) {
       const int r = 2 * wave + i / HB, h = i % HB;   // block row, 64-pixel segment
-      const int k = kb * KB + r;
-      const int tap = fdiv(k, o.fd_cin), c = k - tap * Cin, u = fdiv(tap, o.fd_kw), v = tap - u * kw;
-      const bool ok = k < K && ((rmask[h] >> u) & (cmask[h] >> v) & 1);
-      lds_dma(xr, b + r * BM + h * 64, ok ? (pbase[h] + c * HW + u * W + v) * 4 : kOOB);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(b + r * BM + h * 64), 4, toff[h], (c + r) * hw4, 0, 0);
+    }
+    c += KB;
+    if (c == Cin) {                                  // uniform: next tap
+      c = 0;
+      ++tap;
+      if (++tv == kw) { tv = 0; ++tu; }
+      set_tap();
     }
   };
 
   floatx16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  const bool relu_in = o.pre_relu != 0;
   for (int kb = 0; kb < D - 1 && kb < nkb; ++kb) issue(kb);
+  const float *a_l = aring + (lane >> 5) * BN + wn * 32 + (lane & 31);
+  const float *b_l = bring + (lane >> 5) * BM + wm * 32 + (lane & 31);
   for (int kb = 0; kb < nkb; ++kb) {
     // this wave's loads of block kb have landed once at most those of the
     // blocks issued after it are in flight; the barrier makes every wave's
     // visible and guarantees that block kb - 1's slot is no longer read
-    wait_vmcnt_upto<(D - 2) * PER>(min(D - 2, nkb - 1 - kb) * PER);
-    __syncthreads();
+    if (kb + D - 2 < nkb) wait_vmcnt<(D - 2) * PER>();
+    else wait_vmcnt<0>();
+    ring_barrier();
     if (kb + D - 1 < nkb) issue(kb + D - 1);
-    const float *a = aring + (kb % D) * KB * BN + (lane >> 5) * BN + wn * 32 + (lane & 31);
-    const float *b = bring + (kb % D) * KB * BM + (lane >> 5) * BM + wm * 32 + (lane & 31);
+    const int slot = kb & (D - 1);
+    const float *a = a_l + slot * KB * BN, *b = b_l + slot * KB * BM;
     float av[KB / 2], bv[KB / 2];
 #pragma unroll
     for (int p = 0; p < KB / 2; ++p) {
       av[p] = a[2 * p * BN];
       bv[p] = b[2 * p * BM];
     }
+    __builtin_amdgcn_sched_barrier(0);               // every read of the block in flight before the first MFMA
 #pragma unroll
-    for (int p = 0; p < KB / 2; ++p) acc = mfma32x32x2(av[p], relu_in ? fmaxf(bv[p], 0.f) : bv[p], acc);
+    for (int p = 0; p < KB / 2; ++p) acc = mfma32x32x2(av[p], bv[p], acc);
   }
   // epilogue: element r of lane l is channel n0 + 32 wn + 8 (r/4) + 4 (l/32) + r%4 of pixel m0 + 32 wm + l%32
   const int m = m0 + wm * 32 + (lane & 31);
@@ -468,7 +496,122 @@ __device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op,
     for (int r = 0; r < 16; ++r) {
       const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (n < o.Cout) {
-        float v = acc[r] + bias[r];
+        float v = acc[r] + o.bias[n];
+        if (o.post_relu) v = fmaxf(v, 0.f);
+        st<COH>(route_ptr(sl, op, o, n, img, pix, howo), v);
+      }
+    }
+  }
+}
+
+// Implicit-GEMM convolution tile in which every wave streams its own
+// operands through a private ring in LDS: BM = 32 WMW output pixels (over
+// the whole batch, flattened) x BN = 32 WNW output channels, 8 waves of one
+// 32x32 block each on v_mfma_f32_32x32x2_f32 (output channels as rows,
+// pixels as columns).  The reduction index k = (u kw + v) Cin + c runs in
+// blocks of KB = kWaveKB channels of one tap (Cin is a multiple of KB, so a
+// block never spans two taps).  Per block a wave copies, with direct
+// global -> LDS loads, its weights A[32 ch][KB] and its im2col'd input
+// B[KB][32 px]: one load per k-pair and operand, lane i fetching the element
+// (k = 2 p + i / 32, ch or px = i % 32) that lane i of the MFMA of k-pair p
+// supplies, so the operand reads are conflict-free.  Each wave keeps
+// kWaveStages - 1 blocks in flight while it multiplies one and waits only for
+// its own loads (vmcnt): there is no barrier in the reduction, and the two
+// waves of a SIMD run independently, each hiding the other's waits.
+//
+// Every load's address is a per-lane part (the pixel's offset for the tap,
+// or an out-of-range marker where the tap falls outside the image, which the
+// buffer range check turns into 0; the weight column) plus a uniform part in
+// the scalar offset (the channel row; the block's weight rows), which the
+// range check does not cover: a lane reads an element of its tensor or 0.
+// The walk over (tap, channel) is scalar, so a block costs a wave no vector
+// instruction for addresses.  The writes to LDS go through no register and
+// the compiler does not see them: the memory clobbers order the reads.
+template <int WMW, bool COH>
+__device__ __forceinline__ void conv_wave_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, KB = kWaveKB, D = kWaveStages;
+  static_assert(kPipeKB % KB == 0, "weights packed in blocks of kPipeKB rows");
+  constexpr int NP = KB / 2;                         // k-pairs (MFMAs) per block
+  constexpr int SLOT = 2 * NP * 64;                  // floats per slot: A then B, 64 per k-pair
+  static_assert((D - 2) * 2 * NP < 64, "vmcnt is 6 bits");
+  const int tid = threadIdx.x, lane = tid & 63, kq = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % WMW, wn = wave / WMW;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
+  const int Wo = o.Wo, howo = o.Ho * Wo, M = o.N * howo, H = o.H, W = o.W;
+  const int Cin = o.Cin, kw = o.kw, nkb = o.NG * (kPipeKB / KB), ldw = o.pipe_ldw, hw4 = H * W * 4;
+  const int m = tm * BM + wm * 32 + l32, n0 = tn * BN + wn * 32;
+  float *ring = lds + wave * D * SLOT;
+
+  // this lane's pixel: offset of tap (0, 0) in channel kq, taps inside the
+  // image (bit u kw + v); its weight column in channel row kq
+  int pbase = 0;
+  uint32_t tmask = 0;
+  if (m < M) {
+    const int img = fdiv(m, o.fd_howo), r = m - img * howo, oh = fdiv(r, o.fd_wo), ow = r - oh * Wo;
+    const int ih0 = oh * o.sh - o.ph, iw0 = ow * o.sw - o.pw;
+    pbase = ((img * o.in_ctot[0] + o.in_coff[0] + kq) * H + ih0) * W + iw0;
+    uint32_t cm = 0;
+    for (int v = 0; v < kw; ++v) cm |= (uint32_t)(iw0 + v >= 0 && iw0 + v < W) << v;
+    for (int u = 0; u < o.kh; ++u)
+      if (ih0 + u >= 0 && ih0 + u < H) tmask |= cm << (u * kw);
+  }
+  const int aoff = (kq * ldw + n0 + l32) * 4;
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
+
+  // scalar walk of the next block to issue: tap (u, v), first channel c
+  int tap = 0, tu = 0, tv = 0, c = 0;
+  int toff = tmask & 1 ? pbase * 4 : kOOB;
+  auto issue = [&](int kb) {
+    float *s = ring + (kb & (D - 1)) * SLOT;
+    const int wrow = kb * KB * ldw * 4;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void *)(s + p * 64), 4, aoff, wrow + 2 * p * ldw * 4, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(s + (NP + p) * 64), 4, toff, (c + 2 * p) * hw4, 0, 0);
+    }
+    c += KB;
+    if (c == Cin) {                                  // uniform: next tap
+      c = 0;
+      ++tap;
+      if (++tv == kw) { tv = 0; ++tu; }
+      toff = (tmask >> tap) & 1 ? (pbase + tu * W + tv) * 4 : kOOB;
+    }
+  };
+
+  floatx16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int kb = 0; kb < D - 1 && kb < nkb; ++kb) issue(kb);
+  for (int kb = 0; kb < nkb; ++kb) {
+    // block kb has landed once at most the blocks issued after it are in
+    // flight; its slot's reads below come after the wait
+    if (kb + D - 2 < nkb) wait_vmcnt<(D - 2) * 2 * NP>();
+    else wait_vmcnt<0>();
+    asm volatile("" ::: "memory");
+    // block kb - 1's slot was read (and consumed) in the previous round
+    if (kb + D - 1 < nkb) issue(kb + D - 1);
+    const float *s = ring + (kb & (D - 1)) * SLOT + lane;
+    float av[NP], bv[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      av[p] = s[p * 64];
+      bv[p] = s[(NP + p) * 64];
+    }
+    __builtin_amdgcn_sched_barrier(0);               // every read of the block in flight before the first MFMA
+#pragma unroll
+    for (int p = 0; p < NP; ++p) acc = mfma32x32x2(av[p], bv[p], acc);
+    asm volatile("" ::: "memory");
+  }
+  // epilogue: element r of lane l is channel n0 + 8 (r/4) + 4 (l/32) + r%4 of pixel m
+  if (m < M) {
+    const int img = fdiv(m, o.fd_howo), pix = m - img * howo;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = n0 + 8 * (r >> 2) + 4 * kq + (r & 3);
+      if (n < o.Cout) {
+        float v = acc[r] + o.bias[n];
         if (o.post_relu) v = fmaxf(v, 0.f);
         st<COH>(route_ptr(sl, op, o, n, img, pix, howo), v);
       }
@@ -1103,7 +1246,10 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
           switch (o.tcfg) {
             case TC_P128x64: conv_pipe_tile<4, COH>(sl, op, o, ti, lds); break;
             case TC_P256x32: conv_pipe_tile<8, COH>(sl, op, o, ti, lds); break;
-            default: conv_pipe_tile<2, COH>(sl, op, o, ti, lds); break;
+            case TC_P64x128: conv_pipe_tile<2, COH>(sl, op, o, ti, lds); break;
+            case TC_W128x64: conv_wave_tile<4, COH>(sl, op, o, ti, lds); break;
+            case TC_W256x32: conv_wave_tile<8, COH>(sl, op, o, ti, lds); break;
+            default: conv_wave_tile<2, COH>(sl, op, o, ti, lds); break;
           }
           break;
         }
@@ -1124,7 +1270,7 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
         break;
       }
     case DK_SEP:
-      if constexpr (KV != KV_LIGHT) {
+      if constexpr (KV == KV_SEP || KV == KV_SEPROW || KV == KV_FULL) {
         if (!o.sep_row) {
           if constexpr (KV != KV_SEPROW) sep_tile<COH>(sl, op, o, ti, lds);
         } else if constexpr (KV != KV_SEP) {

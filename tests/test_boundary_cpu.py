@@ -244,6 +244,9 @@ def test_graph_error_paths():
     expect("IOS_E_ARG", I.ios_get_conv_tile, g, x)                            # not a unit
     expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, I.IOS_CONV_TILE_SHAPES)
     expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, -1)
+    for pipelined in range(6, 12):                                            # 4 input channels, not 16k
+        expect("IOS_E_ARG", I.ios_set_conv_tile, g, c, pipelined)
+        expect("IOS_E_ARG", I.ios_set_unit_tiling, g, c, pipelined, -1)
     # per-stage tile choice: argument errors come before any device work
     q = I.ios_schedule_from_stages(g, [[c]], [I.IOS_CONCURRENT])
     o = I.ios_sched_opts_default()

@@ -159,7 +159,7 @@ def test_parity_operator_merge(config, groups):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6", "7", "8"])
+@pytest.mark.parametrize("tile", [str(t) for t in range(12)])
 def test_parity_every_conv_tile_shape(tile, monkeypatch):
     monkeypatch.setenv("IOS_CONV_TILE", tile)
     for config in ["tiny", "inception", "squeeze"]:
@@ -498,7 +498,7 @@ def test_chained_stage_back_to_back_on_different_inputs():
 
 # ------------------------------------------------------------------ ragged shapes
 
-def ragged_spec(batch):
+def ragged_spec(batch, cin=13):
     conv = lambda n, i, co, k, s, p, post=1: {"name": n, "kind": "conv", "in": [i], "cout": co,
                                              "kh": k[0], "kw": k[1], "sh": s, "sw": s, "ph": p[0],
                                              "pw": p[1], "pre_relu": 0, "post_relu": post}
@@ -523,18 +523,20 @@ def ragged_spec(batch):
            {"name": "mn", "kind": "mean", "in": ["c2", "c2", "c2"]},
            {"name": "cat", "kind": "concat", "in": ["c3", "c4"]},
            {"name": "cat2", "kind": "concat", "in": ["c5", "mp"]}]
-    return {"name": "ragged", "batch": batch, "inputs": [{"name": "x", "c": 13, "h": 9, "w": 11}],
+    return {"name": "ragged", "batch": batch, "inputs": [{"name": "x", "c": cin, "h": 9, "w": 11}],
             "ops": ops, "outputs": ["ad", "mn", "cat", "cat2", "s3", "s4"]}
 
 
 # tile None: shapes chosen by measurement, else forced; offset: inputs start
-# 1 or 3 floats past a 16-byte boundary
+# 1 or 3 floats past a 16-byte boundary; the pipelined shapes (6 .. 11) need
+# input channels in multiples of 16, so their cases take 32
 @pytest.mark.parametrize("batch,tile,offset", [(1, None, 0), (2, None, 0), (1, "1", 1), (1, "0", 3),
-                                               (2, "4", 1), (2, "6", 1), (3, "7", 0), (1, "8", 3)])
+                                               (2, "4", 1), (2, "6", 1), (3, "7", 0), (1, "8", 3),
+                                               (2, "9", 3), (3, "10", 1), (1, "11", 0)])
 def test_parity_ragged_shapes(batch, tile, offset, monkeypatch):
     if tile is not None:
         monkeypatch.setenv("IOS_CONV_TILE", tile)
-    spec = ragged_spec(batch)
+    spec = ragged_spec(batch, 32 if tile is not None and int(tile) >= 6 else 13)
     ten = W.make_tensors(spec, 3)
     ref = E.outputs(spec, ten)
     g = I.Graph(spec, ten)
@@ -580,7 +582,7 @@ def test_parity_pool_planes(batch):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "4", "6", "7", "8"])
+@pytest.mark.parametrize("tile", ["0", "1", "4", "6", "7", "8", "9", "10", "11"])
 def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     """Forced conv tile shapes over several small images (the 16-pixel
     blocks of an 8x8 plane never span two images)."""

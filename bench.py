@@ -201,6 +201,20 @@ def load_traffic(workload, sha):
     return d.get("traffic_bytes_per_launch")
 
 
+def recorded_plan(config, batch):
+    """The plan recorded under profiles/ for this configuration (schedule and
+    tuning choices of a DP search on an MI355X, with the kernel sources it
+    was taken with), or (None, None) when there is none for the current
+    sources."""
+    p = os.path.join(ROOT, "profiles", f"plan_{config}_bs{batch}.json")
+    if not os.path.exists(p):
+        return None, None
+    plan = [json.loads(l) for l in open(p) if l.startswith("{") and '"tiling"' in l][-1]
+    if plan.get("kernel_sha") != kernel_sha():
+        return None, None
+    return plan, p
+
+
 def load_trace(workload, sha):
     """Kernel-trace summary of the same plan (profiles/trace_<workload>.json)
     when it was taken from the current kernel sources."""
@@ -671,9 +685,14 @@ def run_network(args):
             o = I.ios_sched_opts_default()
             o.mode = mode
             o.r, o.s = args.r, args.s
-            if net in ("randwire_net", "nasnet_net"):   # tens of thousands of candidate stages per block
+            if net in ("randwire_net", "nasnet_net"):
+                # tens of thousands of candidate stages per block at r = 3:
+                # r = 1 (the paper's Sec. 7.1 finds it close to the full
+                # search; so do the single-block sweeps here) and light
+                # profiling, the picked stages then measured in full
+                o.r = 1
                 o.warmup, o.reps, o.repeats = 1, 3, 1
-                o.verify_reps = 20                      # the picked stages measured in full
+                o.verify_reps = 20
             print(f"[network] {net}: {name} schedule", file=sys.stderr, flush=True)
             for u, t in iso.items():
                 I.ios_set_conv_tile(g.handle, u, t)
@@ -853,6 +872,11 @@ def main():
                          "added per-launch cost would change the search's choices")
     ap.add_argument("--save-plan", default="", metavar="PLAN_JSON",
                     help="write the headline's schedule and tuning choices here (for --plan-from)")
+    ap.add_argument("--search", action="store_true",
+                    help="always search: by default a configuration whose plan was recorded under "
+                         "profiles/ (plan_<config>_bs<batch>.json, from a search on an MI355X with "
+                         "the current kernel sources) replays that plan, so that the number and the "
+                         "committed profiles describe the same schedule")
     ap.add_argument("--mode", choices=("dp", "sequential", "greedy"), default="dp",
                     help="schedule of the timed step: the DP search (default) or a baseline "
                          "(with --plan-from: that run's tile shapes, this mode's schedule)")
@@ -903,9 +927,13 @@ def main():
     import workloads as W
 
     print(f"[bench] config={args.config} batch={args.batch} seed={args.seed}", file=sys.stderr, flush=True)
-    plan = None
+    plan, plan_src = None, None
+    if not args.plan_from and not args.search:
+        plan, plan_src = recorded_plan(args.config, args.batch)
     if args.plan_from:
         plan = [json.loads(l) for l in open(args.plan_from) if l.startswith("{") and '"tiling"' in l][-1]
+        plan_src = args.plan_from
+    if plan is not None:
         if args.mode != "dp":
             # a baseline schedule of the same kernels, with the plan's tile choices
             spec, g, ins, outs = _setup(I, W, torch, args.config, args.batch, args.seed)
@@ -928,7 +956,10 @@ def main():
         I.ios_schedule_dump_costs(g.handle, args.dump_costs)
     if args.save_plan:
         with open(args.save_plan, "w") as f:
-            f.write(json.dumps({k: head[k] for k in ("config", "batch", "schedule", "tiling", "search")}) + "\n")
+            rec = {k: head[k] for k in ("config", "batch", "schedule", "tiling", "search")}
+            rec["kernel_sha"] = kernel_sha()
+            rec["us_when_searched"] = head["us"]
+            f.write(json.dumps(rec) + "\n")
     us = head["us"]
     n_launch = head["launches"]
 
@@ -969,6 +1000,8 @@ def main():
         "schedule": head.get("stages", head["schedule"]),
         "tiling": head["tiling"],
         "search": head["search"],
+        "plan": ("replayed from " + os.path.relpath(plan_src, ROOT)) if plan else
+                "searched in this run (DP with on-device stage profiling, then per-stage tile tuning)",
         "repeats": head["repeats"],
         "throughput_img_per_s": round(args.batch / us * 1e6, 1),
     }
@@ -984,10 +1017,12 @@ def main():
             if config == args.config:
                 continue
             steps = 100 if config in LARGE_SEARCH else 500
+            p2, src2 = (None, None) if args.search else recorded_plan(config, 1)
             _, g2, q2, i2, o2, r2 = measure_config(I, W, torch, config, 1, args.seed, steps, args.warmup, args,
-                                                   baselines=not args.no_baselines)
+                                                   plan=p2, baselines=not args.no_baselines)
+            r2["plan"] = ("replayed from " + os.path.relpath(src2, ROOT)) if p2 else "searched in this run"
             keep = ("us", "launches", "gflop", "tflops", "frac_of_fp32_mfma_peak", "repeats", "gpu_baselines",
-                    "schedule", "search")
+                    "schedule", "search", "plan")
             others[config] = {k: r2[k] for k in keep if k in r2}
             I.ios_schedule_destroy(q2)
             g2.close()

@@ -189,7 +189,10 @@ int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
  * choice (0, 1, 2: runs of 16, 32 or 64 consecutive output pixels with
  * every output channel, input rows staged in LDS; 3 .. 6: 16 pixels of one
  * output row with 1 .. 4 blocks of 16 output channels, for at most 256
- * input channels and windows up to 5 x 5), 0 for the other kinds; `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
+ * input channels and windows up to 5 x 5; 7, 8: whole output rows in 128
+ * or 64 MFMA columns x 64 or 128 output channels, for one input and a
+ * 3 x 3 or 5 x 5 window that keeps the plane size), 0 for the other kinds;
+ * `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
  * unit sends to one XCD (0, 2 or 4), or -1 to let the library's L2-fill
  * model choose (ios_schedule_tune_tiles sets both per stage).  A stage whose
  * units disagree on xcd_lg uses the model.  These are implementation
@@ -275,10 +278,11 @@ int ios_schedule_stats(const ios_schedule_t *q, int64_t *states, int64_t *transi
  * (o's warmup / reps / repeats, or the defaults when o is NULL) to pick, for
  * every stage, (1) how its tiles are spread over the 8 XCDs (runs of 1, 4 or
  * 16 consecutive tiles per XCD, else the library's L2-fill model) and (2) the
- * tile shapes of its convs and the 16-channel output blocks per tile of its
- * SEPCONVs in that stage's company: one operator at a time, each value
- * tried, a change kept when the stage gets more than 2% faster (two passes);
- * a merge stage's convs take one shape together.  The choices stay
+ * tile shapes of its convs and the tile choices of its SEPCONVs in that
+ * stage's company: in a concurrent stage first all its convs (all its
+ * SEPCONVs) moved to one value together, then one operator at a time, each
+ * value tried, a change kept when the stage gets more than 2% faster (two
+ * passes); a merge stage's convs take one shape together.  The choices stay
  * set on the graph's units (ios_get_conv_tile reads the shapes), so call it
  * on the schedule that will run; q's stages are recompiled on its next run.
  * A unit belongs to one stage of a schedule, so the stages do not compete.

@@ -91,6 +91,7 @@ void ios_graph_destroy(ios_graph *g) {
     if (op.d_dw_row) (void)hipFree(op.d_dw_row);
     if (op.d_pw_row) (void)hipFree(op.d_pw_row);
     if (op.d_wg) (void)hipFree(op.d_wg);
+    if (op.d_pw_pipe) (void)hipFree(op.d_pw_pipe);
   }
   CompiledStage &s = g->prof_stage;
   if (s.d_table) (void)hipFree(s.d_table);
@@ -324,13 +325,19 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
           return keep >= 0;
         };
         // knobs: the convs that take one tile shape together (all of a merge
-        // stage's), and each SEPCONV's output blocks per tile
+        // stage's), and each SEPCONV's tile choice; in a concurrent stage
+        // also all its convs, and all its SEPCONVs, moved together first (a
+        // wide stage can be bound by its operators' throughput together,
+        // which no single operator's change shows)
         struct Knob {
           std::vector<int> ops;
           bool sep;
           int lo, hi;
         };
         std::vector<Knob> knobs;
+        std::vector<int> seps;
+        for (int op : ops)
+          if (g->ops[op].d.kind == IOS_SEPCONV) seps.push_back(op);
         if (!forced && !convs.empty()) {
           if (strat == IOS_MERGE) {
             int largest = convs[0];
@@ -340,33 +347,39 @@ int ios_schedule_tune_tiles(ios_graph *g, ios_schedule_t *q, const ios_sched_opt
             best = measure();
             knobs.push_back({convs, false, 0, TC_COUNT - 1});
           } else {
+            if (convs.size() > 1) knobs.push_back({convs, false, 0, TC_COUNT - 1});
             for (int c : convs) knobs.push_back({{c}, false, 0, TC_COUNT - 1});
           }
         }
-        if (!sep_forced)
-          for (int op : ops)
-            if (g->ops[op].d.kind == IOS_SEPCONV) knobs.push_back({{op}, true, 0, kSepTiles - 1});
-        auto get = [&](const Knob &kn) { return kn.sep ? g->ops[kn.ops[0]].sep_tile : g->ops[kn.ops[0]].tcfg; };
-        auto set = [&](const Knob &kn, int v) {
-          for (int c : kn.ops) (kn.sep ? g->ops[c].sep_tile : g->ops[c].tcfg) = v;
+        if (!sep_forced) {
+          if (seps.size() > 1) knobs.push_back({seps, true, 0, kSepTiles - 1});
+          for (int op : seps) knobs.push_back({{op}, true, 0, kSepTiles - 1});
+        }
+        auto val = [&](int op, bool sep) -> int & { return sep ? g->ops[op].sep_tile : g->ops[op].tcfg; };
+        auto ok = [&](int op, bool sep, int v) {
+          return sep ? sep_tile_ok(g->ops[op], v) : conv_tile_ok(g->ops[op], v);
         };
         for (int pass = 0; pass < 2; ++pass) {
           bool improved = pass == 0 && tune_xcd_order();
           for (const auto &kn : knobs) {
-            const int cur = get(kn);
-            int keep = cur;
+            // a value applies to the knob's operators that admit it; the
+            // others keep theirs
+            std::vector<int> keep;
+            for (int c : kn.ops) keep.push_back(val(c, kn.sep));
             for (int v = kn.lo; v <= kn.hi; ++v) {
-              if (v == cur || (kn.sep ? !sep_tile_ok(g->ops[kn.ops[0]], v) : !conv_tile_ok(g->ops[kn.ops[0]], v)))
-                continue;
-              set(kn, v);
+              bool change = false;
+              for (size_t i = 0; i < kn.ops.size(); ++i) change |= ok(kn.ops[i], kn.sep, v) && keep[i] != v;
+              if (!change) continue;
+              for (size_t i = 0; i < kn.ops.size(); ++i)
+                val(kn.ops[i], kn.sep) = ok(kn.ops[i], kn.sep, v) ? v : keep[i];
               const int64_t ns = measure();
               if ((double)ns < (double)best * (1.0 - kStageTileSlack)) {
                 best = ns;
-                keep = v;
+                for (size_t i = 0; i < kn.ops.size(); ++i) keep[i] = val(kn.ops[i], kn.sep);
                 improved = true;
               }
             }
-            set(kn, keep);
+            for (size_t i = 0; i < kn.ops.size(); ++i) val(kn.ops[i], kn.sep) = keep[i];
           }
           if (!improved) break;
         }

@@ -133,6 +133,8 @@ double tile_work(const DevOp &d) {
       return (double)tile_bm(d.tcfg) * tile_bn(d.tcfg) * 16.0 * d.NG / s.wk;
     }
     case DK_SEP:
+      if (d.sep_row == 2)
+        return (double)d.sepg_rout * d.Wo * d.CinP * (d.kh * d.kw + 32.0 * (kWaves / d.sep_nbt)) / kWaves;
       if (d.sep_row) return 16.0 * d.CinP * (d.row_k * d.row_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
       return (double)d.sep_bm * d.CinP * (d.kh * d.kw + 16.0 * d.sep_nbt) / kWaves;
     default:
@@ -323,6 +325,24 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
           }
           break;
         case IOS_SEPCONV: {
+          if (o.sep_tile >= kSepgFirst) {
+            // GEMM tile (see the stage kernel)
+            const SepgGeom sg = sepg_geometry(o.sep_tile - kSepgFirst, (int)o.in.size(), o.d.kh, o.d.kw,
+                                              o.d.pad_h, o.d.pad_w, o.h, o.wd, o.ho, o.wo);
+            if (sg.bm == 0 || !o.d_pw_pipe) fail(IOS_E_UNSUPPORTED, "SEPCONV GEMM tile does not apply");
+            d.kind = DK_SEP; d.sep_row = 2;
+            d.CinP = o.CinP; d.Npad = o.Npad;
+            d.sep_nbt = sg.bm / 32;
+            d.sep_nck = o.CinP / 16;
+            d.sep_rows = sg.rows;
+            d.sepg_rout = sg.rout; d.sepg_rpl = sg.rpl; d.sepg_cr = sg.cr; d.sepg_ps = sg.ps;
+            d.sepg_xs = sg.xs; d.sepg_ws = sg.ws;
+            d.pipe_ldw = round_up(o.d.cout, 128);
+            d.wpk = o.d_pw_pipe; d.bias = o.d_bias; d.dw = o.d_dw;
+            d.w_bytes = (int32_t)((size_t)o.CinP * d.pipe_ldw * sizeof(float));
+            d.dw_bytes = (int32_t)((size_t)o.CinP * o.d.kh * o.d.kw * sizeof(float));
+            break;
+          }
           if (o.sep_tile >= kSepStagedTiles) {
             // row tile (see the stage kernel)
             if (!sep_tile_ok(o, o.sep_tile)) fail(IOS_E_UNSUPPORTED, "SEPCONV row tile does not apply");
@@ -377,6 +397,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     if (d.kind == DK_CONV) {
       d.tiles_m = cdiv(M, tile_bm(d.tcfg));
       d.tiles_n = cdiv(d.Cout, tile_bn(d.tcfg));
+    } else if (d.kind == DK_SEP && d.sep_row == 2) {
+      // GEMM tile: (image, block of sepg_rout output rows) x groups of 32 (8 / sep_nbt) channels
+      d.tiles_per_plane = cdiv(d.Ho, d.sepg_rout);
+      d.tiles_m = d.N * d.tiles_per_plane;
+      d.tiles_n = cdiv(d.Cout, 32 * (kWaves / d.sep_nbt));
     } else if (d.kind == DK_SEP && d.sep_row) {
       // row tile: (image, output row, 16-pixel block of the row) x groups of
       // sep_nbt 16-channel output blocks
@@ -435,7 +460,9 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.fd_wo = fd(d.Wo);
     d.fd_spt = fd(d.CinP / 4);
     d.fd_kw = fd(d.kw);
-    d.fd_pimg = fd(d.kind == DK_SEP && d.sep_row ? d.Ho * d.row_bpr : d.tiles_per_plane);
+    d.fd_pimg = fd(d.kind == DK_SEP && d.sep_row == 1 ? d.Ho * d.row_bpr : d.tiles_per_plane);
+    d.fd_ps = fd(d.sepg_ps);
+    d.fd_rpl = fd(d.sepg_rpl);
     d.fd_rbpr = fd(d.row_bpr);
     d.fd_cin = fd(d.Cin);
     d.fd_rw = fd(d.sep_rows * d.W);
@@ -471,8 +498,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     persistent |= d.n_deps > 0;
     big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg) && !tile_is_pipe(d.tcfg);
     has_pipe |= d.kind == DK_CONV && tile_is_pipe(d.tcfg);
-    has_sep |= d.kind == DK_SEP && !d.sep_row;
-    has_row |= d.kind == DK_SEP && d.sep_row;
+    has_sep |= d.kind == DK_SEP && d.sep_row != 1;
+    has_row |= d.kind == DK_SEP && d.sep_row == 1;
     lds = std::max(lds, op_lds_bytes(d));
   }
   cs->ops = sorted;

@@ -361,6 +361,9 @@ bool conv_tile_ok(const Op &op, int cfg) {
 
 bool sep_tile_ok(const Op &op, int tile) {
   if (tile < 0 || tile >= kSepTiles) return false;
+  if (tile >= kSepgFirst)
+    return sepg_geometry(tile - kSepgFirst, (int)op.in.size(), op.d.kh, op.d.kw, op.d.pad_h, op.d.pad_w, op.h,
+                         op.wd, op.ho, op.wo).bm != 0;
   if (tile < kSepStagedTiles)
     return sep_geometry(tile, op.cin, op.d.cout, op.wd, op.ho, op.wo, op.d.kh, op.d.kw).bm == (16 << tile);
   const int K = sep_row_window(op.d.kh, op.d.kw), nbt = tile - kSepStagedTiles + 1;
@@ -368,7 +371,7 @@ bool sep_tile_ok(const Op &op, int tile) {
          sep_row_lds_bytes(round_up(op.cin, 4), K, nbt) <= kSepMaxLds;
 }
 
-// SEPCONV tile choice before measurement (IOS_SEP_TILE=<0..6> forces one;
+// SEPCONV tile choice before measurement (IOS_SEP_TILE=<0..8> forces one;
 // a choice the operator cannot use falls back to the staged tile of 16
 // pixels).
 static int choose_sep_tile(const Op &op) {
@@ -468,6 +471,13 @@ void ensure_device(ios_graph *g) {
       op.d_dw = upload(dw);
       op.d_wpk = upload(pwk);
       op.d_bias = upload(bias);
+      // the GEMM tile's pointwise layout: [round16(cin)][round128(cout)]
+      if (sep_tile_ok(op, kSepgFirst) || sep_tile_ok(op, kSepgFirst + 1)) {
+        std::vector<float> pwp;
+        int nkb = 0;
+        pack_conv_pipe(op.w.data() + (size_t)op.cin * taps, op.d.cout, op.cin, 1, 1, pwp, &nkb);
+        op.d_pw_pipe = upload(pwp);
+      }
       // the row tile's layouts, where it applies: depthwise taps at the top
       // left of a K x K window, [CinP4][kkp(K)]; pointwise [CinP4][Npad]
       const int K = sep_row_window(op.d.kh, op.d.kw);

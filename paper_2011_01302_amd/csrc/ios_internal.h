@@ -124,10 +124,43 @@ inline bool pipe_conv_ok(int cin, int taps, int pre_relu) {
 // sizes (sep_geometry), within these limits.
 // Tile choices: 0 .. kSepStagedTiles - 1 the staged tile (BM = 16 << choice),
 // then kSepRowMaxNB choices of the row tile (16 output pixels of one output
-// row x 1 .. kSepRowMaxNB channel blocks; Cin <= 256, windows up to 5 x 5).
+// row x 1 .. kSepRowMaxNB channel blocks; Cin <= 256, windows up to 5 x 5),
+// then kSepgTiles choices of the GEMM tile (whole output rows in 128 or 64
+// MFMA columns x 64 or 128 output channels; one input, 3 x 3 or 5 x 5
+// windows that keep the size).
 constexpr int kSepStagedTiles = 3;       // BM = 16, 32, 64
 constexpr int kSepRowMaxNB = 4;
-constexpr int kSepTiles = kSepStagedTiles + kSepRowMaxNB;
+constexpr int kSepgTiles = 2;
+constexpr int kSepgFirst = kSepStagedTiles + kSepRowMaxNB;
+constexpr int kSepTiles = kSepgFirst + kSepgTiles;
+constexpr int kSepgStages = 2;           // GEMM tile: chunks of 16 input channels in LDS (one in flight)
+constexpr int kSepgMaxRun = 8;           // GEMM tile: depthwise outputs per thread and chunk at most
+constexpr int kSepgMaxCopies = 12;       // GEMM tile: 64-float input copies per wave and chunk at most
+constexpr int kSepgMaxLds = 80 * 1024;   // GEMM tile: two workgroups per CU
+// GEMM tile geometry (bm = 0: the choice does not apply).  R_out output rows
+// per tile (rout), depthwise runs per row (rpl) of cr columns, staged input
+// rows (rows), the plane pitch of the staged input (ps, odd) and the floats
+// per ring slot of the input planes (xs) and of the depthwise weights (ws).
+struct SepgGeom {
+  int bm = 0, bn = 0, rout = 0, rpl = 0, cr = 0, rows = 0, ps = 0, xs = 0, ws = 0, lds = 0;
+};
+inline SepgGeom sepg_geometry(int choice, int n_in, int kh, int kw, int ph, int pw, int H, int W, int Ho, int Wo) {
+  SepgGeom g;
+  const int wmw = choice == 0 ? 4 : 2, bm = 32 * wmw, bn = 32 * (8 / wmw);
+  if (n_in != 1 || kh != kw || (kh != 3 && kh != 5) || ph != kh / 2 || pw != kw / 2 || Ho != H || Wo != W ||
+      Wo > bm || Wo < 1)
+    return g;
+  const int rout = std::min(std::min(bm / Wo, Ho), 32), rpl = 32 / rout, cr = (Wo + rpl - 1) / rpl;
+  if (cr > kSepgMaxRun) return g;
+  const int rows = rout + kh - 1, ps = (rows * W) | 1;
+  const int xs = (16 * ps + 63) / 64 * 64, ws = (16 * kh * kw + 63) / 64 * 64;
+  if (xs > kSepgMaxCopies * 8 * 64) return g;
+  const int lds = (kSepgStages * (xs + 16 * bn + ws) + 16 * (bm + 1)) * 4;
+  if (lds > kSepgMaxLds) return g;
+  g.bm = bm; g.bn = bn; g.rout = rout; g.rpl = rpl; g.cr = cr; g.rows = rows; g.ps = ps; g.xs = xs; g.ws = ws;
+  g.lds = lds;
+  return g;
+}
 constexpr int kSepRowMaxChannels = 256;
 constexpr int kSepPairs = 4;             // (pixel block, channel block) pairs per wave at most
 constexpr int kSepStagePerThread = 8;   // staged input floats per thread and chunk at most
@@ -221,7 +254,10 @@ struct alignas(16) DevOp {
   int32_t sep_ck, sep_nck;     // SEP: input channels per chunk, chunks
   int32_t sep_rows;            // SEP: input rows staged per chunk
   int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
-  int32_t sep_row;             // SEP: 1 = row tile, 0 = staged tile
+  int32_t sep_row;             // SEP: 0 = staged tile, 1 = row tile, 2 = GEMM tile (sep_nbt = its waves along pixels)
+  int32_t sepg_rout, sepg_rpl; // SEP GEMM tile: output rows per tile, depthwise runs per row
+  int32_t sepg_cr, sepg_ps;    // SEP GEMM tile: columns per run, staged plane pitch
+  int32_t sepg_xs, sepg_ws;    // SEP GEMM tile: floats per ring slot of the input planes and depthwise weights
   int32_t row_k, row_bpr;      // SEP row tile: padded window K, 16-pixel blocks per output row
   int32_t pipe_ldw;            // CONV pipelined tile: row length of the packed weights (NG = k-blocks)
   int32_t w_bytes;             // size of wpk in bytes
@@ -233,6 +269,7 @@ struct alignas(16) DevOp {
   FDiv fd_pimg, fd_rw, fd_w;   // SEP: pixel tiles (row tile: 16-pixel blocks) per image, staged floats per channel, W
   FDiv fd_rbpr;                // SEP row tile: 16-pixel blocks per row
   FDiv fd_cin;                 // CONV pipelined tile: Cin
+  FDiv fd_ps, fd_rpl;          // SEP GEMM tile: sepg_ps, sepg_rpl
   FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
   FDiv fd_pin;                 // POOL with planes_per_tile > 1: floats staged per plane
   const float *wpk;            // CONV: see pack_conv_weights; SEP: the pointwise weights packed the same way
@@ -308,6 +345,7 @@ struct Op {
   int sep_tile = 1;              // SEPCONV: tile choice (16 << sep_tile output pixels per tile)
   int xcd_lg = -1;               // XCD run length 2^xcd_lg of the stage holding it; -1: modelled
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
+  float *d_pw_pipe = nullptr;    // SEPCONV GEMM tile: pointwise weights packed like a pipelined 1x1 conv's
   float *d_dw_row = nullptr, *d_pw_row = nullptr;   // SEPCONV row tile: [CinP4][kkp(K)], [CinP4][Npad]
   float *d_wg = nullptr;         // CONV, pipelined tiles: [nkb * kPipeKB][round128(Cout)]
   int pipe_nkb = 0;

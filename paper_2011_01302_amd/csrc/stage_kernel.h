@@ -1065,6 +1065,183 @@ __device__ __forceinline__ void sep_row_tile(const Slots &sl, const DevOp &op, c
   }
 }
 
+// The loads of SEPCONV GEMM-tile chunk c into ring slot s: this wave's
+// 64-float pieces of the input planes (per-lane offsets xoff, the chunk's
+// first channel added), of the pointwise weights [16 k][BN] and of the
+// depthwise weights [16][KK].  Offsets that may pass the end of their
+// buffer are per-lane (the range check covers them): the planes of the last
+// chunk past Cin, the copy of the last chunk's depthwise weights rounded up
+// to 64 floats.
+template <int COPIES, int ACOPIES>
+__device__ __forceinline__ void sepg_issue(float *s, const __amdgpu_buffer_rsrc_t &xr, const __amdgpu_buffer_rsrc_t &wr,
+                                           const __amdgpu_buffer_rsrc_t &dr, const int *xoff, const int *aoff, int c,
+                                           int nx, int nw, int XS, int AS, int hw4, int ldw, int KK, int wave,
+                                           int lane) {
+  wave = __builtin_amdgcn_readfirstlane(wave);       // uniform loop bounds around the LDS loads
+#pragma unroll
+  for (int i = 0; i < COPIES; ++i) {
+    const int j = wave + i * kWaves;
+    if (j < nx)                                       // uniform
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void *)(s + j * 64), 4,
+                                               xoff[i] == kOOB ? kOOB : xoff[i] + c * 16 * hw4, 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < ACOPIES; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void *)(s + XS + (wave * ACOPIES + i) * 64), 4, aoff[i],
+                                             c * 16 * ldw * 4, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {                       // nw <= 16 (windows up to 5 x 5)
+    const int j = wave + i * kWaves;
+    if (j < nw)                                       // uniform
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(dr, (lds_void *)(s + XS + AS + j * 64), 4,
+                                               (c * 16 * KK + j * 64 + lane) * 4, 0, 0, 0);
+  }
+}
+
+// "Relu-SepConv" unit, GEMM tile: R_out whole output rows of one image
+// (BM = 32 WMW MFMA columns, R_out = floor(BM / Wo)) x BN = 32 WNW output
+// channels, 8 waves of one 32x32 block each on v_mfma_f32_32x32x2_f32
+// (output channels as rows, pixels as columns).  The pointwise reduction
+// runs over chunks of 16 input channels; per chunk
+//   stage  direct global -> LDS loads (a ring of kSepgStages chunks in
+//          flight) of the chunk's input rows (the R_out rows with the
+//          window's halo, rows outside the image read as 0; one plane per
+//          channel, pitch sepg_ps), its depthwise weights and its
+//          pointwise weights [16 k][BN];
+//   dw     every (channel, output row, run of sepg_cr columns) of the chunk
+//          from the staged rows, the input ReLU applied as the rows are read
+//          (a sliding window over the run: K + sepg_cr - 1 reads per window
+//          row) -> the B operand [16 k][BM] in LDS;
+//   mfma   D[32 ch][32 px] += A[32 ch][2 k] B[2 k][32 px], 8 k-pairs.
+// Two barriers per chunk (the B operand is written and read by every wave).
+// The B rows of channels past Cin are 0 (their pointwise weights are 0 too).
+// Columns of the last 32-pixel block past R_out Wo are never stored.
+template <int WMW, int K, bool COH>
+__device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, D = kSepgStages, CRM = kSepgMaxRun;
+  constexpr int BMP = BM + 1;                        // B row pitch: the 16 channel rows on distinct banks
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % WMW, wn = wave / WMW;
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
+  const int img = fdiv(tm, o.fd_pimg), rb = tm - img * o.tiles_per_plane;
+  const int Wo = o.Wo, W = o.W, H = o.H, howo = o.Ho * Wo;
+  const int rout = o.sepg_rout, oh0 = rb * rout, rt = min(rout, o.Ho - oh0);   // rows of this tile
+  const int R = o.sep_rows, PS = o.sepg_ps, ih0 = oh0 - o.ph;                 // staged rows, plane pitch
+  const int n0 = tn * BN, nck = o.sep_nck, ldw = o.pipe_ldw, KK = K * K;
+  const int XS = o.sepg_xs, AS = 16 * BN, WS = o.sepg_ws;                      // floats per slot part
+  const int SLOT = XS + AS + WS;
+  float *ring = lds, *bsm = lds + D * SLOT;
+  const int nx = XS >> 6, nw = WS >> 6;              // 64-float copies per slot part
+
+  // per-lane offsets of this wave's copies of the input planes: element
+  // e = 64 j + lane of the slot is channel e / PS, staged row (e % PS) / W,
+  // column e % W (elements past a plane's R W floats, and rows outside the
+  // image, read 0); the chunk's first channel is added per chunk
+  const int cbase = img * o.in_ctot[0] + o.in_coff[0];
+  int xoff[kSepgMaxCopies];
+#pragma unroll
+  for (int i = 0; i < kSepgMaxCopies; ++i) {
+    const int e = (wave + i * kWaves) * 64 + lane;
+    const int ch = fdiv(e, o.fd_ps), rem = e - ch * PS, r = fdiv(rem, o.fd_w), col = rem - r * W;
+    const int ih = ih0 + r;
+    xoff[i] = rem < R * W && ih >= 0 && ih < H ? (((cbase + ch) * H + ih) * W + col) * 4 : kOOB;
+  }
+  // pointwise weights of the slot: element f = k BN + col of [16 k][BN]
+  constexpr int AC = 16 * BN / 64 / kWaves;          // 64-float copies per wave
+  int aoff[AC];
+#pragma unroll
+  for (int i = 0; i < AC; ++i) {
+    const int f = (wave * AC + i) * 64 + lane;
+    aoff[i] = ((f / BN) * ldw + n0 + f % BN) * 4;
+  }
+  const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
+  const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
+  const __amdgpu_buffer_rsrc_t dr = rsrc(o.dw, o.dw_bytes);
+  const int hw4 = H * W * 4;
+  // depthwise mapping: channel ch, output row r, columns [col0, col0 + CR)
+  const int ch = tid & 15, grp = tid >> 4, CR = o.sepg_cr;
+  const int r = fdiv(grp, o.fd_rpl), col0 = (grp - r * o.sepg_rpl) * CR;
+  const bool dw_on = r < rt && col0 < Wo;
+  const bool relu_in = o.pre_relu != 0;
+
+  floatx16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  for (int c = 0; c < D - 1 && c < nck; ++c)
+    sepg_issue<kSepgMaxCopies, AC>(ring + (c % D) * SLOT, xr, wr, dr, xoff, aoff, c, nx, nw, XS, AS, hw4, ldw, KK, wave,
+                               lane);
+  for (int c = 0; c < nck; ++c) {
+    // this wave's loads of chunk c have landed once at most the chunks
+    // issued after it are in flight; the barrier publishes every wave's and
+    // guarantees that chunk c - 1's slot and the B operand are no longer read
+    static_assert(D == 2, "one chunk in flight: the wait below drains it");
+    wait_vmcnt<0>();
+    ring_barrier();
+    if (c + D - 1 < nck)
+      sepg_issue<kSepgMaxCopies, AC>(ring + ((c + D - 1) % D) * SLOT, xr, wr, dr, xoff, aoff, c + D - 1, nx, nw, XS,
+                                 AS, hw4, ldw, KK, wave, lane);
+    const float *s = ring + (c % D) * SLOT;
+    // depthwise of the chunk -> B
+    if (dw_on) {
+      const float *xp = s + ch * PS + r * W + col0 - o.pw;
+      const float *wp = s + XS + AS + ch * KK;
+      float d[CRM];
+#pragma unroll
+      for (int i = 0; i < CRM; ++i) d[i] = 0.f;
+#pragma unroll
+      for (int u = 0; u < K; ++u) {
+        float x[CRM + K - 1], w[K];
+#pragma unroll
+        for (int v = 0; v < K; ++v) w[v] = wp[u * K + v];
+#pragma unroll
+        for (int j = 0; j < CRM + K - 1; ++j) {
+          const int col = col0 - o.pw + j;
+          const float v = col >= 0 && col < W && j < CR + K - 1 ? xp[u * W + j] : 0.f;
+          x[j] = relu_in ? fmaxf(v, 0.f) : v;
+        }
+#pragma unroll
+        for (int i = 0; i < CRM; ++i)
+#pragma unroll
+          for (int v = 0; v < K; ++v) d[i] = fmaf(w[v], x[i + v], d[i]);
+      }
+      // channels past Cin (last chunk) write zeros: their staged planes hold
+      // whatever follows the input
+      const bool cv = c * 16 + ch < o.Cin;
+#pragma unroll
+      for (int i = 0; i < CRM; ++i)
+        if (i < CR && col0 + i < Wo) bsm[ch * BMP + r * Wo + col0 + i] = cv ? d[i] : 0.f;
+    }
+    ring_barrier();
+    // pointwise on MFMA: A from the slot, B from the depthwise results
+    const float *a = s + XS + (lane >> 5) * BN + wn * 32 + (lane & 31);
+    const float *b = bsm + (lane >> 5) * BMP + wm * 32 + (lane & 31);
+    float av[8], bv[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      av[p] = a[2 * p * BN];
+      bv[p] = b[2 * p * BMP];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) acc = mfma32x32x2(av[p], bv[p], acc);
+  }
+  // epilogue: element i of lane l is channel n0 + 32 wn + 8 (i/4) + 4 (l/32) + i%4 of tile column 32 wm + l%32
+  const int px = wm * 32 + (lane & 31);
+  if (px < rt * Wo) {
+    const int q = oh0 * Wo + px;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int n = n0 + wn * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+      if (n < o.Cout) {
+        float v = acc[i] + o.bias[n];
+        if (o.post_relu) v = fmaxf(v, 0.f);
+        st<COH>(route_ptr(sl, op, o, n, img, q, howo), v);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ elementwise
 
 constexpr int kPoolBatch = 4;   // staging loads per thread in flight
@@ -1271,7 +1448,15 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
       }
     case DK_SEP:
       if constexpr (KV == KV_SEP || KV == KV_SEPROW || KV == KV_FULL) {
-        if (!o.sep_row) {
+        if (o.sep_row == 2) {
+          if constexpr (KV != KV_SEPROW) {
+            if (o.sep_nbt == 4) {
+              if (o.kh == 3) sep_gemm_tile<4, 3, COH>(sl, op, o, ti, lds); else sep_gemm_tile<4, 5, COH>(sl, op, o, ti, lds);
+            } else {
+              if (o.kh == 3) sep_gemm_tile<2, 3, COH>(sl, op, o, ti, lds); else sep_gemm_tile<2, 5, COH>(sl, op, o, ti, lds);
+            }
+          }
+        } else if (!o.sep_row) {
           if constexpr (KV != KV_SEPROW) sep_tile<COH>(sl, op, o, ti, lds);
         } else if constexpr (KV != KV_SEP) {
           const bool one = o.n_in == 1;

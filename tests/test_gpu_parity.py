@@ -596,11 +596,15 @@ def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     g.close()
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6"])
+@pytest.mark.parametrize("tile", [str(t) for t in range(9)])
 def test_parity_every_sepconv_tile(tile, monkeypatch):
     # SEPCONV tile choice (staged: 16, 32 or 64 output pixels per tile; row:
-    # 1 to 4 channel blocks), forced instead of measured (the wide unit
-    # cannot use the row tile and falls back to the staged one)
+    # 1 to 4 channel blocks; GEMM: whole rows in 128 or 64 columns), forced
+    # instead of measured (a unit a choice does not apply to falls back to
+    # the staged tile: the wide 7x7 unit and multi-input sums for the row and
+    # GEMM tiles; the 3x3 unit over 280 channels, ragged's 5x5 unit over 21
+    # channels on a 9x11 plane and the NASNet / RandWire single-input units
+    # run on the GEMM tile)
     monkeypatch.setenv("IOS_SEP_TILE", tile)
     for config in ["randwire", "nasnet"]:
         spec, ten = case(config)

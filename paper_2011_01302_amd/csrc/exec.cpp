@@ -335,7 +335,7 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
             d.sep_nbt = sg.bm / 32;
             d.sep_nck = o.CinP / 16;
             d.sep_rows = sg.rows;
-            d.sepg_rout = sg.rout; d.sepg_rpl = sg.rpl; d.sepg_cr = sg.cr; d.sepg_ps = sg.ps;
+            d.sepg_rout = sg.rout; d.sepg_w2 = sg.w2; d.sepg_strips = sg.strips; d.sepg_ps = sg.ps;
             d.sepg_xs = sg.xs; d.sepg_ws = sg.ws;
             d.pipe_ldw = round_up(o.d.cout, 128);
             d.wpk = o.d_pw_pipe; d.bias = o.d_bias; d.dw = o.d_dw;
@@ -462,7 +462,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.fd_kw = fd(d.kw);
     d.fd_pimg = fd(d.kind == DK_SEP && d.sep_row == 1 ? d.Ho * d.row_bpr : d.tiles_per_plane);
     d.fd_ps = fd(d.sepg_ps);
-    d.fd_rpl = fd(d.sepg_rpl);
+    d.fd_w2 = fd(d.sepg_w2);
+    d.fd_strips = fd(d.sepg_strips);
     d.fd_rbpr = fd(d.row_bpr);
     d.fd_cin = fd(d.Cin);
     d.fd_rw = fd(d.sep_rows * d.W);

@@ -133,34 +133,43 @@ constexpr int kSepRowMaxNB = 4;
 constexpr int kSepgTiles = 2;
 constexpr int kSepgFirst = kSepStagedTiles + kSepRowMaxNB;
 constexpr int kSepTiles = kSepgFirst + kSepgTiles;
-constexpr int kSepgStages = 2;           // GEMM tile: chunks of 16 input channels in LDS (one in flight)
-constexpr int kSepgMaxRun = 8;           // GEMM tile: depthwise outputs per thread and chunk at most
+constexpr int kSepgStages = 3;           // GEMM tile: ring slots of 16 input channels (two chunks in flight)
+constexpr int kSepgMaxRows = 4;          // GEMM tile: output rows per tile at most
 constexpr int kSepgMaxCopies = 12;       // GEMM tile: 64-float input copies per wave and chunk at most
-constexpr int kSepgMaxLds = 80 * 1024;   // GEMM tile: two workgroups per CU
-// GEMM tile geometry (bm = 0: the choice does not apply).  R_out output rows
-// per tile (rout), depthwise runs per row (rpl) of cr columns, staged input
-// rows (rows), the plane pitch of the staged input (ps, odd) and the floats
-// per ring slot of the input planes (xs) and of the depthwise weights (ws).
+constexpr int kSepgMaxLds = 128 * 1024;  // GEMM tile: LDS bytes at most (the stage table comes on top)
+// GEMM tile geometry (bm = 0: the choice does not apply): rout output rows
+// per tile (2 .. kSepgMaxRows), staged input rows (rows), the staged plane's
+// row pitch (w2 = W + 2 pw, a zero halo on both sides) and pitch (ps, odd),
+// the floats per ring slot of the input planes (xs) and of the depthwise
+// weights (ws), and the depthwise strips of 2 output columns per row.
 struct SepgGeom {
-  int bm = 0, bn = 0, rout = 0, rpl = 0, cr = 0, rows = 0, ps = 0, xs = 0, ws = 0, lds = 0;
+  int bm = 0, bn = 0, rout = 0, rows = 0, w2 = 0, ps = 0, xs = 0, ws = 0, strips = 0, lds = 0;
 };
+// LDS bytes of a GEMM tile: the ring (input planes, pointwise and depthwise
+// weights per slot) and two B operand buffers [16][bm + 1].
+inline int sepg_lds_bytes(int xs, int ws, int bm, int bn) {
+  return (kSepgStages * (xs + 16 * bn + ws) + 2 * 16 * (bm + 1)) * 4;
+}
 inline SepgGeom sepg_geometry(int choice, int n_in, int kh, int kw, int ph, int pw, int H, int W, int Ho, int Wo) {
   SepgGeom g;
   const int wmw = choice == 0 ? 4 : 2, bm = 32 * wmw, bn = 32 * (8 / wmw);
   if (n_in != 1 || kh != kw || (kh != 3 && kh != 5) || ph != kh / 2 || pw != kw / 2 || Ho != H || Wo != W ||
-      Wo > bm || Wo < 1)
+      Wo < 1)
     return g;
-  const int rout = std::min(std::min(bm / Wo, Ho), 32), rpl = 32 / rout, cr = (Wo + rpl - 1) / rpl;
-  if (cr > kSepgMaxRun) return g;
-  const int rows = rout + kh - 1, ps = (rows * W) | 1;
+  const int rout = std::min(std::min(bm / Wo, Ho), kSepgMaxRows);
+  if (rout < 2 && Ho >= 2) return g;
+  if (rout < 1) return g;
+  const int rows = rout + kh - 1, w2 = W + 2 * pw, ps = (rows * w2) | 1;
   const int xs = (16 * ps + 63) / 64 * 64, ws = (16 * kh * kw + 63) / 64 * 64;
   if (xs > kSepgMaxCopies * 8 * 64) return g;
-  const int lds = (kSepgStages * (xs + 16 * bn + ws) + 16 * (bm + 1)) * 4;
-  if (lds > kSepgMaxLds) return g;
-  g.bm = bm; g.bn = bn; g.rout = rout; g.rpl = rpl; g.cr = cr; g.rows = rows; g.ps = ps; g.xs = xs; g.ws = ws;
-  g.lds = lds;
+  if (sepg_lds_bytes(xs, ws, bm, bn) > kSepgMaxLds) return g;
+  g.bm = bm; g.bn = bn; g.rout = std::max(rout, 2); g.rows = g.rout + kh - 1; g.w2 = w2;
+  g.ps = (g.rows * w2) | 1; g.xs = (16 * g.ps + 63) / 64 * 64; g.ws = ws; g.strips = (Wo + 1) / 2;
+  g.lds = sepg_lds_bytes(g.xs, ws, bm, bn);
+  if (g.xs > kSepgMaxCopies * 8 * 64 || g.lds > kSepgMaxLds) return SepgGeom{};
   return g;
 }
+
 constexpr int kSepRowMaxChannels = 256;
 constexpr int kSepPairs = 4;             // (pixel block, channel block) pairs per wave at most
 constexpr int kSepStagePerThread = 8;   // staged input floats per thread and chunk at most
@@ -255,8 +264,8 @@ struct alignas(16) DevOp {
   int32_t sep_rows;            // SEP: input rows staged per chunk
   int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
   int32_t sep_row;             // SEP: 0 = staged tile, 1 = row tile, 2 = GEMM tile (sep_nbt = its waves along pixels)
-  int32_t sepg_rout, sepg_rpl; // SEP GEMM tile: output rows per tile, depthwise runs per row
-  int32_t sepg_cr, sepg_ps;    // SEP GEMM tile: columns per run, staged plane pitch
+  int32_t sepg_rout, sepg_w2;  // SEP GEMM tile: output rows per tile, staged row pitch (W + 2 pw)
+  int32_t sepg_strips, sepg_ps;// SEP GEMM tile: depthwise strips of 2 columns per row, staged plane pitch
   int32_t sepg_xs, sepg_ws;    // SEP GEMM tile: floats per ring slot of the input planes and depthwise weights
   int32_t row_k, row_bpr;      // SEP row tile: padded window K, 16-pixel blocks per output row
   int32_t pipe_ldw;            // CONV pipelined tile: row length of the packed weights (NG = k-blocks)
@@ -269,7 +278,7 @@ struct alignas(16) DevOp {
   FDiv fd_pimg, fd_rw, fd_w;   // SEP: pixel tiles (row tile: 16-pixel blocks) per image, staged floats per channel, W
   FDiv fd_rbpr;                // SEP row tile: 16-pixel blocks per row
   FDiv fd_cin;                 // CONV pipelined tile: Cin
-  FDiv fd_ps, fd_rpl;          // SEP GEMM tile: sepg_ps, sepg_rpl
+  FDiv fd_ps, fd_w2, fd_strips;// SEP GEMM tile: sepg_ps, sepg_w2, sepg_strips
   FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
   FDiv fd_pin;                 // POOL with planes_per_tile > 1: floats staged per plane
   const float *wpk;            // CONV: see pack_conv_weights; SEP: the pointwise weights packed the same way

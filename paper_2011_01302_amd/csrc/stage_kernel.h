@@ -1098,57 +1098,112 @@ __device__ __forceinline__ void sepg_issue(float *s, const __amdgpu_buffer_rsrc_
   }
 }
 
-// "Relu-SepConv" unit, GEMM tile: R_out whole output rows of one image
-// (BM = 32 WMW MFMA columns, R_out = floor(BM / Wo)) x BN = 32 WNW output
-// channels, 8 waves of one 32x32 block each on v_mfma_f32_32x32x2_f32
-// (output channels as rows, pixels as columns).  The pointwise reduction
-// runs over chunks of 16 input channels; per chunk
-//   stage  direct global -> LDS loads (a ring of kSepgStages chunks in
-//          flight) of the chunk's input rows (the R_out rows with the
-//          window's halo, rows outside the image read as 0; one plane per
-//          channel, pitch sepg_ps), its depthwise weights and its
-//          pointwise weights [16 k][BN];
-//   dw     every (channel, output row, run of sepg_cr columns) of the chunk
-//          from the staged rows, the input ReLU applied as the rows are read
-//          (a sliding window over the run: K + sepg_cr - 1 reads per window
-//          row) -> the B operand [16 k][BM] in LDS;
-//   mfma   D[32 ch][32 px] += A[32 ch][2 k] B[2 k][32 px], 8 k-pairs.
-// Two barriers per chunk (the B operand is written and read by every wave).
-// The B rows of channels past Cin are 0 (their pointwise weights are 0 too).
-// Columns of the last 32-pixel block past R_out Wo are never stored.
-template <int WMW, int K, bool COH>
+// s_waitcnt vmcnt(n) for a uniform run-time n <= MAX.
+template <int MAX>
+__device__ __forceinline__ void wait_vmcnt_upto(int n) {
+  if constexpr (MAX > 0) {
+    if (n >= MAX) { wait_vmcnt<MAX>(); return; }
+    wait_vmcnt_upto<MAX - 1>(n);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+// max(v, 0) in one instruction (median of v, 0 and +inf)
+__device__ __forceinline__ float relu1(float v) { return __builtin_amdgcn_fmed3f(v, 0.f, __builtin_inff()); }
+
+// Depthwise outputs of one (channel, strip of 2 output columns) for RG
+// output rows, from its staged plane (rows with the window's halo, columns
+// with a zero halo of pw on each side: no column test), the input ReLU
+// applied as each value is read; written to the B operand (row ch, column
+// r Wo + col), zeros for a channel past Cin.
+template <int K, int RG>
+__device__ __forceinline__ void sepg_dw(const float *xp, const float *w, float *brow, int W2, int Wo, int col0, int rt,
+                                        bool relu_in, bool cv) {
+  float d[RG][2];
+#pragma unroll
+  for (int o = 0; o < RG; ++o) d[o][0] = d[o][1] = 0.f;
+#pragma unroll
+  for (int i = 0; i < RG + K - 1; ++i) {             // staged input row i feeds output rows i - K + 1 .. i
+    float x[K + 1];
+#pragma unroll
+    for (int j = 0; j <= K; ++j) {
+      const float v = xp[i * W2 + j];
+      x[j] = relu_in ? relu1(v) : v;
+    }
+#pragma unroll
+    for (int o = 0; o < RG; ++o) {
+      const int u = i - o;
+      if (u < 0 || u >= K) continue;                  // compile time
+#pragma unroll
+      for (int v = 0; v < K; ++v) {
+        d[o][0] = fmaf(w[u * K + v], x[v], d[o][0]);
+        d[o][1] = fmaf(w[u * K + v], x[v + 1], d[o][1]);
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 0; o < RG; ++o)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      if (o < rt && col0 + j < Wo) brow[o * Wo + col0 + j] = cv ? d[o][j] : 0.f;
+}
+
+// "Relu-SepConv" unit, GEMM tile: RG whole output rows of one image
+// (BM = 32 WMW MFMA columns, RG Wo <= BM) x BN = 32 WNW output channels, 8
+// waves of one 32x32 block each on v_mfma_f32_32x32x2_f32 (output channels
+// as rows, pixels as columns).  The pointwise reduction runs over chunks of
+// 16 input channels; per chunk
+//   stage  direct global -> LDS loads, kSepgStages - 1 chunks in flight, of
+//          the chunk's input planes (the tile's rows with the window's halo,
+//          rows and columns outside the image as 0: one plane of
+//          sepg_w2 = W + 2 pw columns per channel, pitch sepg_ps), its
+//          depthwise weights and its pointwise weights [16 k][BN];
+//   dw     every (channel, strip of 2 output columns) of the chunk over the
+//          tile's rows -> the B operand [16 k][BM] in LDS (two buffers);
+//   mfma   D[32 ch][32 px] += A[32 ch][2 k] B[2 k][32 px], 8 k-pairs, A
+//          from the slot (read into registers a round early), B from the
+//          depthwise results of the round before.
+// One barrier per round: round c runs the depthwise of chunk c and the
+// MFMAs of chunk c - 1; half the waves of each SIMD take the MFMAs first,
+// the other half the depthwise, so that the SIMD's vector ALU works while
+// the matrix core does.  B columns past RG Wo are never stored.
+template <int WMW, int K, int RG, bool COH>
 __device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
-  constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, D = kSepgStages, CRM = kSepgMaxRun;
+  constexpr int WNW = kWaves / WMW, BM = 32 * WMW, BN = 32 * WNW, D = kSepgStages, KK = K * K;
   constexpr int BMP = BM + 1;                        // B row pitch: the 16 channel rows on distinct banks
+  constexpr int AC = 16 * BN / 64 / kWaves;          // 64-float pointwise-weight copies per wave
+  static_assert(D == 3, "slot of chunk c + 2 = slot of chunk c - 1");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave % WMW, wn = wave / WMW;
   const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
   const int img = fdiv(tm, o.fd_pimg), rb = tm - img * o.tiles_per_plane;
-  const int Wo = o.Wo, W = o.W, H = o.H, howo = o.Ho * Wo;
-  const int rout = o.sepg_rout, oh0 = rb * rout, rt = min(rout, o.Ho - oh0);   // rows of this tile
-  const int R = o.sep_rows, PS = o.sepg_ps, ih0 = oh0 - o.ph;                 // staged rows, plane pitch
-  const int n0 = tn * BN, nck = o.sep_nck, ldw = o.pipe_ldw, KK = K * K;
-  const int XS = o.sepg_xs, AS = 16 * BN, WS = o.sepg_ws;                      // floats per slot part
+  const int Wo = o.Wo, W = o.W, H = o.H, howo = o.Ho * Wo, W2 = o.sepg_w2;
+  const int oh0 = rb * RG, rt = min(RG, o.Ho - oh0);                // rows of this tile
+  const int R = o.sep_rows, PS = o.sepg_ps, ih0 = oh0 - o.ph;       // staged rows, plane pitch
+  const int n0 = tn * BN, nck = o.sep_nck, ldw = o.pipe_ldw;
+  const int XS = o.sepg_xs, AS = 16 * BN, WS = o.sepg_ws;            // floats per slot part
   const int SLOT = XS + AS + WS;
   float *ring = lds, *bsm = lds + D * SLOT;
   const int nx = XS >> 6, nw = WS >> 6;              // 64-float copies per slot part
 
   // per-lane offsets of this wave's copies of the input planes: element
-  // e = 64 j + lane of the slot is channel e / PS, staged row (e % PS) / W,
-  // column e % W (elements past a plane's R W floats, and rows outside the
-  // image, read 0); the chunk's first channel is added per chunk
+  // e = 64 j + lane of the slot is channel e / PS, staged row (e % PS) / W2,
+  // plane column (e % PS) % W2 = image column + pw; elements past a plane's
+  // R W2 floats, rows and columns outside the image read 0; the chunk's
+  // first channel is added per chunk
   const int cbase = img * o.in_ctot[0] + o.in_coff[0];
   int xoff[kSepgMaxCopies];
 #pragma unroll
   for (int i = 0; i < kSepgMaxCopies; ++i) {
     const int e = (wave + i * kWaves) * 64 + lane;
-    const int ch = fdiv(e, o.fd_ps), rem = e - ch * PS, r = fdiv(rem, o.fd_w), col = rem - r * W;
+    const int ch = fdiv(e, o.fd_ps), rem = e - ch * PS, r = fdiv(rem, o.fd_w2), col = rem - r * W2 - o.pw;
     const int ih = ih0 + r;
-    xoff[i] = rem < R * W && ih >= 0 && ih < H ? (((cbase + ch) * H + ih) * W + col) * 4 : kOOB;
+    xoff[i] = rem < R * W2 && ih >= 0 && ih < H && col >= 0 && col < W ? (((cbase + ch) * H + ih) * W + col) * 4
+                                                                        : kOOB;
   }
   // pointwise weights of the slot: element f = k BN + col of [16 k][BN]
-  constexpr int AC = 16 * BN / 64 / kWaves;          // 64-float copies per wave
   int aoff[AC];
 #pragma unroll
   for (int i = 0; i < AC; ++i) {
@@ -1159,72 +1214,70 @@ __device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, 
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
   const __amdgpu_buffer_rsrc_t dr = rsrc(o.dw, o.dw_bytes);
   const int hw4 = H * W * 4;
-  // depthwise mapping: channel ch, output row r, columns [col0, col0 + CR)
-  const int ch = tid & 15, grp = tid >> 4, CR = o.sepg_cr;
-  const int r = fdiv(grp, o.fd_rpl), col0 = (grp - r * o.sepg_rpl) * CR;
-  const bool dw_on = r < rt && col0 < Wo;
+  // loads per wave and chunk (the same for every chunk)
+  int per = AC;
+#pragma unroll
+  for (int i = 0; i < kSepgMaxCopies; ++i) per += wave + i * kWaves < nx;
+  per += (wave < nw) + (wave + kWaves < nw);
+  per = __builtin_amdgcn_readfirstlane(per);
+
+  // depthwise items: (channel ch, strip of columns 2 st, 2 st + 1)
+  const int ch = tid & 15, strips = o.sepg_strips;
   const bool relu_in = o.pre_relu != 0;
+  const bool mfma_first = (wave >> 2) & 1;           // waves w and w + 4 share a SIMD
 
   floatx16 acc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-  for (int c = 0; c < D - 1 && c < nck; ++c)
-    sepg_issue<kSepgMaxCopies, AC>(ring + (c % D) * SLOT, xr, wr, dr, xoff, aoff, c, nx, nw, XS, AS, hw4, ldw, KK, wave,
-                               lane);
-  for (int c = 0; c < nck; ++c) {
-    // this wave's loads of chunk c have landed once at most the chunks
-    // issued after it are in flight; the barrier publishes every wave's and
-    // guarantees that chunk c - 1's slot and the B operand are no longer read
-    static_assert(D == 2, "one chunk in flight: the wait below drains it");
-    wait_vmcnt<0>();
+  float avc[8];                                      // A of the chunk whose MFMAs run next
+#pragma unroll
+  for (int p = 0; p < 8; ++p) avc[p] = 0.f;
+  sepg_issue<kSepgMaxCopies, AC>(ring, xr, wr, dr, xoff, aoff, 0, nx, nw, XS, AS, hw4, ldw, KK, wave, lane);
+  if (nck > 1)
+    sepg_issue<kSepgMaxCopies, AC>(ring + SLOT, xr, wr, dr, xoff, aoff, 1, nx, nw, XS, AS, hw4, ldw, KK, wave, lane);
+  for (int c = 0; c <= nck; ++c) {
+    // chunk c has landed once only chunk c + 1's loads (if any) are in
+    // flight; the barrier publishes every wave's loads and the depthwise
+    // results of round c - 1, and guarantees that round c - 1 no longer
+    // reads chunk c - 1's slot (its A is in registers) or the B buffer that
+    // round c writes
+    if (c + 1 < nck) wait_vmcnt_upto<kSepgMaxCopies + 4 + 2>(per);
+    else wait_vmcnt<0>();
     ring_barrier();
-    if (c + D - 1 < nck)
-      sepg_issue<kSepgMaxCopies, AC>(ring + ((c + D - 1) % D) * SLOT, xr, wr, dr, xoff, aoff, c + D - 1, nx, nw, XS,
-                                 AS, hw4, ldw, KK, wave, lane);
+    if (c + 2 < nck)
+      sepg_issue<kSepgMaxCopies, AC>(ring + ((c + 2) % D) * SLOT, xr, wr, dr, xoff, aoff, c + 2, nx, nw, XS, AS, hw4,
+                                     ldw, KK, wave, lane);
     const float *s = ring + (c % D) * SLOT;
-    // depthwise of the chunk -> B
-    if (dw_on) {
-      const float *xp = s + ch * PS + r * W + col0 - o.pw;
-      const float *wp = s + XS + AS + ch * KK;
-      float d[CRM];
+    float avn[8];
+    if (c < nck) {
+      const float *a = s + XS + (lane >> 5) * BN + wn * 32 + (lane & 31);
 #pragma unroll
-      for (int i = 0; i < CRM; ++i) d[i] = 0.f;
+      for (int p = 0; p < 8; ++p) avn[p] = a[2 * p * BN];
+    }
 #pragma unroll
-      for (int u = 0; u < K; ++u) {
-        float x[CRM + K - 1], w[K];
+    for (int ph = 0; ph < 2; ++ph) {
+      if ((ph == 0) == mfma_first) {
+        if (c >= 1) {                                 // MFMAs of chunk c - 1
+          const float *b = bsm + ((c - 1) & 1) * 16 * BMP + (lane >> 5) * BMP + wm * 32 + (lane & 31);
+          float bv[8];
 #pragma unroll
-        for (int v = 0; v < K; ++v) w[v] = wp[u * K + v];
+          for (int p = 0; p < 8; ++p) bv[p] = b[2 * p * BMP];
 #pragma unroll
-        for (int j = 0; j < CRM + K - 1; ++j) {
-          const int col = col0 - o.pw + j;
-          const float v = col >= 0 && col < W && j < CR + K - 1 ? xp[u * W + j] : 0.f;
-          x[j] = relu_in ? fmaxf(v, 0.f) : v;
+          for (int p = 0; p < 8; ++p) acc = mfma32x32x2(avc[p], bv[p], acc);
         }
+      } else if (c < nck) {                           // depthwise of chunk c
+        const bool cv = c * 16 + ch < o.Cin;          // channels past Cin (last chunk): zeros
+        float *brow = bsm + (c & 1) * 16 * BMP + ch * BMP;
+        float w[KK];
+        const float *wp = s + XS + AS + ch * KK;
 #pragma unroll
-        for (int i = 0; i < CRM; ++i)
-#pragma unroll
-          for (int v = 0; v < K; ++v) d[i] = fmaf(w[v], x[i + v], d[i]);
+        for (int i = 0; i < KK; ++i) w[i] = wp[i];
+        for (int st = tid >> 4; st < strips; st += kThreads / 16)
+          sepg_dw<K, RG>(s + ch * PS + 2 * st, w, brow, W2, Wo, 2 * st, rt, relu_in, cv);
       }
-      // channels past Cin (last chunk) write zeros: their staged planes hold
-      // whatever follows the input
-      const bool cv = c * 16 + ch < o.Cin;
-#pragma unroll
-      for (int i = 0; i < CRM; ++i)
-        if (i < CR && col0 + i < Wo) bsm[ch * BMP + r * Wo + col0 + i] = cv ? d[i] : 0.f;
     }
-    ring_barrier();
-    // pointwise on MFMA: A from the slot, B from the depthwise results
-    const float *a = s + XS + (lane >> 5) * BN + wn * 32 + (lane & 31);
-    const float *b = bsm + (lane >> 5) * BMP + wm * 32 + (lane & 31);
-    float av[8], bv[8];
 #pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      av[p] = a[2 * p * BN];
-      bv[p] = b[2 * p * BMP];
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int p = 0; p < 8; ++p) acc = mfma32x32x2(av[p], bv[p], acc);
+    for (int p = 0; p < 8; ++p) avc[p] = c < nck ? avn[p] : 0.f;
   }
   // epilogue: element i of lane l is channel n0 + 32 wn + 8 (i/4) + 4 (l/32) + i%4 of tile column 32 wm + l%32
   const int px = wm * 32 + (lane & 31);
@@ -1239,6 +1292,24 @@ __device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, 
         st<COH>(route_ptr(sl, op, o, n, img, q, howo), v);
       }
     }
+  }
+}
+
+// GEMM SEPCONV tile variants: waves along pixels (sep_nbt), window, rows per tile.
+template <int WMW, int K, bool COH>
+__device__ __forceinline__ void sep_gemm_rows(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  switch (o.sepg_rout) {
+    case 2: sep_gemm_tile<WMW, K, 2, COH>(sl, op, o, t, lds); break;
+    case 3: sep_gemm_tile<WMW, K, 3, COH>(sl, op, o, t, lds); break;
+    default: sep_gemm_tile<WMW, K, 4, COH>(sl, op, o, t, lds); break;
+  }
+}
+template <bool COH>
+__device__ __forceinline__ void sep_gemm_dispatch(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  if (o.sep_nbt == 4) {
+    if (o.kh == 3) sep_gemm_rows<4, 3, COH>(sl, op, o, t, lds); else sep_gemm_rows<4, 5, COH>(sl, op, o, t, lds);
+  } else {
+    if (o.kh == 3) sep_gemm_rows<2, 3, COH>(sl, op, o, t, lds); else sep_gemm_rows<2, 5, COH>(sl, op, o, t, lds);
   }
 }
 
@@ -1449,13 +1520,7 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
     case DK_SEP:
       if constexpr (KV == KV_SEP || KV == KV_SEPROW || KV == KV_FULL) {
         if (o.sep_row == 2) {
-          if constexpr (KV != KV_SEPROW) {
-            if (o.sep_nbt == 4) {
-              if (o.kh == 3) sep_gemm_tile<4, 3, COH>(sl, op, o, ti, lds); else sep_gemm_tile<4, 5, COH>(sl, op, o, ti, lds);
-            } else {
-              if (o.kh == 3) sep_gemm_tile<2, 3, COH>(sl, op, o, ti, lds); else sep_gemm_tile<2, 5, COH>(sl, op, o, ti, lds);
-            }
-          }
+          if constexpr (KV != KV_SEPROW) sep_gemm_dispatch<COH>(sl, op, o, ti, lds);
         } else if (!o.sep_row) {
           if constexpr (KV != KV_SEPROW) sep_tile<COH>(sl, op, o, ti, lds);
         } else if constexpr (KV != KV_SEP) {

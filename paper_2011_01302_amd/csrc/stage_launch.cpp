@@ -34,8 +34,7 @@ int op_lds_bytes(const DevOp &op) {
     return s.wk * tile_bn(op.tcfg) * (tile_bm(op.tcfg) + 1) * (int)sizeof(float);
   }
   if (op.kind == DK_SEP && op.sep_row == 2)
-    return (kSepgStages * (op.sepg_xs + 16 * 32 * (kWaves / op.sep_nbt) + op.sepg_ws) + 16 * (32 * op.sep_nbt + 1)) *
-           (int)sizeof(float);
+    return sepg_lds_bytes(op.sepg_xs, op.sepg_ws, 32 * op.sep_nbt, 32 * (kWaves / op.sep_nbt));
   if (op.kind == DK_SEP && op.sep_row) return sep_row_lds_bytes(op.CinP, op.row_k, op.sep_nbt);
   if (op.kind == DK_SEP)
     return sep_lds_floats(op.sep_bm, op.sep_ck, op.sep_rows, op.W, op.kh * op.kw, op.sep_nbt) * (int)sizeof(float);

@@ -387,19 +387,21 @@ def batched_reference(config, batch, seed=0):
 
 
 @pytest.mark.parametrize("config,batch,kinds", [
-    ("inception", 16, ("dp", "sequential")),
+    ("inception", 16, ("dp", "sequential", "dp_tuned")),
     ("squeeze", 32, ("dp", "greedy")),
     ("squeeze", 128, ("dp", "greedy")),
-    ("nasnet", 32, ("block_stage", "greedy")),
+    ("nasnet", 32, ("block_stage", "greedy", "greedy_tuned")),
 ])
 def test_parity_batched_every_image(config, batch, kinds):
     """Every image of the batched configurations against the oracle, under
     the DP's schedule (on-device profiling, light) where the search is
-    affordable, a one-stage chained schedule for NASNet and a baseline."""
+    affordable, a one-stage chained schedule for NASNet and a baseline; the
+    "_tuned" kinds then choose every stage's tiles in its company
+    (ios_schedule_tune_tiles: pipelined conv shapes, the GEMM SEPCONV tile)."""
     spec, ten, refs = batched_reference(config, batch)
     g = I.Graph(spec, ten)
     for kind in kinds:
-        if kind == "dp":
+        if kind.startswith("dp"):
             o = I.ios_sched_opts_default()
             o.warmup, o.reps, o.repeats = 1, 3, 1
             q, _ = I.ios_schedule(g.handle, o)
@@ -407,7 +409,45 @@ def test_parity_batched_every_image(config, batch, kinds):
             q = block_stages(g)
         else:
             q = sched(g, I.IOS_SCHED_SEQUENTIAL if kind == "sequential" else I.IOS_SCHED_GREEDY)
+        if kind.endswith("_tuned"):
+            o = I.ios_sched_opts_default()
+            o.warmup, o.reps, o.repeats = 1, 3, 1
+            assert I.ios_schedule_tune_tiles(g.handle, q, o) > 0
         check(run(g, q, spec, ten), refs, f"{config}/bs{batch}/{kind}")
+        I.ios_schedule_destroy(q)
+    g.close()
+
+
+def sepg_spec(batch):
+    """SEPCONVs the 64-column GEMM tile applies to (planes up to 32 wide):
+    21x21 planes (3 output rows per tile, the last tile of an image short),
+    40 input channels (a short last chunk), 100 output channels (a short
+    channel tile), 3x3 and 5x5 windows, chained."""
+    sep = lambda n, i, co, k: {"name": n, "kind": "sepconv", "in": [i], "cout": co, "kh": k, "kw": k, "sh": 1,
+                               "sw": 1, "ph": k // 2, "pw": k // 2, "pre_relu": 1, "post_relu": 0}
+    ops = [sep("g1", "x", 100, 3), sep("g2", "x", 36, 5), sep("g3", "g1", 40, 5)]
+    return {"name": "sepg", "batch": batch, "inputs": [{"name": "x", "c": 40, "h": 20, "w": 21}],
+            "ops": ops, "outputs": ["g2", "g3"]}
+
+
+@pytest.mark.parametrize("tile", ["7", "8"])
+def test_parity_sepconv_gemm_batched(tile, monkeypatch):
+    """The GEMM SEPCONV tile forced on every unit of a NASNet cell (128
+    columns: 42-wide planes) or of sepg_spec (64 columns), over three images
+    (row blocks of every image, halo rows at image borders), under greedy
+    stages and one chained stage."""
+    monkeypatch.setenv("IOS_SEP_TILE", tile)
+    if tile == "7":
+        spec, ten, refs = batched_reference("nasnet", 3)
+    else:
+        spec = sepg_spec(3)
+        ten = W.make_tensors(spec, 5)
+        refs = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    seps = [u["name"] for u in W.unit_ops(spec) if u["kind"] == "sepconv"]
+    assert all(I.ios_get_unit_tiling(g.handle, g.tid[n])[0] == int(tile) for n in seps)
+    for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), refs, f"{spec['name']}/bs3/sep tile {tile}")
         I.ios_schedule_destroy(q)
     g.close()
 

@@ -84,6 +84,8 @@ void fill_common(const ios_graph *g, const Op &op, DevOp &d) {
 
 // The kernel's tile order across XCDs (workgroup b on XCD b % 8 runs tile
 // xcd_tile(b, n, lg), per round of `grid` tiles).
+constexpr int kXcdsHost = 8;   // XCDs of an MI355X: workgroup b runs on XCD b % 8
+
 static int xcd_tile_host(int b, int n, int lg) {
   const int full = (n >> (3 + lg)) << (3 + lg);
   if (b >= full) return b;
@@ -110,7 +112,7 @@ static int choose_xcd_runs(const std::vector<DevOp> &ops, const std::vector<int3
         const int t = base + xcd_tile_host(b, std::min(grid, n - base), lg);
         const int i = (int)(std::upper_bound(start.begin(), start.end(), t) - start.begin()) - 1;
         const DevOp &d = ops[i];
-        if (d.kind != DK_CONV) continue;
+        if (d.kind != DK_CONV || t - start[i] >= d.n_tiles) continue;   // padding between op ranges
         const int ti = t - start[i], tm = ti / d.tiles_n, tn = ti % d.tiles_n;
         if (a_seen.insert({i, b & 7, tm}).second) bytes += 4.0 * tile_bm(d.tcfg) * d.CinP * d.kh;
         if (b_seen.insert({i, b & 7, tn}).second)
@@ -490,13 +492,21 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
   std::vector<DevOp> sorted;
   std::vector<int32_t> start{0};
   bool persistent = false, big_conv = false, has_sep = false, has_row = false, has_pipe = false;
+  for (const DevOp &d : dops) persistent |= d.n_deps > 0;
   int lds = 0;
-  for (int i : order) {
-    DevOp d = dops[i];
-    for (int k = 0; k < d.n_deps; ++k) d.dep[k] = pos[d.dep[k]];
+  for (size_t k = 0; k < order.size(); ++k) {
+    DevOp d = dops[order[k]];
+    for (int j = 0; j < d.n_deps; ++j) d.dep[j] = pos[d.dep[j]];
     sorted.push_back(d);
-    start.push_back(start.back() + d.n_tiles);
-    persistent |= d.n_deps > 0;
+    // Each op's range starts at a multiple of the XCD count (one tile per
+    // workgroup launches): workgroup b runs on XCD b % 8, so tile i of every
+    // op lands on the same XCD, and ops that read one tensor with the same
+    // pixel tiling (the 1x1 convs of an Inception block) share its L2 lines
+    // instead of fetching them once per op.  The padding workgroups exit at
+    // once.
+    int end = start.back() + d.n_tiles;
+    if (!persistent && k + 1 < order.size()) end = round_up(end, kXcdsHost);
+    start.push_back(end);
     big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg) && !tile_is_pipe(d.tcfg);
     has_pipe |= d.kind == DK_CONV && tile_is_pipe(d.tcfg);
     has_sep |= d.kind == DK_SEP && d.sep_row != 1;

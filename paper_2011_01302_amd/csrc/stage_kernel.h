@@ -1556,6 +1556,7 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl
   int ti = t - s0;
   const DevOp *ops = (const DevOp *)(tab + __builtin_amdgcn_readlane(hv, 2));
   const DevOp &op = ops[opi];
+  if (ti >= U(op.n_tiles)) return;                   // padding between ops' ranges (see the stage table)
 
   const DevOp o = op_scalars(op);
   const int n_deps = o.n_deps, signal = o.signal;

@@ -241,8 +241,10 @@ typedef struct {
 void ios_sched_opts_default(ios_sched_opts *opts);
 
 /* Find a schedule (Algorithm 1, block by block).  With fn == NULL each
- * candidate stage is measured with ios_profile_stage; otherwise fn(ctx, ...)
- * supplies latencies.  Ties: a stage keeps concurrent execution only if it is
+ * candidate stage is measured with ios_profile_stage (a concurrent stage
+ * holding two or more SEPCONVs that admit the GEMM SEPCONV tile is measured
+ * also with them on it, and the faster figure counts, unless IOS_SEP_TILE
+ * fixes the tile choices); otherwise fn(ctx, ...) supplies latencies.  Ties: a stage keeps concurrent execution only if it is
  * strictly faster than merge; among equal-cost endings the smallest
  * block-local mask wins.  *out receives a schedule owned by the caller (free
  * with ios_schedule_destroy) and *cost_ns the minimised sum of stage

@@ -191,7 +191,10 @@ int ios_set_conv_tile(ios_graph *g, int32_t unit_id, int32_t shape);
  * output row with 1 .. 4 blocks of 16 output channels, for at most 256
  * input channels and windows up to 5 x 5; 7, 8: whole output rows in 128
  * or 64 MFMA columns x 64 or 128 output channels, for one input and a
- * 3 x 3 or 5 x 5 window that keeps the plane size), 0 for the other kinds;
+ * 3 x 3 or 5 x 5 window that keeps the plane size; 9, 10: 32 / W whole
+ * output rows x 32 or 64 output channels, with 16-byte loads, for a 3 x 3
+ * window that keeps the plane size, rows of a multiple of 4 up to 32 floats
+ * and at most 96 input channels), 0 for the other kinds;
  * `xcd_lg` is log2 of the run of consecutive tiles a stage holding the
  * unit sends to one XCD (0, 2 or 4), or -1 to let the library's L2-fill
  * model choose (ios_schedule_tune_tiles sets both per stage).  A stage whose

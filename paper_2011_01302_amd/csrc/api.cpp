@@ -92,6 +92,7 @@ void ios_graph_destroy(ios_graph *g) {
     if (op.d_pw_row) (void)hipFree(op.d_pw_row);
     if (op.d_wg) (void)hipFree(op.d_wg);
     if (op.d_pw_pipe) (void)hipFree(op.d_pw_pipe);
+    if (op.d_pw_line) (void)hipFree(op.d_pw_line);
   }
   CompiledStage &s = g->prof_stage;
   if (s.d_table) (void)hipFree(s.d_table);

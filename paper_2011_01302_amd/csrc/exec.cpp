@@ -137,6 +137,7 @@ double tile_work(const DevOp &d) {
     case DK_SEP:
       if (d.sep_row == 2)
         return (double)d.sepg_rout * d.Wo * d.CinP * (d.kh * d.kw + 32.0 * (kWaves / d.sep_nbt)) / kWaves;
+      if (d.sep_row == 3) return 32.0 * d.CinP * (9.0 * d.n_in + 32.0 * d.sep_nbt) / kWaves;
       if (d.sep_row) return 16.0 * d.CinP * (d.row_k * d.row_k * d.n_in + 16.0 * d.sep_nbt) / kWaves;
       return (double)d.sep_bm * d.CinP * (d.kh * d.kw + 16.0 * d.sep_nbt) / kWaves;
     default:
@@ -327,6 +328,23 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
           }
           break;
         case IOS_SEPCONV: {
+          if (o.sep_tile >= kSepLineFirst) {
+            // line tile (see the stage kernel)
+            const int nb = 1 << (o.sep_tile - kSepLineFirst);
+            const LineGeom lg = line_geometry(nb, o.cin, o.d.cout, o.d.kh, o.d.kw, o.d.pad_h, o.d.pad_w,
+                                              o.d.stride_h, o.d.stride_w, o.h, o.wd, o.ho, o.wo);
+            if (lg.r == 0 || !o.d_pw_line || !o.d_dw_row) fail(IOS_E_UNSUPPORTED, "SEPCONV line tile does not apply");
+            d.kind = DK_SEP; d.sep_row = 3;
+            d.CinP = round_up(o.cin, 4); d.Npad = o.Npad;
+            d.sep_nbt = nb;
+            d.row_k = 3;
+            d.line_r = lg.r; d.line_rows = lg.rows; d.line_q = lg.q; d.line_chp = lg.chp;
+            d.line_nks = lg.nks; d.line_pitch = lg.pitch;
+            d.wpk = o.d_pw_line; d.bias = o.d_bias; d.dw = o.d_dw_row;
+            d.w_bytes = (int32_t)((size_t)cdiv(o.d.cout, 32) * lg.nks * 64 * sizeof(float));
+            d.dw_bytes = (int32_t)((size_t)d.CinP * sep_kkp(3) * sizeof(float));
+            break;
+          }
           if (o.sep_tile >= kSepgFirst) {
             // GEMM tile (see the stage kernel)
             const SepgGeom sg = sepg_geometry(o.sep_tile - kSepgFirst, (int)o.in.size(), o.d.kh, o.d.kw,
@@ -404,6 +422,11 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.tiles_per_plane = cdiv(d.Ho, d.sepg_rout);
       d.tiles_m = d.N * d.tiles_per_plane;
       d.tiles_n = cdiv(d.Cout, 32 * (kWaves / d.sep_nbt));
+    } else if (d.kind == DK_SEP && d.sep_row == 3) {
+      // line tile: (image, block of line_r output rows) x groups of 32 sep_nbt channels
+      d.tiles_per_plane = cdiv(d.Ho, d.line_r);
+      d.tiles_m = d.N * d.tiles_per_plane;
+      d.tiles_n = cdiv(d.Cout, 32 * d.sep_nbt);
     } else if (d.kind == DK_SEP && d.sep_row) {
       // row tile: (image, output row, 16-pixel block of the row) x groups of
       // sep_nbt 16-channel output blocks
@@ -473,6 +496,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     d.fd_tpp = fd(d.tiles_per_plane);
     d.fd_c = fd(d.Cout);
     d.fd_pin = fd(d.pool_in_rows * d.W);
+    d.fd_lq = fd(d.line_q);
+    d.fd_lw4 = fd(d.W / 4);
   }
   // tile order: producers before consumers (depth), longer tiles first; the
   // ops are stored in that order so that each owns a contiguous tile range
@@ -509,8 +534,8 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
     start.push_back(end);
     big_conv |= d.kind == DK_CONV && !tile_is_light(d.tcfg) && !tile_is_pipe(d.tcfg);
     has_pipe |= d.kind == DK_CONV && tile_is_pipe(d.tcfg);
-    has_sep |= d.kind == DK_SEP && d.sep_row != 1;
-    has_row |= d.kind == DK_SEP && d.sep_row == 1;
+    has_sep |= d.kind == DK_SEP && (d.sep_row == 0 || d.sep_row == 2);
+    has_row |= d.kind == DK_SEP && (d.sep_row == 1 || d.sep_row == 3);
     lds = std::max(lds, op_lds_bytes(d));
   }
   cs->ops = sorted;

@@ -361,6 +361,9 @@ bool conv_tile_ok(const Op &op, int cfg) {
 
 bool sep_tile_ok(const Op &op, int tile) {
   if (tile < 0 || tile >= kSepTiles) return false;
+  if (tile >= kSepLineFirst)
+    return line_geometry(1 << (tile - kSepLineFirst), op.cin, op.d.cout, op.d.kh, op.d.kw, op.d.pad_h, op.d.pad_w,
+                         op.d.stride_h, op.d.stride_w, op.h, op.wd, op.ho, op.wo).r != 0;
   if (tile >= kSepgFirst)
     return sepg_geometry(tile - kSepgFirst, (int)op.in.size(), op.d.kh, op.d.kw, op.d.pad_h, op.d.pad_w, op.h,
                          op.wd, op.ho, op.wo).bm != 0;
@@ -371,7 +374,7 @@ bool sep_tile_ok(const Op &op, int tile) {
          sep_row_lds_bytes(round_up(op.cin, 4), K, nbt) <= kSepMaxLds;
 }
 
-// SEPCONV tile choice before measurement (IOS_SEP_TILE=<0..8> forces one;
+// SEPCONV tile choice before measurement (IOS_SEP_TILE=<0..10> forces one;
 // a choice the operator cannot use falls back to the staged tile of 16
 // pixels).
 static int choose_sep_tile(const Op &op) {
@@ -493,6 +496,22 @@ void ensure_device(ios_graph *g) {
           for (int ci = 0; ci < op.cin; ++ci) pwr[(size_t)ci * op.Npad + co] = pw[(size_t)co * op.cin + ci];
         op.d_dw_row = upload(dwr);
         op.d_pw_row = upload(pwr);
+      }
+      // the line tile's pointwise layout, where it applies: the A operands of
+      // v_mfma_f32_32x32x2_f32, [block of 32 output channels][k-step of 2
+      // input channels][lane = 32 k + channel in the block]
+      if (sep_tile_ok(op, kSepLineFirst)) {
+        const int nblk = (op.d.cout + 31) / 32, nks = (op.cin + 1) / 2;
+        const float *pw = op.w.data() + (size_t)op.cin * taps;
+        std::vector<float> pwl((size_t)nblk * nks * 64, 0.f);
+        for (int b = 0; b < nblk; ++b)
+          for (int ks = 0; ks < nks; ++ks)
+            for (int l = 0; l < 64; ++l) {
+              const int co = b * 32 + (l & 31), ci = 2 * ks + (l >> 5);
+              if (co < op.d.cout && ci < op.cin)
+                pwl[((size_t)b * nks + ks) * 64 + l] = pw[(size_t)co * op.cin + ci];
+            }
+        op.d_pw_line = upload(pwl);
       }
     }
   }

@@ -127,12 +127,16 @@ inline bool pipe_conv_ok(int cin, int taps, int pre_relu) {
 // row x 1 .. kSepRowMaxNB channel blocks; Cin <= 256, windows up to 5 x 5),
 // then kSepgTiles choices of the GEMM tile (whole output rows in 128 or 64
 // MFMA columns x 64 or 128 output channels; one input, 3 x 3 or 5 x 5
-// windows that keep the size).
+// windows that keep the size), then kSepLineTiles choices of the line tile
+// (32 / Wo whole output rows x 32 or 64 output channels; 3 x 3 windows that
+// keep the size, rows of a multiple of 4 floats up to 32, Cin <= 96).
 constexpr int kSepStagedTiles = 3;       // BM = 16, 32, 64
 constexpr int kSepRowMaxNB = 4;
 constexpr int kSepgTiles = 2;
 constexpr int kSepgFirst = kSepStagedTiles + kSepRowMaxNB;
-constexpr int kSepTiles = kSepgFirst + kSepgTiles;
+constexpr int kSepLineTiles = 2;
+constexpr int kSepLineFirst = kSepgFirst + kSepgTiles;
+constexpr int kSepTiles = kSepLineFirst + kSepLineTiles;
 constexpr int kSepgStages = 3;           // GEMM tile: ring slots of 16 input channels (two chunks in flight)
 constexpr int kSepgMaxRows = 4;          // GEMM tile: output rows per tile at most
 constexpr int kSepgMaxCopies = 12;       // GEMM tile: 64-float input copies per wave and chunk at most
@@ -170,6 +174,49 @@ inline SepgGeom sepg_geometry(int choice, int n_in, int kh, int kw, int ph, int 
   return g;
 }
 
+// Line tile geometry (r = 0: the choice does not apply): r output rows per
+// tile (r Wo <= 32 MFMA columns), rows = r + 2 input rows staged per channel,
+// q = rows W / 4 16-byte pieces per channel, chp = 512 / q channels loaded at
+// once (a thread loads kLineMaxLoads channels of one piece at most), nks =
+// k-steps of 2 channels, pitch = W + 8 floats per staged row (the data at
+// column 4, zeros around it).  LDS (floats): the staged rows [2 nks][rows]
+// [pitch] (later the partial sums [8 waves][16][64]), the depthwise outputs
+// [nks][64] (at dwb), the depthwise weights [2 nks][kkp] (dww), the pointwise
+// weights [nb][nks][64] (al), the biases [32 nb] (bl).
+constexpr int kLineInFlight = 4;         // inputs whose loads are in flight at once
+constexpr int kLineMaxLoads = 4;         // 16-byte loads per thread and input
+constexpr int kLineMaxCin = 96;
+constexpr int kLineMaxLds = 128 * 1024;  // bytes (the stage table comes on top)
+struct LineGeom {
+  int r = 0, rows = 0, q = 0, chp = 0, nks = 0, pitch = 0;
+  int dwb = 0, dww = 0, al = 0, bl = 0, floats = 0;
+};
+__host__ __device__ inline void line_offsets(LineGeom &g, int nb) {
+  const int slab = 2 * g.nks * g.rows * g.pitch, red = 8 * 1024;
+  g.dwb = slab > red ? slab : red;
+  g.dww = g.dwb + g.nks * 64;
+  g.al = g.dww + 2 * g.nks * 12;
+  g.bl = g.al + nb * g.nks * 64;
+  g.floats = g.bl + ((32 * nb + 63) & ~63);
+}
+inline LineGeom line_geometry(int nb, int cin, int cout, int kh, int kw, int ph, int pw, int sh, int sw, int H,
+                              int W, int Ho, int Wo) {
+  LineGeom g;
+  if (kh != 3 || kw != 3 || ph != 1 || pw != 1 || sh != 1 || sw != 1 || Ho != H || Wo != W || W % 4 != 0 ||
+      W > 32 || cin < 1 || cin > kLineMaxCin || cout < 1 || (nb > 1 && cout <= 16 * nb))
+    return g;
+  g.r = std::min(32 / W, Ho);
+  g.rows = g.r + 2;
+  g.q = g.rows * (W / 4);
+  g.chp = 512 / g.q;
+  g.nks = (cin + 1) / 2;
+  g.pitch = W + 8;
+  if (g.chp < 1 || (2 * g.nks + g.chp - 1) / g.chp > kLineMaxLoads) return LineGeom{};
+  line_offsets(g, nb);
+  if (g.floats * 4 > kLineMaxLds) return LineGeom{};
+  return g;
+}
+
 constexpr int kSepRowMaxChannels = 256;
 constexpr int kSepPairs = 4;             // (pixel block, channel block) pairs per wave at most
 constexpr int kSepStagePerThread = 8;   // staged input floats per thread and chunk at most
@@ -204,9 +251,13 @@ __host__ __device__ inline int sep_row_wave_floats(int CinP, int K, int nbt) {
   const int ksw = (CinP / 4 + 7) / 8;
   return ((ksw * 4 * (sep_kkp(K) + 16 * nbt) + 63) & ~63) + 64;
 }
-__host__ __device__ inline int sep_row_lds_bytes(int CinP, int K, int nbt) {
+// The tile's biases (16 nbt floats, 64 reserved) follow both regions.
+__host__ __device__ inline int sep_row_bias_offset(int CinP, int K, int nbt) {
   const int w = 8 * sep_row_wave_floats(CinP, K, nbt), r = 8 * kSepRowMaxNB * 16 * 17;
-  return (w > r ? w : r) * 4;
+  return w > r ? w : r;
+}
+__host__ __device__ inline int sep_row_lds_bytes(int CinP, int K, int nbt) {
+  return (sep_row_bias_offset(CinP, K, nbt) + 64) * 4;
 }
 // LDS of a SEPCONV tile in floats: the staged input and depthwise weights of
 // one chunk, two pointwise weight buffers, the depthwise outputs and the
@@ -263,11 +314,15 @@ struct alignas(16) DevOp {
   int32_t sep_ck, sep_nck;     // SEP: input channels per chunk, chunks
   int32_t sep_rows;            // SEP: input rows staged per chunk
   int32_t sep_nbt;             // SEP: 16-channel output blocks per tile
-  int32_t sep_row;             // SEP: 0 = staged tile, 1 = row tile, 2 = GEMM tile (sep_nbt = its waves along pixels)
+  int32_t sep_row;             // SEP: 0 = staged tile, 1 = row tile, 2 = GEMM tile (sep_nbt = its waves along
+                               // pixels), 3 = line tile (sep_nbt = its 32-channel output blocks)
   int32_t sepg_rout, sepg_w2;  // SEP GEMM tile: output rows per tile, staged row pitch (W + 2 pw)
   int32_t sepg_strips, sepg_ps;// SEP GEMM tile: depthwise strips of 2 columns per row, staged plane pitch
   int32_t sepg_xs, sepg_ws;    // SEP GEMM tile: floats per ring slot of the input planes and depthwise weights
   int32_t row_k, row_bpr;      // SEP row tile: padded window K, 16-pixel blocks per output row
+  int32_t line_r, line_rows;   // SEP line tile: output rows per tile, staged input rows (see LineGeom)
+  int32_t line_q, line_chp;    // SEP line tile: 16-byte pieces per staged channel, channels loaded at once
+  int32_t line_nks, line_pitch;// SEP line tile: k-steps of 2 channels, staged row pitch
   int32_t pipe_ldw;            // CONV pipelined tile: row length of the packed weights (NG = k-blocks)
   int32_t w_bytes;             // size of wpk in bytes
   int32_t dw_bytes;            // SEP: size of dw in bytes
@@ -281,6 +336,7 @@ struct alignas(16) DevOp {
   FDiv fd_ps, fd_w2, fd_strips;// SEP GEMM tile: sepg_ps, sepg_w2, sepg_strips
   FDiv fd_tpp, fd_c;           // POOL / ADD / MEAN: tiles_per_plane, Cout
   FDiv fd_pin;                 // POOL with planes_per_tile > 1: floats staged per plane
+  FDiv fd_lq, fd_lw4;          // SEP line tile: line_q, W / 4
   const float *wpk;            // CONV: see pack_conv_weights; SEP: the pointwise weights packed the same way
   const float *bias;           // [Npad]
   const float *dw;             // SEP: depthwise [round16(Cin)][kh * kw], channels past Cin zero
@@ -356,6 +412,7 @@ struct Op {
   float *d_wpk = nullptr, *d_bias = nullptr, *d_dw = nullptr;
   float *d_pw_pipe = nullptr;    // SEPCONV GEMM tile: pointwise weights packed like a pipelined 1x1 conv's
   float *d_dw_row = nullptr, *d_pw_row = nullptr;   // SEPCONV row tile: [CinP4][kkp(K)], [CinP4][Npad]
+  float *d_pw_line = nullptr;    // SEPCONV line tile: pointwise [ceil(Cout/32)][ceil(Cin/2)][64] (A operands)
   float *d_wg = nullptr;         // CONV, pipelined tiles: [nkb * kPipeKB][round128(Cout)]
   int pipe_nkb = 0;
 };

@@ -54,6 +54,22 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *p, int bytes)
 __device__ __forceinline__ float bld(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
+__device__ __forceinline__ floatx4 bld4(__amdgpu_buffer_rsrc_t r, int voff) {
+  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+// Biases of a 32x32 MFMA accumulator's channels: lane l holds the bias of
+// channel base + l % 32, loaded before the tile's main loop so that its round
+// trip overlaps the operand loads; element r of lane l belongs to channel
+// base + 8 (r / 4) + 4 (l / 32) + r % 4, taken from that lane by a permute.
+__device__ __forceinline__ float bias32_load(const float *bias, int base, int cout, int lane) {
+  const int n = base + (lane & 31);
+  return bld(rsrc(bias, cout * 4), n < cout ? n * 4 : kOOB, 0);
+}
+__device__ __forceinline__ float bias32_of(float bl, int r, int lane) {
+  const int src = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src * 4, __builtin_bit_cast(int, bl)));
+}
 
 // Activation accesses.  COH = true for outputs consumed by another tile of
 // the same launch: agent-coherent (sc1) stores, performed beyond the
@@ -432,6 +448,7 @@ __device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op,
   }
   const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
+  const float bl = bias32_load(o.bias, n0 + wn * 32, o.Cout, lane);
 
   // scalar walk of the next block to issue: tap (u, v), first channel c
   int tap = 0, tu = 0, tv = 0, c = 0;
@@ -490,13 +507,16 @@ __device__ __forceinline__ void conv_pipe_tile(const Slots &sl, const DevOp &op,
   }
   // epilogue: element r of lane l is channel n0 + 32 wn + 8 (r/4) + 4 (l/32) + r%4 of pixel m0 + 32 wm + l%32
   const int m = m0 + wm * 32 + (lane & 31);
+  float bv16[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) bv16[r] = bias32_of(bl, r, lane);
   if (m < M) {
     const int img = fdiv(m, o.fd_howo), pix = m - img * howo;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (n < o.Cout) {
-        float v = acc[r] + o.bias[n];
+        float v = acc[r] + bv16[r];
         if (o.post_relu) v = fmaxf(v, 0.f);
         st<COH>(route_ptr(sl, op, o, n, img, pix, howo), v);
       }
@@ -559,6 +579,7 @@ __device__ __forceinline__ void conv_wave_tile(const Slots &sl, const DevOp &op,
   const int aoff = (kq * ldw + n0 + l32) * 4;
   const __amdgpu_buffer_rsrc_t xr = rsrc(sl[o.in_slot[0]], o.in_bytes[0]);
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
+  const float bl = bias32_load(o.bias, n0, o.Cout, lane);
 
   // scalar walk of the next block to issue: tap (u, v), first channel c
   int tap = 0, tu = 0, tv = 0, c = 0;
@@ -605,13 +626,16 @@ __device__ __forceinline__ void conv_wave_tile(const Slots &sl, const DevOp &op,
     asm volatile("" ::: "memory");
   }
   // epilogue: element r of lane l is channel n0 + 8 (r/4) + 4 (l/32) + r%4 of pixel m
+  float bv16[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) bv16[r] = bias32_of(bl, r, lane);
   if (m < M) {
     const int img = fdiv(m, o.fd_howo), pix = m - img * howo;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int n = n0 + 8 * (r >> 2) + 4 * kq + (r & 3);
       if (n < o.Cout) {
-        float v = acc[r] + o.bias[n];
+        float v = acc[r] + bv16[r];
         if (o.post_relu) v = fmaxf(v, 0.f);
         st<COH>(route_ptr(sl, op, o, n, img, pix, howo), v);
       }
@@ -933,6 +957,12 @@ __device__ __forceinline__ void sep_row_tile(const Slots &sl, const DevOp &op, c
   const int nb0 = tn * o.sep_nbt, nbc = min(o.sep_nbt, (o.Npad >> 4) - nb0);
   const int pitch = nbc * 16;                         // pointwise weights row in LDS
   const int Cin = o.Cin, kh = o.kh, ph = o.ph;
+  const int NC = nbc * 16;
+
+  // (0) the tile's biases -> LDS past the weights and partial sums, copied
+  //     first so that their round trip overlaps the weights' and inputs'
+  float *bl = lds + sep_row_bias_offset(o.CinP, K, o.sep_nbt);
+  if (wave == 0 && lane < NC) lds_dma(rsrc(o.bias, o.Npad * 4), bl, (nb0 * 16 + lane) * 4);
 
   // (1) this wave's weights -> its LDS region: depthwise [4 nks][KKP], then
   //     pointwise rows 4 ks0 .. 4 (ks0 + nks) - 1, columns of this tile
@@ -1052,16 +1082,203 @@ __device__ __forceinline__ void sep_row_tile(const Slots &sl, const DevOp &op, c
       for (int e = 0; e < 4; ++e) lds[(wave * NBT * 16 + nb * 16 + j) * LDR + 4 * g + e] = acc[nb][e];
     }
   __syncthreads();
-  const int NC = nbc * 16;
   for (int idx = tid; idx < NC * 16; idx += kThreads) {
     const int col = idx >> 4, px = idx & 15;
     const int n = nb0 * 16 + col, ow = ow0 + px;
     if (ow >= Wo || n >= o.Cout) continue;
-    float v = o.bias[n];
+    float v = bl[col];
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += lds[(w * NBT * 16 + col) * LDR + px];
     if (o.post_relu) v = fmaxf(v, 0.f);
     st<COH>(route_ptr(sl, op, o, n, img, oh * Wo + ow, howo), v);
+  }
+}
+
+// "Relu-SepConv" unit, line tile: R = line_r whole output rows (R Wo <= 32
+// pixels) x 32 NB output channels per workgroup (NB = 1 or 2), 3 x 3 windows, rows of a
+// multiple of 4 floats.  Every global load is 16 bytes wide, so that a
+// workgroup issues few vector memory instructions for what it reads (at batch
+// 1 the stage is bound by that issue rate, not by bytes):
+//  (1) the R + 2 input rows of every channel (contiguous in memory) are
+//      loaded by thread (channel cp + chp j, 16-byte piece q), the loads of up
+//      to kLineInFlight inputs in flight at once; their sum, rectified, goes
+//      to LDS with four zero columns on each side.  The depthwise weights, the
+//      tile's pointwise weights and biases are loaded before the inputs.
+//  (2) the depthwise output of (channel c, pixel p) goes to LDS word
+//      32 c + p: k-step ks of v_mfma_f32_32x32x2_f32 (channels 2 ks, 2 ks + 1)
+//      then reads its B operand [k = lane / 32][pixel = lane % 32] as the 64
+//      words from 64 ks, and the pointwise weights are packed the same way
+//      ([block][ks][lane], lane = 32 k + output channel).
+//  (3) wave w multiplies output block w % NB over k-steps [kw KSW, (kw + 1)
+//      KSW), kw = w / NB, and the 8 / NB waves of a block add their partial
+//      sums in LDS before the bias and the store.
+template <int NB, bool COH>
+__device__ __forceinline__ void sep_line_tile(const Slots &sl, const DevOp &op, const DevOp &o, int t, float *lds) {
+  constexpr int KW = kWaves / NB, IF = kLineInFlight, NLD = kLineMaxLoads;
+  constexpr int MAXKS = (kLineMaxCin + 1) / 2;
+  constexpr int AJ = (NB * MAXKS * 16 + kThreads - 1) / kThreads;     // 16-byte pointwise loads per thread
+  constexpr int DJ = (2 * MAXKS * 12 / 4 + kThreads - 1) / kThreads;  // 16-byte depthwise loads per thread
+  static_assert(kWaves % NB == 0, "waves split evenly over the output blocks");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tm = fdiv(t, o.fd_tn), tn = t - tm * o.tiles_n;
+  const int img = fdiv(tm, o.fd_pimg), rb = tm - img * o.tiles_per_plane;
+  const int H = o.H, W = o.W, Wo = o.Wo, Ho = o.Ho, howo = Ho * Wo, HW = H * W;
+  LineGeom g;
+  g.r = o.line_r; g.rows = o.line_rows; g.q = o.line_q; g.chp = o.line_chp; g.nks = o.line_nks;
+  g.pitch = o.line_pitch;
+  line_offsets(g, NB);
+  const int R = g.r, ROWS = g.rows, PITCH = g.pitch, NKS = g.nks, CE = 2 * NKS;
+  const int oh0 = rb * R, ih0 = oh0 - o.ph, cb0 = tn * NB, Cin = o.Cin;
+  float *slab = lds, *dwb = lds + g.dwb, *dww = lds + g.dww, *al = lds + g.al, *bl = lds + g.bl;
+
+  // (0) weights and biases: issued first, stored to LDS once the first
+  //     inputs' loads are in flight
+  if (tid < 32 * NB) lds_dma(rsrc(o.bias, o.Cout * 4), bl + wave * 64, (cb0 * 32 + tid) * 4);
+  floatx4 av[AJ], dv[DJ];
+  {
+    const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes), dr = rsrc(o.dw, o.dw_bytes);
+    const int na = NB * NKS * 16, nd = CE * 3;        // 16-byte pieces
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+      const int f = tid + j * kThreads;
+      av[j] = bld4(wr, f < na ? (cb0 * NKS * 64 + 4 * f) * 4 : kOOB);
+    }
+#pragma unroll
+    for (int j = 0; j < DJ; ++j) {
+      const int f = tid + j * kThreads;
+      dv[j] = bld4(dr, f < nd ? 16 * f : kOOB);
+    }
+  }
+  // zero columns of the staged rows
+  for (int i = tid; i < CE * ROWS; i += kThreads) {
+    *(floatx4 *)(slab + i * PITCH) = floatx4{0.f, 0.f, 0.f, 0.f};
+    *(floatx4 *)(slab + i * PITCH + 4 + W) = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // (1) this thread's piece: channel cp + chp j, staged row r, columns 4 c4 ..
+  const int cp = fdiv(tid, o.fd_lq), qq = tid - cp * g.q;
+  const int r = fdiv(qq, o.fd_lw4), c4 = qq - r * (W >> 2), ih = ih0 + r;
+  const bool act = cp < g.chp && ih >= 0 && ih < H;
+  const int pix4 = (ih * W + 4 * c4) * 4;
+  floatx4 S[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) S[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int n_in = o.n_in;
+  for (int k0 = 0; k0 < n_in; k0 += IF) {
+    floatx4 X[IF][NLD];
+#pragma unroll
+    for (int i = 0; i < IF; ++i) {
+      const int k = k0 + i;
+      if (k < n_in) {                                 // uniform
+        const __amdgpu_buffer_rsrc_t xr = rsrc(sl[U(op.in_slot[k])], U(op.in_bytes[k]));
+        const int base = (img * U(op.in_ctot[k]) + U(op.in_coff[k]) + cp) * HW * 4 + pix4;
+#pragma unroll
+        for (int j = 0; j < NLD; ++j)
+          X[i][j] = bld4(xr, act && cp + g.chp * j < Cin ? base + g.chp * j * HW * 4 : kOOB);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NLD; ++j) X[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if (k0 == 0) {
+      const int na = NB * NKS * 16, nd = CE * 3;
+#pragma unroll
+      for (int j = 0; j < AJ; ++j)
+        if (tid + j * kThreads < na) *(floatx4 *)(al + 4 * (tid + j * kThreads)) = av[j];
+#pragma unroll
+      for (int j = 0; j < DJ; ++j)
+        if (tid + j * kThreads < nd) *(floatx4 *)(dww + 4 * (tid + j * kThreads)) = dv[j];
+    }
+#pragma unroll
+    for (int i = 0; i < IF; ++i)
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) S[j] += X[i][j];
+  }
+  const bool relu_in = o.pre_relu != 0;
+  if (cp < g.chp) {
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      const int ch = cp + g.chp * j;
+      if (ch < CE) {
+        floatx4 v = S[j];
+        if (relu_in) {
+          v.x = fmaxf(v.x, 0.f); v.y = fmaxf(v.y, 0.f); v.z = fmaxf(v.z, 0.f); v.w = fmaxf(v.w, 0.f);
+        }
+        *(floatx4 *)(slab + (ch * ROWS + r) * PITCH + 4 + 4 * c4) = v;
+      }
+    }
+  }
+  lds_dma_wait();                                     // the biases' copy (wave 0, 1)
+  __syncthreads();
+
+  // (2) depthwise: item e = (channel e / 8, pixels 4 (e % 8) .. + 3)
+  for (int e = tid; e < CE * 8; e += kThreads) {
+    const int ch = e >> 3, p0 = (e & 7) * 4;
+    const int ro = fdiv(p0, o.fd_wo), x0 = p0 - ro * Wo;
+    floatx4 d{0.f, 0.f, 0.f, 0.f};
+    if (ro < R) {
+      float w[12];
+#pragma unroll
+      for (int q4 = 0; q4 < 3; ++q4) {
+        const floatx4 t4 = *(const floatx4 *)(dww + ch * 12 + 4 * q4);
+        w[4 * q4] = t4.x; w[4 * q4 + 1] = t4.y; w[4 * q4 + 2] = t4.z; w[4 * q4 + 3] = t4.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const float *row = slab + (ch * ROWS + ro + u) * PITCH + x0;   // columns x0 - 4 .. x0 + 7
+        const floatx4 a0 = *(const floatx4 *)row, a1 = *(const floatx4 *)(row + 4),
+                      a2 = *(const floatx4 *)(row + 8);
+        const float v[12] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w, a2.x, a2.y, a2.z, a2.w};
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+          const float wt = w[u * 3 + c];
+          d.x = fmaf(wt, v[3 + c], d.x);
+          d.y = fmaf(wt, v[4 + c], d.y);
+          d.z = fmaf(wt, v[5 + c], d.z);
+          d.w = fmaf(wt, v[6 + c], d.w);
+        }
+      }
+    }
+    *(floatx4 *)(dwb + ch * 32 + p0) = d;
+  }
+  __syncthreads();
+
+  // (3) pointwise on the matrix cores: wave w multiplies block w % NB over
+  //     k-steps [kw KSW, (kw + 1) KSW), kw = w / NB; then the partial sums of
+  //     the KW waves of each block through LDS (over the staged rows, which
+  //     are no longer read)
+  const int cbl = wave % NB, kw = wave / NB;
+  const int ksw = (NKS + KW - 1) / KW, ks0 = kw * ksw, ks1 = min(NKS, ks0 + ksw);
+  floatx16 acc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  {
+    const float *ap = al + cbl * NKS * 64 + lane, *bp = dwb + lane;
+    int ks = ks0;
+    for (; ks + 2 <= ks1; ks += 2) {
+      const float a0 = ap[ks * 64], b0 = bp[ks * 64], a1 = ap[ks * 64 + 64], b1 = bp[ks * 64 + 64];
+      acc = mfma32x32x2(a0, b0, acc);
+      acc = mfma32x32x2(a1, b1, acc);
+    }
+    if (ks < ks1) acc = mfma32x32x2(ap[ks * 64], bp[ks * 64], acc);
+  }
+  float *red = lds;                                   // [kw][block][16][64]
+#pragma unroll
+  for (int i = 0; i < 16; ++i) red[((kw * NB + cbl) * 16 + i) * 64 + lane] = acc[i];
+  __syncthreads();
+  for (int idx = tid; idx < NB * 1024; idx += kThreads) {
+    const int b = idx >> 10, i = (idx >> 6) & 15, l = idx & 63;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < KW; ++w) v += red[((w * NB + b) * 16 + i) * 64 + l];
+    const int cl = b * 32 + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3), n = cb0 * 32 + cl, p = l & 31;
+    const int ro = fdiv(p, o.fd_wo), x = p - ro * Wo, oh = oh0 + ro;
+    if (n < o.Cout && ro < R && oh < Ho) {
+      v += bl[cl];
+      if (o.post_relu) v = fmaxf(v, 0.f);
+      st<COH>(route_ptr(sl, op, o, n, img, oh * Wo + x, howo), v);
+    }
   }
 }
 
@@ -1214,6 +1431,7 @@ __device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, 
   const __amdgpu_buffer_rsrc_t wr = rsrc(o.wpk, o.w_bytes);
   const __amdgpu_buffer_rsrc_t dr = rsrc(o.dw, o.dw_bytes);
   const int hw4 = H * W * 4;
+  const float bl = bias32_load(o.bias, n0 + wn * 32, o.Cout, lane);
   // loads per wave and chunk (the same for every chunk)
   int per = AC;
 #pragma unroll
@@ -1281,13 +1499,16 @@ __device__ __forceinline__ void sep_gemm_tile(const Slots &sl, const DevOp &op, 
   }
   // epilogue: element i of lane l is channel n0 + 32 wn + 8 (i/4) + 4 (l/32) + i%4 of tile column 32 wm + l%32
   const int px = wm * 32 + (lane & 31);
+  float bv16[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) bv16[i] = bias32_of(bl, i, lane);
   if (px < rt * Wo) {
     const int q = oh0 * Wo + px;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int n = n0 + wn * 32 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
       if (n < o.Cout) {
-        float v = acc[i] + o.bias[n];
+        float v = acc[i] + bv16[i];
         if (o.post_relu) v = fmaxf(v, 0.f);
         st<COH>(route_ptr(sl, op, o, n, img, q, howo), v);
       }
@@ -1524,6 +1745,11 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
         } else if (!o.sep_row) {
           if constexpr (KV != KV_SEPROW) sep_tile<COH>(sl, op, o, ti, lds);
         } else if constexpr (KV != KV_SEP) {
+          if (o.sep_row == 3) {
+            if (o.sep_nbt == 1) sep_line_tile<1, COH>(sl, op, o, ti, lds);
+            else sep_line_tile<2, COH>(sl, op, o, ti, lds);
+            break;
+          }
           const bool one = o.n_in == 1;
           if (o.row_k == 3) {
             if (one) sep_row_tile<3, true, COH>(sl, op, o, ti, lds); else sep_row_tile<3, false, COH>(sl, op, o, ti, lds);

@@ -35,6 +35,13 @@ int op_lds_bytes(const DevOp &op) {
   }
   if (op.kind == DK_SEP && op.sep_row == 2)
     return sepg_lds_bytes(op.sepg_xs, op.sepg_ws, 32 * op.sep_nbt, 32 * (kWaves / op.sep_nbt));
+  if (op.kind == DK_SEP && op.sep_row == 3) {
+    LineGeom g;
+    g.r = op.line_r; g.rows = op.line_rows; g.q = op.line_q; g.chp = op.line_chp; g.nks = op.line_nks;
+    g.pitch = op.line_pitch;
+    line_offsets(g, op.sep_nbt);
+    return g.floats * (int)sizeof(float);
+  }
   if (op.kind == DK_SEP && op.sep_row) return sep_row_lds_bytes(op.CinP, op.row_k, op.sep_nbt);
   if (op.kind == DK_SEP)
     return sep_lds_floats(op.sep_bm, op.sep_ck, op.sep_rows, op.W, op.kh * op.kw, op.sep_nbt) * (int)sizeof(float);

@@ -636,10 +636,11 @@ def test_parity_conv_tiles_batched_small(tile, monkeypatch):
     g.close()
 
 
-@pytest.mark.parametrize("tile", [str(t) for t in range(9)])
+@pytest.mark.parametrize("tile", [str(t) for t in range(11)])
 def test_parity_every_sepconv_tile(tile, monkeypatch):
     # SEPCONV tile choice (staged: 16, 32 or 64 output pixels per tile; row:
-    # 1 to 4 channel blocks; GEMM: whole rows in 128 or 64 columns), forced
+    # 1 to 4 channel blocks; GEMM: whole rows in 128 or 64 columns; line:
+    # 32 / W whole rows x 32 or 64 channels, RandWire's 28-wide nodes), forced
     # instead of measured (a unit a choice does not apply to falls back to
     # the staged tile: the wide 7x7 unit and multi-input sums for the row and
     # GEMM tiles; the 3x3 unit over 280 channels, ragged's 5x5 unit over 21
@@ -658,6 +659,56 @@ def test_parity_every_sepconv_tile(tile, monkeypatch):
         g = I.Graph(spec, ten)
         for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
             check(run(g, q, spec, ten), E.outputs(spec, ten), f"{spec['name']}/sep tile {tile}")
+            I.ios_schedule_destroy(q)
+        g.close()
+
+
+def line_spec(batch):
+    """SEPCONVs the line tile applies to: 28-wide planes (one output row per
+    tile) of 77 channels (an odd channel padded to a k-step), a six-input sum
+    (two rounds of loads), chained; 16-wide planes of 15 rows (two output rows
+    per tile, the last tile half past the image) and 33 channels; 8-wide
+    planes of 96 channels (four rows per tile, the most channels); 32-wide
+    planes (four loads per thread).  Output channels 77, 50, 40, 20 and 64:
+    short and whole last blocks of 32 and 64 channels."""
+    sep = lambda n, ins, co: {"name": n, "kind": "sepconv", "in": ins, "cout": co, "kh": 3, "kw": 3, "sh": 1,
+                              "sw": 1, "ph": 1, "pw": 1, "pre_relu": 1, "post_relu": 0}
+    ops = [sep("l1", ["x"], 77),
+           sep("l2", ["x", "y", "l1", "x", "y", "l1"], 50),
+           sep("l3", ["z"], 40),
+           sep("l4", ["u", "u"], 20),
+           sep("l5", ["v"], 64)]
+    return {"name": "line", "batch": batch,
+            "inputs": [{"name": "x", "c": 77, "h": 28, "w": 28}, {"name": "y", "c": 77, "h": 28, "w": 28},
+                       {"name": "z", "c": 33, "h": 15, "w": 16}, {"name": "u", "c": 96, "h": 10, "w": 8},
+                       {"name": "v", "c": 70, "h": 6, "w": 32}],
+            "ops": ops, "outputs": ["l2", "l3", "l4", "l5"]}
+
+
+@pytest.mark.parametrize("tile", ["9", "10"])
+def test_parity_sepconv_line_tile(tile, monkeypatch):
+    """The line SEPCONV tile forced on every unit of line_spec over two
+    images (sequential, greedy and chained stages) and of the RandWire block
+    at batch 1 and 2, every image against the oracle."""
+    monkeypatch.setenv("IOS_SEP_TILE", tile)
+    spec = line_spec(2)
+    ten = W.make_tensors(spec, 6)
+    refs = E.outputs(spec, ten)
+    g = I.Graph(spec, ten)
+    # the two-block choice needs more than 32 output channels: not l4's 20
+    units = ("l1", "l2", "l3", "l4", "l5") if tile == "9" else ("l1", "l2", "l3", "l5")
+    assert all(I.ios_get_unit_tiling(g.handle, g.tid[n])[0] == int(tile) for n in units)
+    for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+        check(run(g, q, spec, ten), refs, f"line/bs2/sep tile {tile}")
+        I.ios_schedule_destroy(q)
+    g.close()
+    for batch in (1, 2):
+        spec, ten, refs = batched_reference("randwire", batch)
+        g = I.Graph(spec, ten)
+        seps = [u["name"] for u in W.unit_ops(spec) if u["kind"] == "sepconv"]
+        assert all(I.ios_get_unit_tiling(g.handle, g.tid[n])[0] == int(tile) for n in seps)
+        for q in (sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
+            check(run(g, q, spec, ten), refs, f"randwire/bs{batch}/sep tile {tile}")
             I.ios_schedule_destroy(q)
         g.close()
 

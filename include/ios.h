@@ -246,8 +246,8 @@ void ios_sched_opts_default(ios_sched_opts *opts);
 /* Find a schedule (Algorithm 1, block by block).  With fn == NULL each
  * candidate stage is measured with ios_profile_stage (a concurrent stage
  * holding two or more SEPCONVs that admit the GEMM SEPCONV tile is measured
- * also with them on it, and the faster figure counts, unless IOS_SEP_TILE
- * fixes the tile choices); otherwise fn(ctx, ...) supplies latencies.  Ties: a stage keeps concurrent execution only if it is
+ * also with them on it, likewise on the 64-channel line tile, and the fastest
+ * figure counts, unless IOS_SEP_TILE fixes the tile choices); otherwise fn(ctx, ...) supplies latencies.  Ties: a stage keeps concurrent execution only if it is
  * strictly faster than merge; among equal-cost endings the smallest
  * block-local mask wins.  *out receives a schedule owned by the caller (free
  * with ios_schedule_destroy) and *cost_ns the minimised sum of stage

@@ -95,39 +95,44 @@ struct Provider {
   int64_t measured = 0;
 
   // A stage of several SEPCONVs can be bound by their throughput together,
-  // which the isolated tile choice of each (the row tile, at batch 1)
-  // misjudges; such a stage is also measured with every SEPCONV that admits
-  // it on the GEMM tile, and the faster figure is the stage's latency (the
-  // per-stage tile tuning of the chosen schedule makes the same choice).
-  // IOS_SEP_TILE in the environment keeps the choices fixed.
+  // which the isolated tile choice of each (the row or the 32-channel line
+  // tile, at batch 1) misjudges; such a stage is also measured with every
+  // SEPCONV that admits it on the GEMM tile, and again on the 64-channel line
+  // tile, and the fastest figure is the stage's latency (the per-stage tile
+  // tuning of the chosen schedule makes the same choice).  IOS_SEP_TILE in
+  // the environment keeps the choices fixed.
   int64_t measure(const std::vector<int> &ops, int strategy, int warmup, int reps, int repeats) {
-    const int64_t ns = profile_stage(g, ops, strategy, warmup, reps, repeats);
+    int64_t ns = profile_stage(g, ops, strategy, warmup, reps, repeats);
     if (strategy != IOS_CONCURRENT || std::getenv("IOS_SEP_TILE")) return ns;
-    std::vector<std::pair<int, int>> saved;
-    for (int oi : ops) {
-      Op &op = g->ops[oi];
-      if (op.d.kind != IOS_SEPCONV) continue;
-      const int v = sep_tile_ok(op, kSepgFirst) ? kSepgFirst : sep_tile_ok(op, kSepgFirst + 1) ? kSepgFirst + 1 : -1;
-      if (v < 0 || v == op.sep_tile) continue;
-      saved.push_back({oi, op.sep_tile});
-      op.sep_tile = v;
-    }
-    auto restore = [&] {
-      for (const auto &p : saved) g->ops[p.first].sep_tile = p.second;
-    };
-    if (saved.size() < 2) {
+    for (const int first : {kSepgFirst, kSepLineFirst + 1}) {
+      const int second = first == kSepgFirst ? kSepgFirst + 1 : kSepLineFirst;
+      std::vector<std::pair<int, int>> saved;
+      for (int oi : ops) {
+        Op &op = g->ops[oi];
+        if (op.d.kind != IOS_SEPCONV) continue;
+        const int v = sep_tile_ok(op, first) ? first : sep_tile_ok(op, second) ? second : -1;
+        if (v < 0 || v == op.sep_tile) continue;
+        saved.push_back({oi, op.sep_tile});
+        op.sep_tile = v;
+      }
+      auto restore = [&] {
+        for (const auto &p : saved) g->ops[p.first].sep_tile = p.second;
+      };
+      if (saved.size() < 2) {
+        restore();
+        continue;
+      }
+      int64_t ns2;
+      try {
+        ns2 = profile_stage(g, ops, strategy, warmup, reps, repeats);
+      } catch (...) {
+        restore();
+        throw;
+      }
       restore();
-      return ns;
+      ns = std::min(ns, ns2);
     }
-    int64_t ns2;
-    try {
-      ns2 = profile_stage(g, ops, strategy, warmup, reps, repeats);
-    } catch (...) {
-      restore();
-      throw;
-    }
-    restore();
-    return std::min(ns, ns2);
+    return ns;
   }
 
   int64_t latency(int block, uint64_t mask, int strategy, bool verify = false) {

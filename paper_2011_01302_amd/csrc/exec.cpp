@@ -461,12 +461,15 @@ void compile_stage(ios_graph *g, const std::vector<int> &ops, int strategy, Comp
       d.planes_per_tile = 1;
       const int in_rows_all = std::min(d.H, (d.Ho - 1) * d.sh - d.ph + d.kh);
       if (rows == d.Ho && in_rows_all > 0) {
-        // small planes: several whole planes per tile, so that the threads
-        // of a tile have outputs to compute
+        // several whole planes per tile when the planes are small (so that
+        // the threads of a tile have outputs to compute) or many (batches:
+        // up to kPoolTileOutputs outputs per tile, so that fewer workgroups
+        // pay the launch prologue), as long as the pool keeps kPoolMinTiles
+        // tiles
         const int in_rows = in_rows_all;
         const int planes = d.N * d.Cout;
-        const int p = std::min({kThreads / (d.Ho * d.Wo), kPoolLdsFloats / (in_rows * d.W),
-                                planes / kPoolMinTiles});
+        const int p = std::min({std::max(kThreads, kPoolTileOutputs) / (d.Ho * d.Wo),
+                                kPoolLdsFloats / (in_rows * d.W), planes / kPoolMinTiles});
         if (p > 1) {
           d.planes_per_tile = p;
           d.pool_in_rows = in_rows;

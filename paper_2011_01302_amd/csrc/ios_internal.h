@@ -270,10 +270,11 @@ __host__ __device__ inline int sep_lds_floats(int bm, int ck, int rows, int w, i
 // whose input rows (with halo) fit in kPoolLdsFloats of LDS.
 constexpr int kEltPerTile = 4 * kThreads;
 constexpr int kPoolLdsFloats = 8192;
-// Pools whose whole plane fits one tile take several planes per tile when a
-// plane has fewer outputs than a workgroup has threads, as long as the launch
-// keeps at least this many pool tiles.
+// Pools whose whole plane fits one tile take several planes per tile, up to
+// max(threads, kPoolTileOutputs) outputs, as long as the launch keeps at
+// least kPoolMinTiles pool tiles.
 constexpr int kPoolMinTiles = 256;
+constexpr int kPoolTileOutputs = 4096;
 
 // Division by a run-time constant d >= 1 as a multiply-high and a shift:
 // n / d == (umulhi(n, mul) + n) >> shr for 0 <= n < 2^31 (Granlund and

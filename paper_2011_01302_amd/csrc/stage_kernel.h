@@ -1536,7 +1536,7 @@ __device__ __forceinline__ void sep_gemm_dispatch(const Slots &sl, const DevOp &
 
 // ------------------------------------------------------------------ elementwise
 
-constexpr int kPoolBatch = 4;   // staging loads per thread in flight
+constexpr int kPoolBatch = 8;   // staging loads per thread in flight
 
 // planes_per_tile whole (image, channel) planes of a pool whose planes are
 // small: the planes' input rows are staged in LDS one plane after another
@@ -1766,25 +1766,12 @@ __device__ __forceinline__ void run_tile(const Slots &sl, const DevOp &op, const
   }
 }
 
-// One tile: find its op, wait for in-stage producers, compute, signal.
-// `tab` is the stage table in LDS.
+// Wait for in-stage producers, compute, signal (one tile of op `opi`, whose
+// descriptor is `op` in LDS and `o` for uniform use).
 template <int KV>
-__device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl, const int32_t *tab, int t,
-                                             float *lds) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  // op_start is non-decreasing with op_start[0] = 0: the tile's op is the
-  // last one starting at or before t.  Lane i holds op_start[i] and word
-  // i % 4 of the header; the values are taken out with v_readlane.
-  const int hv = tab[lane & 3], ov = tab[4 + lane];
-  const int n_ops = __builtin_amdgcn_readlane(hv, 0);
-  const int opi = __popcll(__ballot(lane < n_ops && t >= ov)) - 1;
-  const int s0 = __builtin_amdgcn_readlane(ov, opi);
-  int ti = t - s0;
-  const DevOp *ops = (const DevOp *)(tab + __builtin_amdgcn_readlane(hv, 2));
-  const DevOp &op = ops[opi];
-  if (ti >= U(op.n_tiles)) return;                   // padding between ops' ranges (see the stage table)
-
-  const DevOp o = op_scalars(op);
+__device__ __forceinline__ void tile_body(const StageArgs &a, const Slots &sl, const DevOp *ops, const DevOp &op,
+                                          const DevOp &o, int opi, int ti, float *lds) {
+  const int tid = threadIdx.x;
   const int n_deps = o.n_deps, signal = o.signal;
   if (n_deps) {
     // one thread polls the producers' counters with coherent loads (its own
@@ -1825,6 +1812,41 @@ __device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl
     __syncthreads();
     if (tid < kCtrCopies)
       __hip_atomic_fetch_add(&a.ctr[2 + opi + kCtrStride * tid], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+
+// One tile: find its op, then tile_body.
+// `tab` is the stage table in LDS, `gtab` the same table in global memory.
+template <int KV>
+__device__ __forceinline__ void process_tile(const StageArgs &a, const Slots &sl, const int32_t *tab,
+                                             const int4 *__restrict__ gtab, int t, float *lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  // op_start is non-decreasing with op_start[0] = 0: the tile's op is the
+  // last one starting at or before t.  Lane i holds op_start[i] and word
+  // i % 4 of the header; the values are taken out with v_readlane.
+  const int hv = tab[lane & 3], ov = tab[4 + lane];
+  const int n_ops = __builtin_amdgcn_readlane(hv, 0);
+  const int opi = __popcll(__ballot(lane < n_ops && t >= ov)) - 1;
+  const int s0 = __builtin_amdgcn_readlane(ov, opi);
+  int ti = t - s0;
+  const int devop_off = __builtin_amdgcn_readlane(hv, 2);
+  const DevOp *ops = (const DevOp *)(tab + devop_off);
+  const DevOp &op = ops[opi];
+  if (ti >= U(op.n_tiles)) return;                   // padding between ops' ranges (see the stage table)
+
+  // The descriptor's fields for uniform use.  The light and pipelined
+  // variants, which read few of them, move the LDS copy into scalar
+  // registers at once (op_scalars); the SEPCONV and full variants, which
+  // read many (a v_readlane per word and hundreds of spilled scalars), load
+  // each field where it is used with scalar loads from the table in global
+  // memory (read-only while the kernel runs, a uniform address).
+  if constexpr (KV == KV_LIGHT || KV == KV_PIPE) {
+    const DevOp o = op_scalars(op);
+    tile_body<KV>(a, sl, ops, op, o, opi, ti, lds);
+  } else {
+    const DevOp &o = ((const DevOp *)((const int32_t *)gtab + devop_off))[opi];
+    tile_body<KV>(a, sl, ops, op, o, opi, ti, lds);
   }
 }
 
@@ -1874,8 +1896,11 @@ __device__ __forceinline__ int xcd_tile(int b, int n, int lg) {
   return ((((local >> lg) << 3) + xcd) << lg) + (local & ((1 << lg) - 1));
 }
 
+// The one-tile-per-workgroup kernels of the light, pipelined and row-SEPCONV
+// variants keep two workgroups per CU (at most 128 VGPRs).
 template <int KV, bool PERSIST>
-__global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restrict__ table, int table_words,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(
+    (!PERSIST && (KV == KV_LIGHT || KV == KV_PIPE || KV == KV_SEPROW)) ? 4 : 1))) void ios_stage_kernel(const int4 *__restrict__ table, int table_words,
                                                              StageArgs a) {
   extern __shared__ int4 lds_base[];
   int32_t *meta = (int32_t *)lds_base;
@@ -1883,7 +1908,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   const Slots sl{(float *const *)meta};
   const int32_t *tab = meta + kSlotWords;
   if constexpr (!PERSIST) {
-    process_tile<KV>(a, sl, tab, xcd_tile(blockIdx.x, gridDim.x, U(tab[3])), lds);
+    process_tile<KV>(a, sl, tab, table, xcd_tile(blockIdx.x, gridDim.x, U(tab[3])), lds);
     return;
   }
   // round r takes tiles [r G, r G + G), permuted inside the round as above:
@@ -1891,7 +1916,7 @@ __global__ __launch_bounds__(kThreads) void ios_stage_kernel(const int4 *__restr
   // unfinished tile always has its producers done and its workgroup free
   const int n_tiles = U(tab[1]), n_ops = U(tab[0]), lg = U(tab[3]), G = gridDim.x, b = blockIdx.x;
   for (int base = 0; base + b < n_tiles; base += G) {
-    process_tile<KV>(a, sl, tab, base + xcd_tile(b, min(G, n_tiles - base), lg), lds);
+    process_tile<KV>(a, sl, tab, table, base + xcd_tile(b, min(G, n_tiles - base), lg), lds);
     __syncthreads();   // the next tile reuses LDS
   }
   if (threadIdx.x == 0) {

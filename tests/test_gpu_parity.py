@@ -669,20 +669,25 @@ def line_spec(batch):
     (two rounds of loads), chained; 16-wide planes of 15 rows (two output rows
     per tile, the last tile half past the image) and 33 channels; 8-wide
     planes of 96 channels (four rows per tile, the most channels); 32-wide
-    planes (four loads per thread).  Output channels 77, 50, 40, 20 and 64:
-    short and whole last blocks of 32 and 64 channels."""
+    planes (four loads per thread); l1 and l6 written into one concat (the
+    graph output), read back as slices by l2 (channel offset 0 of 117) and l7
+    (offset 77).  Output channels 77, 50, 40, 20, 64, 40 and 24: short and
+    whole last blocks of 32 and 64 channels."""
     sep = lambda n, ins, co: {"name": n, "kind": "sepconv", "in": ins, "cout": co, "kh": 3, "kw": 3, "sh": 1,
                               "sw": 1, "ph": 1, "pw": 1, "pre_relu": 1, "post_relu": 0}
     ops = [sep("l1", ["x"], 77),
            sep("l2", ["x", "y", "l1", "x", "y", "l1"], 50),
            sep("l3", ["z"], 40),
            sep("l4", ["u", "u"], 20),
-           sep("l5", ["v"], 64)]
+           sep("l5", ["v"], 64),
+           sep("l6", ["y"], 40),
+           {"name": "cat", "kind": "concat", "in": ["l1", "l6"]},
+           sep("l7", ["l6"], 24)]
     return {"name": "line", "batch": batch,
             "inputs": [{"name": "x", "c": 77, "h": 28, "w": 28}, {"name": "y", "c": 77, "h": 28, "w": 28},
                        {"name": "z", "c": 33, "h": 15, "w": 16}, {"name": "u", "c": 96, "h": 10, "w": 8},
                        {"name": "v", "c": 70, "h": 6, "w": 32}],
-            "ops": ops, "outputs": ["l2", "l3", "l4", "l5"]}
+            "ops": ops, "outputs": ["l2", "l3", "l4", "l5", "cat", "l7"]}
 
 
 @pytest.mark.parametrize("tile", ["9", "10"])
@@ -695,8 +700,8 @@ def test_parity_sepconv_line_tile(tile, monkeypatch):
     ten = W.make_tensors(spec, 6)
     refs = E.outputs(spec, ten)
     g = I.Graph(spec, ten)
-    # the two-block choice needs more than 32 output channels: not l4's 20
-    units = ("l1", "l2", "l3", "l4", "l5") if tile == "9" else ("l1", "l2", "l3", "l5")
+    # the two-block choice needs more than 32 output channels: not l4's 20 or l7's 24
+    units = ("l1", "l2", "l3", "l4", "l5", "l6", "l7") if tile == "9" else ("l1", "l2", "l3", "l5", "l6")
     assert all(I.ios_get_unit_tiling(g.handle, g.tid[n])[0] == int(tile) for n in units)
     for q in (sched(g, I.IOS_SCHED_SEQUENTIAL), sched(g, I.IOS_SCHED_GREEDY), block_stages(g)):
         check(run(g, q, spec, ten), refs, f"line/bs2/sep tile {tile}")

@@ -335,3 +335,31 @@ def test_cost_table_dump(tmp_path):
         else:
             assert r["merge_ns"] is None
     g.close()
+
+
+def test_line_sep_tile_refused_where_it_does_not_apply():
+    """The line SEPCONV tile choices (9: 32 output channels, 10: 64) take
+    3x3 windows that keep the plane size, rows of a multiple of 4 floats up
+    to 32 and at most 96 input channels; the two-block choice needs more than
+    32 output channels.  Every other case is refused before any device work."""
+    g = I.ios_graph_create(1)
+
+    def sep(c, h, w, cout, k):
+        x = I.ios_add_input(g, c, h, w)
+        wts = np.zeros(c * k * k + cout * c, np.float32)
+        return I.ios_add_op(g, desc(I.IOS_SEPCONV, cout, k, p=k // 2), [x], wts)
+    cases = {
+        "width 6": (sep(8, 6, 6, 40, 3), (9, 10)),
+        "width 40": (sep(8, 40, 40, 40, 3), (9, 10)),
+        "97 channels": (sep(97, 8, 8, 40, 3), (9, 10)),
+        "5x5 window": (sep(8, 8, 8, 40, 5), (9, 10)),
+        "32 outputs": (sep(8, 8, 8, 32, 3), (10,)),
+    }
+    for name, (u, tiles) in cases.items():
+        I.ios_mark_output(g, u)
+    I.ios_graph_finalize(g)
+    for name, (u, tiles) in cases.items():
+        for t in tiles:
+            expect("IOS_E_ARG", I.ios_set_unit_tiling, g, u, t, -1)
+        expect("IOS_E_ARG", I.ios_set_unit_tiling, g, u, 11, -1)             # past the last choice
+    I.ios_graph_destroy(g)

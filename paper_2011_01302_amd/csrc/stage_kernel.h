@@ -1212,7 +1212,49 @@ __device__ __forceinline__ void sep_line_tile(const Slots &sl, const DevOp &op, 
   lds_dma_wait();                                     // the biases' copy (wave 0, 1)
   __syncthreads();
 
-  // (2) depthwise: item e = (channel e / 8, pixels 4 (e % 8) .. + 3)
+  // (2) depthwise.  One output row per tile: item e = (channel e / 4,
+  //     pixels 8 (e % 4) .. + 7), reading columns x0 - 4 .. x0 + 11 of each
+  //     staged row (the second four pixels only where they are in the row)
+  if (R == 1) {
+    for (int e = tid; e < CE * 4; e += kThreads) {
+      const int ch = e >> 2, x0 = (e & 3) * 8;
+      const bool two = x0 + 4 < Wo;
+      floatx4 d0{0.f, 0.f, 0.f, 0.f}, d1{0.f, 0.f, 0.f, 0.f};
+      if (x0 < Wo) {
+        float w[12];
+#pragma unroll
+        for (int q4 = 0; q4 < 3; ++q4) {
+          const floatx4 t4 = *(const floatx4 *)(dww + ch * 12 + 4 * q4);
+          w[4 * q4] = t4.x; w[4 * q4 + 1] = t4.y; w[4 * q4 + 2] = t4.z; w[4 * q4 + 3] = t4.w;
+        }
+#pragma unroll
+        for (int u = 0; u < 3; ++u) {
+          const float *row = slab + (ch * ROWS + u) * PITCH + x0;
+          const floatx4 a0 = *(const floatx4 *)row, a1 = *(const floatx4 *)(row + 4),
+                        a2 = *(const floatx4 *)(row + 8);
+          const floatx4 a3 = two ? *(const floatx4 *)(row + 12) : floatx4{0.f, 0.f, 0.f, 0.f};
+          const float v[16] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w,
+                               a2.x, a2.y, a2.z, a2.w, a3.x, a3.y, a3.z, a3.w};
+#pragma unroll
+          for (int c = 0; c < 3; ++c) {
+            const float wt = w[u * 3 + c];
+            d0.x = fmaf(wt, v[3 + c], d0.x);
+            d0.y = fmaf(wt, v[4 + c], d0.y);
+            d0.z = fmaf(wt, v[5 + c], d0.z);
+            d0.w = fmaf(wt, v[6 + c], d0.w);
+            d1.x = fmaf(wt, v[7 + c], d1.x);
+            d1.y = fmaf(wt, v[8 + c], d1.y);
+            d1.z = fmaf(wt, v[9 + c], d1.z);
+            d1.w = fmaf(wt, v[10 + c], d1.w);
+          }
+        }
+        if (!two) d1 = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+      *(floatx4 *)(dwb + ch * 32 + x0) = d0;
+      *(floatx4 *)(dwb + ch * 32 + x0 + 4) = d1;
+    }
+  } else
+  // several rows per tile: item e = (channel e / 8, pixels 4 (e % 8) .. + 3)
   for (int e = tid; e < CE * 8; e += kThreads) {
     const int ch = e >> 3, p0 = (e & 7) * 4;
     const int ro = fdiv(p0, o.fd_wo), x0 = p0 - ro * Wo;
